@@ -1,0 +1,83 @@
+"""Pin the oracle's building blocks to library routines (scipy, numpy, torch).
+
+Softmax, quantile, population std, top-k, SiLU/SwiGLU and the bf16 widening
+each reduce to a textbook routine; a transposed operand, a wrong
+interpolation position or a biased variance fails here.
+"""
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import oracle as O
+from workload import bf16_bits
+
+
+def test_router_softmax_matches_scipy():
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((7, 24)).astype(np.float32)
+    w = rng.standard_normal((5, 24)).astype(np.float32)
+    for inv_t in (1.0, 2.0):
+        ref = scipy.special.softmax((x.astype(np.float64) @ w.astype(np.float64).T) * inv_t, axis=1)
+        np.testing.assert_allclose(O.router_probs(x, w, inv_t), ref, rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("E", [4, 8, 60, 64])
+def test_quantile_matches_numpy_linear(E):
+    rng = np.random.default_rng(E)
+    for _ in range(20):
+        v = rng.dirichlet(np.ones(E))
+        for q in (0.1, 0.9, 0.0, 1.0, 0.5):
+            assert O.quantile(v, q) == pytest.approx(np.quantile(v, q, method="linear"), abs=1e-15)
+
+
+def test_grounding_matches_numpy_population_std():
+    rng = np.random.default_rng(1)
+    for E in (4, 8, 64):
+        g = rng.dirichlet(np.ones(E))
+        mu, sigma, tau = O.grounding(g, 0.5, 1.0)
+        assert mu == pytest.approx(np.mean(g), abs=1e-15)
+        assert sigma == pytest.approx(np.std(g, ddof=0), rel=1e-12)
+        assert tau == pytest.approx(max(0.5 * np.mean(g), np.mean(g) - np.std(g)), rel=1e-12)
+
+
+def test_topk_matches_torch_topk():
+    rng = np.random.default_rng(2)
+    for E, K in ((8, 2), (64, 8), (60, 4)):
+        p = rng.dirichlet(np.ones(E), size=50)
+        ref = torch.topk(torch.from_numpy(p), K, dim=1).indices.numpy()
+        for t in range(50):
+            assert O.select_topk(p[t], K) == sorted(ref[t].tolist())
+
+
+def test_swiglu_matches_torch_silu_reference():
+    # non-square everywhere so that a transposed operand cannot pass
+    rng = np.random.default_rng(3)
+    n, d, F = 5, 12, 20
+    x = rng.standard_normal((n, d))
+    w1 = rng.standard_normal((F, d)); w3 = rng.standard_normal((F, d)); w2 = rng.standard_normal((d, F))
+    X = torch.from_numpy(x)
+    ref = torch.nn.functional.linear(
+        torch.nn.functional.silu(torch.nn.functional.linear(X, torch.from_numpy(w1)))
+        * torch.nn.functional.linear(X, torch.from_numpy(w3)),
+        torch.from_numpy(w2))
+    np.testing.assert_allclose(O.swiglu(x, w1, w3, w2), ref.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_widen_bf16_matches_torch():
+    rng = np.random.default_rng(4)
+    a = (rng.standard_normal(1000) * 10).astype(np.float32)
+    bits = bf16_bits(a)
+    ref = torch.from_numpy(a).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.widen(bits), ref)
+
+
+def test_router_softmax_rows_far_apart():
+    # each row is shifted by its own maximum: a row whose logits are all far
+    # below another row's must still come out as a proper distribution
+    x = np.array([[1.0, 0.0], [0.0, 1.0]], np.float32)
+    w = np.array([[2000.0, 0.0], [1999.0, 0.0], [0.0, 1.0]], np.float32)
+    p = O.router_probs(x, w)
+    ref = scipy.special.softmax(x.astype(np.float64) @ w.astype(np.float64).T, axis=1)
+    np.testing.assert_allclose(p, ref, rtol=1e-12, atol=1e-300)
+    assert np.isfinite(p).all()
