@@ -1,0 +1,186 @@
+/*
+ * eat.h - C ABI of the EAT (Expert Account Tracker) MoE-layer forward for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The library computes one Mixture-of-Experts layer forward with the
+ * history-aware dynamic routing of "EAT: Expert Account Tracker for
+ * Efficient MoE Inference" (Sec. 3), with fixed Top-K and Top-P routing as
+ * switchable baselines:
+ *
+ *   router scores + softmax ............................ Sec. 3.1
+ *   account statistics N, P_total, C_s; history score
+ *     S_h (Eq. 1) and final importance I (Eq. 2) ........ Sec. 3.2
+ *   adaptive threshold: grounding (Eq. 3-5), perplexity
+ *     adjustment, boundedness, smoothing ................ Sec. 3.3
+ *   activation set (Eq. 6), mask + renormalisation
+ *     (Eq. 7-8), weighted fusion of expert outputs ...... Sec. 3.4
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Ownership: the caller owns every device buffer, including the account
+ *    state and the workspace.  The library never allocates device memory.
+ *  - Asynchrony: every call that takes a stream only enqueues kernels on it
+ *    and returns; inputs must stay alive and unmodified until the stream
+ *    has passed the enqueued work.  No call synchronises the device.
+ *  - Validation: all arguments are checked on the host before anything is
+ *    enqueued.  On any error status nothing is launched and no output,
+ *    workspace byte or account value is touched.
+ *  - Errors: no C++ exception crosses this interface.  A HIP launch failure
+ *    is reported as EAT_ERR_HIP (the enqueued work up to the failure may
+ *    have run).
+ *  - Limits: 1 <= E <= 64 (one bit per expert in a 64-bit mask);
+ *    1 <= top_k <= E; d_model, d_ffn and d_shared are multiples of 64;
+ *    activations and expert weights are both fp32 or both bf16.
+ *  - Layouts (all row-major, densely packed, 16-byte aligned):
+ *      x        [T][d_model]            act_dtype
+ *      w_router [E][d_model]            fp32
+ *      w1, w3   [E][d_ffn][d_model]     expert_dtype  (gate / up rows)
+ *      w2       [E][d_model][d_ffn]     expert_dtype  (down rows)
+ *      ws1, ws3 [d_shared][d_model], ws2 [d_model][d_shared]
+ *      y        [T][d_model]            act_dtype
+ *      masks    [T] uint64, bit i set <=> expert i selected
+ *      gates    [T][E] fp32, renormalised gate (0 for unselected experts)
+ *  - Thread safety: a handle is immutable after eat_create; calls that use
+ *    different workspaces and account buffers may run concurrently.
+ *    Calls sharing an account buffer must be ordered on one stream.
+ */
+#ifndef EAT_H
+#define EAT_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    EAT_OK = 0,
+    EAT_ERR_INVALID_ARG = 1,   /* null / misaligned pointer, bad size or value */
+    EAT_ERR_UNSUPPORTED = 2,   /* a shape or dtype outside the limits above   */
+    EAT_ERR_WORKSPACE = 3,     /* workspace missing or smaller than required  */
+    EAT_ERR_HIP = 4,           /* a HIP runtime call or kernel launch failed  */
+    EAT_ERR_INTERNAL = 5
+} eat_status_t;
+
+typedef enum {
+    EAT_MODE_EAT = 0,          /* history-aware adaptive threshold (Sec. 3.2-3.4) */
+    EAT_MODE_TOPK = 1,         /* vanilla Top-K (Sec. 3.1)                        */
+    EAT_MODE_TOPP = 2          /* Top-P nucleus baseline (Sec. 4.1)               */
+} eat_mode_t;
+
+typedef enum { EAT_F32 = 0, EAT_BF16 = 1 } eat_dtype_t;
+
+/* Layer shape and routing hyper-parameters.  eat_params_default() fills the
+ * values of the paper's hyper-parameter table (Sec. 4.1) and the constants
+ * of Sec. 3.3 / Eq. 7; the caller then sets the shape fields. */
+typedef struct {
+    int32_t mode;            /* eat_mode_t                                          */
+    int32_t E;               /* routed experts, 1..64                               */
+    int32_t d_model;         /* hidden width d                                      */
+    int32_t d_ffn;           /* expert FFN width F                                  */
+    int32_t top_k;           /* K: EAT's cap (Eq. 6) and Top-K's k; default 2       */
+    float top_p;             /* Top-P threshold in (0, 1]; default 0.6              */
+    int32_t top_p_cap;       /* 0 = uncapped nucleus, else max experts per token    */
+    float alpha;             /* EMA factor of C_s (Sec. 3.2); 0.95                  */
+    float w1, w2, w3;        /* Eq. 1 weights; 0.3, 0.3, 0.4                        */
+    float beta;              /* Eq. 2 balance; 0.6                                  */
+    float alpha1, alpha2;    /* Eq. 5 scaling; 0.5, 1.0                             */
+    float kappa1, kappa2;    /* smoothing weights (Sec. 3.3); 0.7, 0.3              */
+    float ppl_up, ppl_down;  /* tau factor when perplexity rose / otherwise; 1.2, 0.9 */
+    float q_lo, q_hi;        /* bounds: these points of each token's routing
+                                weights (linear interpolation, h = q (E-1)); 0.1, 0.9 */
+    float eps;               /* Eq. 7 epsilon; 1e-8                                 */
+    float inv_temperature;   /* router logits are multiplied by this; 1.0           */
+    int32_t cs_mode;         /* 0: C_s enters Eq. 1 as is; 1: as C_s,i / sum C_s    */
+    int32_t act_dtype;       /* eat_dtype_t of x and y                              */
+    int32_t expert_dtype;    /* eat_dtype_t of w1/w3/w2 (and ws1/ws3/ws2)           */
+    int32_t d_shared;        /* width of an always-on shared SwiGLU expert, 0 = none */
+} eat_params_t;
+
+/* Per-layer account state (Sec. 3.2), device memory, length E each, owned by
+ * the caller: activation counts N (int64), total gating probability P_total
+ * (fp32) and the smoothed contribution C_s (fp32).  The state persists
+ * across calls until eat_reset_accounts. */
+typedef struct {
+    int64_t* n;
+    float* p_total;
+    float* c_s;
+} eat_accounts_t;
+
+typedef struct eat_ctx* eat_handle_t;
+
+/* Fill *out with the default hyper-parameters (mode EAT, E = 8,
+ * d_model = 4096, d_ffn = 14336, bf16).  Returns EAT_ERR_INVALID_ARG for
+ * a null pointer. */
+eat_status_t eat_params_default(eat_params_t* out);
+
+/* Validate params and build a handle for up to max_tokens tokens per call.
+ * Host-only: no HIP call, no device memory.  Errors: INVALID_ARG for a null
+ * pointer, a non-finite or out-of-range hyper-parameter or max_tokens < 1;
+ * UNSUPPORTED for a shape or dtype outside the limits in the file header. */
+eat_status_t eat_create(const eat_params_t* params, int32_t max_tokens, eat_handle_t* out);
+
+/* Release a handle (host memory only).  Null is accepted. */
+eat_status_t eat_destroy(eat_handle_t h);
+
+/* Bytes of device workspace a call with T tokens needs (0 <= T <=
+ * max_tokens).  The workspace holds router probabilities, gates, masks,
+ * the token permutation and the expert intermediates; its size is linear
+ * in T and sized for the mode's largest possible number of
+ * (token, expert) assignments (T*K for Top-K, T*E for EAT and uncapped
+ * Top-P, since Eq. 6 keeps exact ties and the nucleus is unbounded). */
+eat_status_t eat_workspace_size(eat_handle_t h, int32_t T, size_t* bytes);
+
+/* Zero the account state N, P_total, C_s (Sec. 3.2: the statistics start
+ * empty) with a kernel on `stream` (no memset node, so it can be captured
+ * in a graph). */
+eat_status_t eat_reset_accounts(eat_handle_t h, eat_accounts_t acc, hipStream_t stream);
+
+/* Routing only (Sec. 3.1-3.4, no experts, accounts read but not updated).
+ *   x          [T][d_model] act_dtype, device
+ *   w_router   [E][d_model] fp32, device
+ *   acc        account snapshot every token is judged against (EAT mode;
+ *              ignored by Top-K / Top-P, may then hold null pointers)
+ *   ppl_trend  [T] int8 or NULL: > 0 means the perplexity rose for that
+ *              token's sequence (tau x ppl_up), anything else tau x ppl_down
+ *   mask_out   [T] uint64, k_out [T] int32, gate_out [T][E] fp32: required
+ *   prob_out   [T][E] fp32 router probabilities, or NULL
+ *   ws         device workspace of at least eat_workspace_size(h, T) bytes
+ */
+eat_status_t eat_route(eat_handle_t h, const void* x, int32_t T, const float* w_router,
+                       eat_accounts_t acc, const int8_t* ppl_trend,
+                       uint64_t* mask_out, int32_t* k_out, float* gate_out, float* prob_out,
+                       void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Whole layer forward over T tokens:
+ *   y_t = sum over selected e of g_norm,t,e * SwiGLU_e(x_t)  (+ SwiGLU_shared(x_t))
+ * with SwiGLU_e(x) = W2_e (silu(W1_e x) * (W3_e x)), no biases.
+ * Every token routes against the accounts as they are when the call
+ * starts; in EAT mode the accounts are then updated in place once for the
+ * whole call (N += tokens routed to each expert, P_total += their router
+ * probabilities, C_s <- (1 - alpha) C_s + alpha * mean ||o||_2 of the
+ * expert's un-gated outputs); experts no token chose keep their values.
+ * Top-K / Top-P neither read nor write the accounts.
+ *   w1, w3, w2     routed experts (layouts in the file header)
+ *   ws1, ws3, ws2  shared expert when d_shared > 0, else all NULL
+ *   y              [T][d_model] act_dtype output
+ *   mask_out       [T] uint64 or NULL
+ *   expert_load_out [E] int32 tokens per expert, or NULL
+ */
+eat_status_t eat_moe_forward(eat_handle_t h, const void* x, int32_t T, const float* w_router,
+                             const void* w1, const void* w3, const void* w2,
+                             const void* ws1, const void* ws3, const void* ws2,
+                             eat_accounts_t acc, const int8_t* ppl_trend, void* y,
+                             uint64_t* mask_out, int32_t* expert_load_out,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Static description of a status code (never NULL). */
+const char* eat_status_string(eat_status_t s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EAT_H */

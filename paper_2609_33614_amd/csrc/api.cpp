@@ -1,0 +1,260 @@
+// C ABI of the EAT MoE-layer library: argument validation, workspace
+// carve-up and the launch sequence.  Every check runs on the host before
+// any HIP call; no exception leaves this file.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+
+#include "eat_internal.h"
+
+namespace {
+
+constexpr int32_t kMaxTokens = 1 << 24;
+
+bool finite(float v) { return isfinite(v) != 0; }
+bool in01(float v) { return finite(v) && v >= 0.f && v <= 1.f; }
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+eat_status_t check_params(const eat_params_t& p) {
+    if (p.mode < EAT_MODE_EAT || p.mode > EAT_MODE_TOPP) return EAT_ERR_INVALID_ARG;
+    if (p.E < 1 || p.d_model < 1 || p.d_ffn < 1 || p.d_shared < 0) return EAT_ERR_INVALID_ARG;
+    if (p.top_k < 1 || p.top_k > p.E) return EAT_ERR_INVALID_ARG;
+    if (p.mode == EAT_MODE_TOPP && !(finite(p.top_p) && p.top_p > 0.f && p.top_p <= 1.f))
+        return EAT_ERR_INVALID_ARG;
+    if (p.top_p_cap < 0 || p.top_p_cap > p.E) return EAT_ERR_INVALID_ARG;
+    if (!in01(p.alpha) || !in01(p.beta)) return EAT_ERR_INVALID_ARG;
+    const float fin[] = {p.w1, p.w2, p.w3, p.alpha1, p.alpha2, p.kappa1, p.kappa2,
+                         p.ppl_up, p.ppl_down, p.eps, p.inv_temperature};
+    for (float v : fin)
+        if (!finite(v)) return EAT_ERR_INVALID_ARG;
+    if (!in01(p.q_lo) || !in01(p.q_hi) || p.q_lo > p.q_hi) return EAT_ERR_INVALID_ARG;
+    if (p.eps < 0.f || p.inv_temperature <= 0.f) return EAT_ERR_INVALID_ARG;
+    if (p.cs_mode != 0 && p.cs_mode != 1) return EAT_ERR_INVALID_ARG;
+    if ((p.act_dtype != EAT_F32 && p.act_dtype != EAT_BF16) ||
+        (p.expert_dtype != EAT_F32 && p.expert_dtype != EAT_BF16))
+        return EAT_ERR_INVALID_ARG;
+    // supported shapes and dtype pairs
+    if (p.E > 64) return EAT_ERR_UNSUPPORTED;
+    if (p.d_model % 64 || p.d_ffn % 64 || p.d_shared % 64) return EAT_ERR_UNSUPPORTED;
+    if (p.act_dtype != p.expert_dtype) return EAT_ERR_UNSUPPORTED;
+    return EAT_OK;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+}  // namespace
+
+namespace eat {
+
+Workspace plan_workspace(const eat_ctx& c, int32_t T) {
+    const eat_params_t& p = c.p;
+    Workspace w{};
+    const size_t t = static_cast<size_t>(T), E = static_cast<size_t>(p.E);
+    const size_t es = p.expert_dtype == EAT_BF16 ? 2 : 4;
+    w.rows = static_cast<int64_t>(T) * c.kmax;
+    w.splits = down_splits(p, T);
+    const size_t rows = static_cast<size_t>(w.rows);
+    size_t off = 0;
+    auto take = [&](size_t bytes) { const size_t at = off; off += align256(bytes); return at; };
+    w.prob = take(t * E * 4);
+    w.gate = take(t * E * 4);
+    w.mask = take(t * 8);
+    w.k = take(t * 4);
+    w.offsets = take((E + 1) * 4);
+    w.tok_idx = take(rows * 4);
+    w.inv = take(t * E * 4);
+    w.row_expert = take(rows * 4);
+    w.h = take(rows * p.d_ffn * es);
+    w.yp = take(static_cast<size_t>(w.splits) * rows * p.d_model * 4);
+    w.nrm = take(rows * 4);
+    w.hs = take(p.d_shared ? t * p.d_shared * es : 0);
+    w.ys = take(p.d_shared ? t * p.d_model * 4 : 0);
+    w.total = off;
+    return w;
+}
+
+}  // namespace eat
+
+extern "C" {
+
+eat_status_t eat_params_default(eat_params_t* out) {
+    if (!out) return EAT_ERR_INVALID_ARG;
+    memset(out, 0, sizeof(*out));
+    out->mode = EAT_MODE_EAT;
+    out->E = 8;
+    out->d_model = 4096;
+    out->d_ffn = 14336;
+    out->top_k = 2;
+    out->top_p = 0.6f;
+    out->top_p_cap = 0;
+    out->alpha = 0.95f;
+    out->w1 = 0.3f; out->w2 = 0.3f; out->w3 = 0.4f;
+    out->beta = 0.6f;
+    out->alpha1 = 0.5f; out->alpha2 = 1.0f;
+    out->kappa1 = 0.7f; out->kappa2 = 0.3f;
+    out->ppl_up = 1.2f; out->ppl_down = 0.9f;
+    out->q_lo = 0.1f; out->q_hi = 0.9f;
+    out->eps = 1e-8f;
+    out->inv_temperature = 1.0f;
+    out->cs_mode = 0;
+    out->act_dtype = EAT_BF16;
+    out->expert_dtype = EAT_BF16;
+    out->d_shared = 0;
+    return EAT_OK;
+}
+
+eat_status_t eat_create(const eat_params_t* params, int32_t max_tokens, eat_handle_t* out) {
+    if (!params || !out) return EAT_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (max_tokens < 1 || max_tokens > kMaxTokens) return EAT_ERR_INVALID_ARG;
+    const eat_status_t st = check_params(*params);
+    if (st != EAT_OK) return st;
+    eat_ctx* c = new (std::nothrow) eat_ctx;
+    if (!c) return EAT_ERR_INTERNAL;
+    c->p = *params;
+    c->max_tokens = max_tokens;
+    if (params->mode == EAT_MODE_TOPK) c->kmax = params->top_k;
+    else if (params->mode == EAT_MODE_TOPP && params->top_p_cap > 0) c->kmax = params->top_p_cap;
+    else c->kmax = params->E;
+    *out = c;
+    return EAT_OK;
+}
+
+eat_status_t eat_destroy(eat_handle_t h) {
+    delete h;
+    return EAT_OK;
+}
+
+eat_status_t eat_workspace_size(eat_handle_t h, int32_t T, size_t* bytes) {
+    if (!h || !bytes || T < 0 || T > h->max_tokens) return EAT_ERR_INVALID_ARG;
+    *bytes = eat::plan_workspace(*h, T).total;
+    return EAT_OK;
+}
+
+eat_status_t eat_reset_accounts(eat_handle_t h, eat_accounts_t acc, hipStream_t stream) {
+    if (!h || !acc.n || !acc.p_total || !acc.c_s) return EAT_ERR_INVALID_ARG;
+    if (!aligned(acc.n, 8) || !aligned(acc.p_total, 4) || !aligned(acc.c_s, 4)) return EAT_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    return eat::launch_reset_accounts(h->p, acc, stream) == hipSuccess ? EAT_OK : EAT_ERR_HIP;
+}
+
+static eat_status_t check_accounts(const eat_ctx& c, const eat_accounts_t& acc) {
+    if (c.p.mode != EAT_MODE_EAT) return EAT_OK;
+    if (!acc.n || !acc.p_total || !acc.c_s) return EAT_ERR_INVALID_ARG;
+    if (!aligned(acc.n, 8) || !aligned(acc.p_total, 4) || !aligned(acc.c_s, 4)) return EAT_ERR_INVALID_ARG;
+    return EAT_OK;
+}
+
+eat_status_t eat_route(eat_handle_t h, const void* x, int32_t T, const float* w_router,
+                       eat_accounts_t acc, const int8_t* ppl_trend, uint64_t* mask_out,
+                       int32_t* k_out, float* gate_out, float* prob_out, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+    (void)ws;
+    (void)ws_bytes;  // routing alone needs no workspace
+    if (!h || T < 0 || T > h->max_tokens) return EAT_ERR_INVALID_ARG;
+    if (!x || !w_router || !mask_out || !k_out || !gate_out) return EAT_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(w_router, 16) || !aligned(mask_out, 8) || !aligned(k_out, 4) ||
+        !aligned(gate_out, 4) || (prob_out && !aligned(prob_out, 4)))
+        return EAT_ERR_INVALID_ARG;
+    const eat_status_t st = check_accounts(*h, acc);
+    if (st != EAT_OK) return st;
+    if (T == 0) return EAT_OK;
+    (void)hipGetLastError();
+    const hipError_t e = eat::launch_route(h->p, x, T, w_router, acc, ppl_trend, mask_out, k_out, gate_out,
+                                           prob_out, stream);
+    return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;
+}
+
+eat_status_t eat_moe_forward(eat_handle_t h, const void* x, int32_t T, const float* w_router,
+                             const void* w1, const void* w3, const void* w2, const void* ws1,
+                             const void* ws3, const void* ws2, eat_accounts_t acc,
+                             const int8_t* ppl_trend, void* y, uint64_t* mask_out,
+                             int32_t* expert_load_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (!h || T < 0 || T > h->max_tokens) return EAT_ERR_INVALID_ARG;
+    const eat_params_t& p = h->p;
+    if (!x || !w_router || !w1 || !w3 || !w2 || !y) return EAT_ERR_INVALID_ARG;
+    const void* a16[] = {x, w_router, w1, w3, w2, y};
+    for (const void* q : a16)
+        if (!aligned(q, 16)) return EAT_ERR_INVALID_ARG;
+    if (p.d_shared > 0) {
+        if (!ws1 || !ws3 || !ws2) return EAT_ERR_INVALID_ARG;
+        if (!aligned(ws1, 16) || !aligned(ws3, 16) || !aligned(ws2, 16)) return EAT_ERR_INVALID_ARG;
+    } else if (ws1 || ws3 || ws2) {
+        return EAT_ERR_INVALID_ARG;
+    }
+    if ((mask_out && !aligned(mask_out, 8)) || (expert_load_out && !aligned(expert_load_out, 4)))
+        return EAT_ERR_INVALID_ARG;
+    const eat_status_t st = check_accounts(*h, acc);
+    if (st != EAT_OK) return st;
+    const eat::Workspace w = eat::plan_workspace(*h, T);
+    if (T > 0 && (!ws || ws_bytes < w.total)) return EAT_ERR_WORKSPACE;
+    if (ws && !aligned(ws, 256)) return EAT_ERR_INVALID_ARG;
+    if (T == 0) return EAT_OK;
+
+    char* base = static_cast<char*>(ws);
+    eat::Buffers b;
+    b.prob = reinterpret_cast<float*>(base + w.prob);
+    b.gate = reinterpret_cast<float*>(base + w.gate);
+    b.mask = mask_out ? mask_out : reinterpret_cast<uint64_t*>(base + w.mask);
+    b.k = reinterpret_cast<int32_t*>(base + w.k);
+    b.offsets = reinterpret_cast<int32_t*>(base + w.offsets);
+    b.tok_idx = reinterpret_cast<int32_t*>(base + w.tok_idx);
+    b.inv = reinterpret_cast<int32_t*>(base + w.inv);
+    b.row_expert = reinterpret_cast<int32_t*>(base + w.row_expert);
+    b.h = base + w.h;
+    b.yp = reinterpret_cast<float*>(base + w.yp);
+    b.nrm = reinterpret_cast<float*>(base + w.nrm);
+    b.hs = base + w.hs;
+    b.ys = reinterpret_cast<float*>(base + w.ys);
+
+    (void)hipGetLastError();
+    hipError_t e = eat::launch_route(p, x, T, w_router, acc, ppl_trend, b.mask, b.k, b.gate, b.prob, stream);
+    if (e == hipSuccess)
+        e = eat::launch_permute(p, T, b.mask, b.offsets, b.tok_idx, b.inv, b.row_expert, expert_load_out,
+                                stream);
+    if (e == hipSuccess) {
+        if (p.expert_dtype == EAT_BF16)
+            e = eat::launch_experts_bf16(p, T, w.rows, static_cast<const uint16_t*>(x),
+                                         static_cast<const uint16_t*>(w1), static_cast<const uint16_t*>(w3),
+                                         static_cast<const uint16_t*>(w2), b.offsets, b.tok_idx,
+                                         static_cast<uint16_t*>(b.h), b.yp, stream);
+        else
+            e = eat::launch_experts_f32(p, T, w.rows, static_cast<const float*>(x),
+                                        static_cast<const float*>(w1), static_cast<const float*>(w3),
+                                        static_cast<const float*>(w2), b.offsets, b.tok_idx, b.row_expert,
+                                        static_cast<float*>(b.h), b.yp, stream);
+    }
+    const bool shared = p.d_shared > 0;
+    if (e == hipSuccess && shared) {
+        if (p.expert_dtype == EAT_BF16)
+            e = eat::launch_shared_bf16(p, T, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(ws1),
+                                        static_cast<const uint16_t*>(ws3), static_cast<const uint16_t*>(ws2),
+                                        static_cast<uint16_t*>(b.hs), b.ys, stream);
+        else
+            e = eat::launch_shared_f32(p, T, static_cast<const float*>(x), static_cast<const float*>(ws1),
+                                       static_cast<const float*>(ws3), static_cast<const float*>(ws2),
+                                       static_cast<float*>(b.hs), b.ys, stream);
+    }
+    if (e == hipSuccess)
+        e = eat::launch_combine(p, T, b.mask, b.gate, b.inv, b.yp, shared ? b.ys : nullptr, y, b.nrm, w.splits,
+                                w.rows * p.d_model, stream);
+    if (e == hipSuccess && p.mode == EAT_MODE_EAT)
+        e = eat::launch_update_accounts(p, b.offsets, b.tok_idx, b.prob, b.nrm, acc, stream);
+    return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;
+}
+
+const char* eat_status_string(eat_status_t s) {
+    switch (s) {
+        case EAT_OK: return "ok";
+        case EAT_ERR_INVALID_ARG: return "invalid argument";
+        case EAT_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+        case EAT_ERR_WORKSPACE: return "workspace missing or too small";
+        case EAT_ERR_HIP: return "HIP runtime error";
+        case EAT_ERR_INTERNAL: return "internal error";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,92 @@
+// Host-side internals of the EAT library: the validated handle, the
+// workspace carve-up and the kernel launchers each .hip file provides.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/eat.h"
+
+struct eat_ctx {
+    eat_params_t p;
+    int32_t max_tokens;
+    int32_t kmax;            // largest possible experts per token in this mode
+};
+
+namespace eat {
+
+// Offsets (bytes) of the workspace regions for T tokens.  Every region
+// starts on a 256-byte boundary.
+struct Workspace {
+    size_t prob, gate, mask, k, offsets, tok_idx, inv, row_expert, h, yp, nrm, hs, ys;
+    size_t total;
+    int64_t rows;            // capacity in (token, expert) rows = T * kmax
+    int splits;              // down-projection slices held in yp
+};
+Workspace plan_workspace(const eat_ctx& c, int32_t T);
+
+// Pointers into a workspace for one call.
+struct Buffers {
+    float* prob;             // [T][E] router probabilities
+    float* gate;             // [T][E] renormalised gates
+    uint64_t* mask;          // [T]
+    int32_t* k;              // [T]
+    int32_t* offsets;        // [E+1] expert-major row offsets
+    int32_t* tok_idx;        // [rows] token of each expert-major row
+    int32_t* inv;            // [T][E] row of (t, e), valid where selected
+    int32_t* row_expert;     // [rows] expert of each row
+    void* h;                 // [rows][F] SwiGLU hidden (bf16 or fp32)
+    float* yp;               // [splits][rows][d] un-gated expert outputs (partials)
+    float* nrm;              // [rows] ||yp row||_2
+    void* hs;                // [T][F_sh] shared-expert hidden
+    float* ys;               // [T][d] shared-expert output
+};
+
+// ---- launchers (return hipGetLastError() after enqueueing) -------------
+
+hipError_t launch_reset_accounts(const eat_params_t& p, eat_accounts_t acc, hipStream_t s);
+
+hipError_t launch_route(const eat_params_t& p, const void* x, int32_t T, const float* w_router,
+                        eat_accounts_t acc, const int8_t* trend, uint64_t* mask, int32_t* k,
+                        float* gate, float* prob, hipStream_t s);
+
+hipError_t launch_permute(const eat_params_t& p, int32_t T, const uint64_t* mask,
+                          int32_t* offsets, int32_t* tok_idx, int32_t* inv, int32_t* row_expert,
+                          int32_t* expert_load, hipStream_t s);
+
+// Routed experts, fp32 weights and activations (small layers).
+hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap, const float* x,
+                              const float* w1, const float* w3, const float* w2,
+                              const int32_t* offsets, const int32_t* tok_idx,
+                              const int32_t* row_expert, float* h, float* yp, hipStream_t s);
+
+// Routed experts, bf16 weights and activations: MFMA kernels.
+hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_cap,
+                               const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
+                               const uint16_t* w2, const int32_t* offsets, const int32_t* tok_idx,
+                               uint16_t* h, float* yp, hipStream_t s);
+
+// Always-on shared expert over all T tokens.
+hipError_t launch_shared_f32(const eat_params_t& p, int32_t T, const float* x, const float* ws1,
+                             const float* ws3, const float* ws2, float* hs, float* ys,
+                             hipStream_t s);
+hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* x,
+                              const uint16_t* ws1, const uint16_t* ws3, const uint16_t* ws2,
+                              uint16_t* hs, float* ys, hipStream_t s);
+
+// yp holds `splits` partial slices of the down projection, `split_stride`
+// floats apart; they are added in slice order.
+hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask,
+                          const float* gate, const int32_t* inv, const float* yp,
+                          const float* ys, void* y, float* nrm, int splits,
+                          int64_t split_stride, hipStream_t s);
+
+// Number of reduction-dimension slices the bf16 down projection uses for T
+// tokens (1 for fp32 layers).
+int down_splits(const eat_params_t& p, int32_t T);
+
+hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets,
+                                  const int32_t* tok_idx, const float* prob, const float* nrm,
+                                  eat_accounts_t acc, hipStream_t s);
+
+}  // namespace eat

@@ -1,0 +1,318 @@
+// Expert FFN kernels (gfx950): SwiGLU experts over the expert-major rows.
+//
+//   up/gate:  H[r][f] = silu(x_t . W1_e[f]) * (x_t . W3_e[f])   t = tok_idx[r]
+//   down:     Yp[r][j] = H[r] . W2_e[j]
+//
+// bf16 path ("stream" kernels): each wave owns 16 consecutive weight rows
+// (the 16-row A operand of v_mfma_f32_16x16x32_bf16) and streams them over
+// the whole reduction dimension once, applying them to up to 16*NSUB
+// tokens of the same expert (the B operand, zero-padded).  Weight bytes are
+// read from HBM exactly once per token tile, which is what bounds decode.
+// The down projection may split its reduction dimension over gridDim.z;
+// the partial tiles are added, in split order, by the combine kernel.
+//
+// fp32 path: plain dot products, one thread per output element, for layers
+// whose weights are fp32 (small correctness-sized layers).
+#include <algorithm>
+
+#include "eat_device.h"
+#include "eat_internal.h"
+
+namespace eat {
+namespace {
+
+// ---------------------------------------------------------------- fp32 --
+
+struct F32Args {
+    const float* x;            // [*, d] token activations
+    const float* w1;           // [E][F][d]
+    const float* w3;
+    const float* w2;           // [E][d][F]
+    const int32_t* tok_idx;    // row -> token, or null (row == token)
+    const int32_t* row_expert; // row -> expert, or null (expert 0)
+    const int32_t* rows_dev;   // device row count (offsets[E]), or null
+    int rows_host;             // row count when rows_dev is null
+    int d, F;
+    float* h;                  // [rows][F]
+    float* yp;                 // [rows][d]
+};
+
+__global__ __launch_bounds__(256) void ffn_up_f32(F32Args a) {
+    const int64_t rows = a.rows_dev ? *a.rows_dev : a.rows_host;
+    const int64_t total = rows * a.F;
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < total;
+         i += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t r = i / a.F;
+        const int f = static_cast<int>(i % a.F);
+        const int t = a.tok_idx ? a.tok_idx[r] : static_cast<int>(r);
+        const int e = a.row_expert ? a.row_expert[r] : 0;
+        const float* xr = a.x + static_cast<size_t>(t) * a.d;
+        const float* g = a.w1 + (static_cast<size_t>(e) * a.F + f) * a.d;
+        const float* u = a.w3 + (static_cast<size_t>(e) * a.F + f) * a.d;
+        float sg = 0.f, su = 0.f;
+        for (int k = 0; k < a.d; ++k) {
+            sg = fmaf(xr[k], g[k], sg);
+            su = fmaf(xr[k], u[k], su);
+        }
+        a.h[r * a.F + f] = silu(sg) * su;
+    }
+}
+
+__global__ __launch_bounds__(256) void ffn_down_f32(F32Args a) {
+    const int64_t rows = a.rows_dev ? *a.rows_dev : a.rows_host;
+    const int64_t total = rows * a.d;
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < total;
+         i += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t r = i / a.d;
+        const int j = static_cast<int>(i % a.d);
+        const int e = a.row_expert ? a.row_expert[r] : 0;
+        const float* hr = a.h + r * a.F;
+        const float* w = a.w2 + (static_cast<size_t>(e) * a.d + j) * a.F;
+        float s = 0.f;
+        for (int f = 0; f < a.F; ++f) s = fmaf(hr[f], w[f], s);
+        a.yp[r * a.d + j] = s;
+    }
+}
+
+hipError_t launch_f32_pair(F32Args a, int64_t rows_cap, hipStream_t s) {
+    const int64_t up = rows_cap * a.F, dn = rows_cap * a.d;
+    const int gu = static_cast<int>(std::min<int64_t>((up + 255) / 256, 8192));
+    const int gd = static_cast<int>(std::min<int64_t>((dn + 255) / 256, 8192));
+    if (gu > 0) ffn_up_f32<<<gu, 256, 0, s>>>(a);
+    if (gd > 0) ffn_down_f32<<<gd, 256, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------- bf16 streaming --
+
+struct StreamArgs {
+    const uint16_t* wa;        // [groups][M][K]  (W1 for up/gate, W2 for down)
+    const uint16_t* wb;        // [groups][M][K]  (W3, gated kernel only)
+    const uint16_t* src;       // activation rows, K wide
+    const int32_t* gather;     // row -> source row, or null (identity)
+    const int32_t* offsets;    // [groups+1] expert-major row offsets, or null
+    int nrows;                 // rows of the single group when offsets is null
+    int groups, M, K;
+    int ksplit;                // reduction length per gridDim.z slice
+    int64_t split_stride;      // elements between split slices of out
+    void* out;                 // gated: bf16 [rows][M]; plain: fp32 [split][rows][M]
+};
+
+__device__ __forceinline__ bf16x8 ld16(const uint16_t* p) {
+    return *reinterpret_cast<const bf16x8*>(p);
+}
+
+template <bool GATED, int NSUB>
+__global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
+    constexpr int BN = 16 * NSUB;
+    __shared__ int tstart[65];
+    const int lane = lane_id(), wave = threadIdx.x / kWave;
+
+    // per-group first tile index (prefix over ceil(n_e / BN))
+    int ntiles;
+    if (a.offsets) {
+        if (threadIdx.x == 0) {
+            int acc = 0;
+            for (int e = 0; e < a.groups; ++e) {
+                tstart[e] = acc;
+                acc += (a.offsets[e + 1] - a.offsets[e] + BN - 1) / BN;
+            }
+            tstart[a.groups] = acc;
+        }
+        __syncthreads();
+        ntiles = tstart[a.groups];
+    } else {
+        ntiles = (a.nrows + BN - 1) / BN;
+    }
+
+    const int i = lane & 15, g = lane >> 4;
+    const int m0 = blockIdx.x * 64 + wave * 16;
+    const int kbeg = blockIdx.z * a.ksplit;
+    const int kend = kbeg + a.ksplit;
+
+    for (int tile = blockIdx.y; tile < ntiles; tile += gridDim.y) {
+        int e = 0, r0, n;
+        if (a.offsets) {
+            while (tstart[e + 1] <= tile) ++e;
+            r0 = a.offsets[e] + (tile - tstart[e]) * BN;
+            n = min(BN, a.offsets[e + 1] - r0);
+        } else {
+            r0 = tile * BN;
+            n = min(BN, a.nrows - r0);
+        }
+        const size_t wrow = (static_cast<size_t>(e) * a.M + m0 + i) * a.K + 8 * g;
+        const uint16_t* pa = a.wa + wrow;
+        const uint16_t* pb = GATED ? a.wb + wrow : nullptr;
+        const uint16_t* px[NSUB];
+        bool xok[NSUB];
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+            const int c = s * 16 + i;
+            xok[s] = c < n;
+            const int srow = xok[s] ? (a.gather ? a.gather[r0 + c] : r0 + c) : 0;
+            px[s] = a.src + static_cast<size_t>(srow) * a.K + 8 * g;
+        }
+        f32x4 acc_a[NSUB], acc_b[NSUB];
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+            acc_a[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+            acc_b[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        const bf16x8 zero = {};
+        // groups of U k-steps: all loads of a group are issued before its MFMAs
+        constexpr int U = NSUB >= 4 ? 4 : 8;
+        int k = kbeg;
+        for (; k + 32 * U <= kend; k += 32 * U) {
+            bf16x8 A[U], B[U], X[U][NSUB];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                A[u] = ld16(pa + k + 32 * u);
+                if constexpr (GATED) B[u] = ld16(pb + k + 32 * u);
+#pragma unroll
+                for (int s = 0; s < NSUB; ++s) X[u][s] = xok[s] ? ld16(px[s] + k + 32 * u) : zero;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int s = 0; s < NSUB; ++s) {
+                    acc_a[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[u], X[u][s], acc_a[s], 0, 0, 0);
+                    if constexpr (GATED)
+                        acc_b[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(B[u], X[u][s], acc_b[s], 0, 0, 0);
+                }
+        }
+        for (; k < kend; k += 32) {
+            const bf16x8 A = ld16(pa + k);
+            bf16x8 B;
+            if constexpr (GATED) B = ld16(pb + k);
+#pragma unroll
+            for (int s = 0; s < NSUB; ++s) {
+                const bf16x8 X = xok[s] ? ld16(px[s] + k) : zero;
+                acc_a[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, X, acc_a[s], 0, 0, 0);
+                if constexpr (GATED)
+                    acc_b[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(B, X, acc_b[s], 0, 0, 0);
+            }
+        }
+        // result: lane holds weight rows m0 + 4g + q (q < 4) for token column s*16 + i
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+            const int c = s * 16 + i;
+            if (c >= n) continue;
+            const size_t o = static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g;
+            if constexpr (GATED) {
+                uint16_t hv[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) hv[q] = f32_to_bf16(silu(acc_a[s][q]) * acc_b[s][q]);
+                uint2 pk;
+                pk.x = static_cast<uint32_t>(hv[0]) | (static_cast<uint32_t>(hv[1]) << 16);
+                pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
+                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + o) = pk;
+            } else {
+                float* op = static_cast<float*>(a.out) + blockIdx.z * a.split_stride + o;
+                *reinterpret_cast<float4*>(op) =
+                    make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
+            }
+        }
+    }
+}
+
+template <bool GATED>
+hipError_t launch_stream(const StreamArgs& a, int nsub, int tiles_y, int splits, hipStream_t s) {
+    const dim3 grid(a.M / 64, tiles_y, splits), block(256);
+    switch (nsub) {
+        case 1: stream_kernel<GATED, 1><<<grid, block, 0, s>>>(a); break;
+        case 2: stream_kernel<GATED, 2><<<grid, block, 0, s>>>(a); break;
+        default: stream_kernel<GATED, 4><<<grid, block, 0, s>>>(a); break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+// Token sub-tiles per stream tile: enough to cover the expected tokens per
+// expert in one pass over the weights, at most 4 (64 tokens).
+static int pick_nsub(int64_t rows_expected_per_group) {
+    if (rows_expected_per_group <= 16) return 1;
+    if (rows_expected_per_group <= 32) return 2;
+    return 4;
+}
+
+int down_splits(const eat_params_t& p, int32_t T) {
+    if (p.expert_dtype != EAT_BF16) return 1;
+    // Split the down projection's reduction dimension while the number of
+    // 16-row wave tiles over the likely-active experts is below ~2048.
+    const int64_t assign = std::max<int64_t>(1, static_cast<int64_t>(T) * p.top_k);
+    const int64_t active = std::min<int64_t>(p.E, assign);
+    const int64_t waves = static_cast<int64_t>(p.d_model / 16) * active;
+    int s = 1;
+    while (s < 8 && p.d_ffn % (64 * s) == 0 && waves * s < 2048) s *= 2;
+    return s;
+}
+
+hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap, const float* x,
+                              const float* w1, const float* w3, const float* w2,
+                              const int32_t* offsets, const int32_t* tok_idx,
+                              const int32_t* row_expert, float* h, float* yp, hipStream_t s) {
+    F32Args a{x, w1, w3, w2, tok_idx, row_expert, offsets + p.E, 0, p.d_model, p.d_ffn, h, yp};
+    (void)T;
+    return launch_f32_pair(a, rows_cap, s);
+}
+
+hipError_t launch_shared_f32(const eat_params_t& p, int32_t T, const float* x, const float* ws1,
+                             const float* ws3, const float* ws2, float* hs, float* ys,
+                             hipStream_t s) {
+    F32Args a{x, ws1, ws3, ws2, nullptr, nullptr, nullptr, T, p.d_model, p.d_shared, hs, ys};
+    return launch_f32_pair(a, T, s);
+}
+
+hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_cap, const uint16_t* x,
+                               const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
+                               const int32_t* offsets, const int32_t* tok_idx, uint16_t* h,
+                               float* yp, hipStream_t s) {
+    // Expected rows per active expert: T*K spread over min(E, T*K) experts.
+    const int64_t assign = static_cast<int64_t>(T) * p.top_k;
+    const int64_t active = std::max<int64_t>(1, std::min<int64_t>(p.E, assign));
+    const int nsub = pick_nsub((assign + active - 1) / active);
+    const int bn = 16 * nsub;
+    const int64_t max_tiles = std::min<int64_t>(rows_cap, (rows_cap + bn - 1) / bn + p.E);
+    // keep roughly 8 workgroups per CU in flight; extra tiles loop
+    const int cap_up = std::max(1, 2048 / std::max(1, p.d_ffn / 64));
+    const int tiles_up = static_cast<int>(std::min<int64_t>(max_tiles, cap_up));
+
+    StreamArgs up{};
+    up.wa = w1; up.wb = w3; up.src = x; up.gather = tok_idx; up.offsets = offsets;
+    up.groups = p.E; up.M = p.d_ffn; up.K = p.d_model; up.ksplit = p.d_model; up.split_stride = 0;
+    up.out = h;
+    hipError_t err = launch_stream<true>(up, nsub, tiles_up, 1, s);
+    if (err != hipSuccess) return err;
+
+    const int splits = down_splits(p, T);
+    const int cap_dn = std::max(1, 2048 / std::max(1, (p.d_model / 64) * splits));
+    const int tiles_dn = static_cast<int>(std::min<int64_t>(max_tiles, cap_dn));
+    StreamArgs dn{};
+    dn.wa = w2; dn.wb = nullptr; dn.src = h; dn.gather = nullptr; dn.offsets = offsets;
+    dn.groups = p.E; dn.M = p.d_model; dn.K = p.d_ffn; dn.ksplit = p.d_ffn / splits;
+    dn.split_stride = rows_cap * p.d_model; dn.out = yp;
+    return launch_stream<false>(dn, nsub, tiles_dn, splits, s);
+}
+
+hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* x, const uint16_t* ws1,
+                              const uint16_t* ws3, const uint16_t* ws2, uint16_t* hs, float* ys,
+                              hipStream_t s) {
+    const int nsub = T <= 16 ? 1 : (T <= 32 ? 2 : 4);
+    const int bn = 16 * nsub;
+    const int tiles = (T + bn - 1) / bn;
+    StreamArgs up{};
+    up.wa = ws1; up.wb = ws3; up.src = x; up.gather = nullptr; up.offsets = nullptr; up.nrows = T;
+    up.groups = 1; up.M = p.d_shared; up.K = p.d_model; up.ksplit = p.d_model; up.out = hs;
+    const int cap_up = std::max(1, 2048 / std::max(1, p.d_shared / 64));
+    hipError_t err = launch_stream<true>(up, nsub, std::min(tiles, cap_up), 1, s);
+    if (err != hipSuccess) return err;
+    StreamArgs dn{};
+    dn.wa = ws2; dn.wb = nullptr; dn.src = hs; dn.gather = nullptr; dn.offsets = nullptr; dn.nrows = T;
+    dn.groups = 1; dn.M = p.d_model; dn.K = p.d_shared; dn.ksplit = p.d_shared; dn.split_stride = 0;
+    dn.out = ys;
+    const int cap_dn = std::max(1, 2048 / std::max(1, p.d_model / 64));
+    return launch_stream<false>(dn, nsub, std::min(tiles, cap_dn), 1, s);
+}
+
+}  // namespace eat

@@ -1,0 +1,100 @@
+"""A small owner object around one EAT layer handle.
+
+Holds the handle, the caller-owned account tensors and a workspace
+allocated with torch (device memory plumbing only), and forwards to the C
+entry points of ``_lib``.  All compute runs in libeat.so.
+"""
+from __future__ import annotations
+
+from typing import Dict, Optional
+
+import torch
+
+from . import _lib as L
+
+
+class EatLayer:
+    def __init__(self, params: L.eat_params_t, max_tokens: int, weights: Dict[str, torch.Tensor],
+                 device: str = "cuda"):
+        self.params = params
+        self.max_tokens = int(max_tokens)
+        self.device = torch.device(device)
+        self.handle = L.eat_create(params, max_tokens)
+        self.w = weights
+        E = params.E
+        self.n = torch.zeros(E, dtype=torch.int64, device=self.device)
+        self.p_total = torch.zeros(E, dtype=torch.float32, device=self.device)
+        self.c_s = torch.zeros(E, dtype=torch.float32, device=self.device)
+        self._ws: Optional[torch.Tensor] = None
+
+    # account state -------------------------------------------------------
+    @property
+    def acc(self) -> L.eat_accounts_t:
+        return L.accounts(self.n, self.p_total, self.c_s)
+
+    def reset_accounts(self, stream=None) -> None:
+        L.eat_reset_accounts(self.handle, self.acc, stream)
+
+    def load_accounts(self, n, p_total, c_s) -> None:
+        self.n.copy_(torch.as_tensor(n, dtype=torch.int64))
+        self.p_total.copy_(torch.as_tensor(p_total, dtype=torch.float32))
+        self.c_s.copy_(torch.as_tensor(c_s, dtype=torch.float32))
+
+    def accounts_host(self):
+        return (self.n.cpu().numpy(), self.p_total.cpu().numpy(), self.c_s.cpu().numpy())
+
+    # workspace -----------------------------------------------------------
+    def workspace(self, T: int) -> torch.Tensor:
+        need = L.eat_workspace_size(self.handle, T)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        return self._ws
+
+    # calls ---------------------------------------------------------------
+    def forward(self, x: torch.Tensor, trend: Optional[torch.Tensor] = None, y: Optional[torch.Tensor] = None,
+                mask_out: Optional[torch.Tensor] = None, load_out: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+        T = x.shape[0]
+        if y is None:
+            y = torch.empty_like(x)
+        ws = self.workspace(T)
+        w = self.w
+        L.eat_moe_forward(self.handle, x, T, w["w_router"], w["w1"], w["w3"], w["w2"],
+                          w.get("ws1"), w.get("ws3"), w.get("ws2"), self.acc, trend, y, mask_out,
+                          load_out, ws, ws.numel(), stream)
+        return y
+
+    def route(self, x: torch.Tensor, trend: Optional[torch.Tensor] = None, stream=None):
+        T = x.shape[0]
+        E = self.params.E
+        mask = torch.empty(T, dtype=torch.int64, device=self.device)
+        k = torch.empty(T, dtype=torch.int32, device=self.device)
+        gate = torch.empty(T, E, dtype=torch.float32, device=self.device)
+        prob = torch.empty(T, E, dtype=torch.float32, device=self.device)
+        L.eat_route(self.handle, x, T, self.w["w_router"], self.acc, trend, mask, k, gate, prob,
+                    None, 0, stream)
+        return mask, k, gate, prob
+
+    def close(self) -> None:
+        if self.handle:
+            L.eat_destroy(self.handle)
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def to_device(weights: Dict, device: str = "cuda") -> Dict[str, torch.Tensor]:
+    """Upload generator output (fp32 arrays or bf16 bit patterns as uint16)
+    to device tensors (torch.bfloat16 for bf16)."""
+    import numpy as np
+    out = {}
+    for k, v in weights.items():
+        t = torch.from_numpy(np.ascontiguousarray(v))
+        if v.dtype == np.uint16:
+            t = t.view(torch.bfloat16)
+        out[k] = t.to(device)
+    return out

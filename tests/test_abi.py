@@ -1,0 +1,213 @@
+"""C-ABI checks that need no GPU.
+
+* libeat.so loads and exports every function include/eat.h declares;
+* the ctypes mirror of eat_params_t / eat_accounts_t has the C layout
+  (checked against a probe compiled with gcc from the header itself);
+* eat_params_default fills the paper's hyper-parameter table;
+* every validation path returns its status on the host, before any HIP
+  call (these calls use fake addresses that are never dereferenced).
+"""
+import ctypes as C
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+import paper_2609_33614_amd as eat
+from paper_2609_33614_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "eat.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH), reason="libeat.so not built")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(eat_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    lib = C.CDLL(L.LIB_PATH)
+    names = _declared_functions()
+    assert {"eat_create", "eat_route", "eat_moe_forward", "eat_reset_accounts"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), f"{n} not exported"
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="gcc missing")
+def test_struct_layout_matches_header(tmp_path):
+    fields = [f for f, _ in L.eat_params_t._fields_]
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "eat.h"', "int main(void){",
+             'printf("%zu\\n", sizeof(eat_params_t));',
+             'printf("%zu\\n", sizeof(eat_accounts_t));']
+    for f in fields:
+        lines.append(f'printf("%zu\\n", offsetof(eat_params_t, {f}));')
+    lines.append("return 0;}")
+    c = tmp_path / "probe.c"
+    c.write_text("\n".join(lines))
+    exe = tmp_path / "probe"
+    r = subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+                        "-I", "/opt/rocm/include", str(c), "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    out = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()]
+    assert out[0] == C.sizeof(L.eat_params_t)
+    assert out[1] == C.sizeof(L.eat_accounts_t)
+    for f, off in zip(fields, out[2:]):
+        assert getattr(L.eat_params_t, f).offset == off, f
+
+
+def test_defaults_are_the_papers_table():
+    p = eat.eat_params_default()
+    assert p.mode == eat.EAT_MODE_EAT and p.top_k == 2
+    expect = dict(alpha=0.95, w1=0.3, w2=0.3, w3=0.4, beta=0.6, alpha1=0.5, alpha2=1.0,
+                  kappa1=0.7, kappa2=0.3, ppl_up=1.2, ppl_down=0.9, q_lo=0.1, q_hi=0.9, eps=1e-8,
+                  inv_temperature=1.0)
+    for k, v in expect.items():
+        assert getattr(p, k) == pytest.approx(v, rel=1e-6), k
+    assert p.cs_mode == 0 and p.d_shared == 0
+
+
+def _params(**kw):
+    base = dict(E=8, d_model=128, d_ffn=256, top_k=2, act_dtype=eat.EAT_F32, expert_dtype=eat.EAT_F32)
+    base.update(kw)
+    return eat.eat_params_default(**base)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("E", 0, L.EAT_ERR_INVALID_ARG),
+    ("E", 65, L.EAT_ERR_UNSUPPORTED),
+    ("top_k", 0, L.EAT_ERR_INVALID_ARG),
+    ("top_k", 9, L.EAT_ERR_INVALID_ARG),
+    ("d_model", 100, L.EAT_ERR_UNSUPPORTED),
+    ("d_ffn", 0, L.EAT_ERR_INVALID_ARG),
+    ("d_shared", 96, L.EAT_ERR_UNSUPPORTED),
+    ("alpha", 1.5, L.EAT_ERR_INVALID_ARG),
+    ("beta", -0.1, L.EAT_ERR_INVALID_ARG),
+    ("q_lo", 0.95, L.EAT_ERR_INVALID_ARG),
+    ("inv_temperature", 0.0, L.EAT_ERR_INVALID_ARG),
+    ("w3", float("nan"), L.EAT_ERR_INVALID_ARG),
+    ("cs_mode", 2, L.EAT_ERR_INVALID_ARG),
+    ("mode", 3, L.EAT_ERR_INVALID_ARG),
+    ("act_dtype", 7, L.EAT_ERR_INVALID_ARG),
+    ("expert_dtype", 1, L.EAT_ERR_UNSUPPORTED),
+    ("top_p_cap", 9, L.EAT_ERR_INVALID_ARG),
+])
+def test_create_rejects_bad_params(field, value, status):
+    p = _params(**{field: value})
+    with pytest.raises(eat.EatError) as ei:
+        eat.eat_create(p, 32)
+    assert ei.value.status == status
+
+
+def test_create_rejects_bad_top_p_and_token_limits():
+    with pytest.raises(eat.EatError):
+        eat.eat_create(_params(mode=eat.EAT_MODE_TOPP, top_p=0.0), 32)
+    with pytest.raises(eat.EatError):
+        eat.eat_create(_params(mode=eat.EAT_MODE_TOPP, top_p=1.5), 32)
+    for bad in (0, -1, (1 << 24) + 1):
+        with pytest.raises(eat.EatError):
+            eat.eat_create(_params(), bad)
+
+
+def test_workspace_grows_with_tokens_and_mode():
+    h_eat = eat.eat_create(_params(), 1024)
+    h_topk = eat.eat_create(_params(mode=eat.EAT_MODE_TOPK), 1024)
+    try:
+        sizes = [eat.eat_workspace_size(h_eat, T) for T in (0, 1, 16, 1024)]
+        assert sizes == sorted(sizes) and sizes[-1] > sizes[0]
+        # EAT keeps exact ties (up to E per token), Top-K exactly K
+        assert eat.eat_workspace_size(h_eat, 1024) > eat.eat_workspace_size(h_topk, 1024)
+        with pytest.raises(eat.EatError):
+            eat.eat_workspace_size(h_eat, 1025)
+        with pytest.raises(eat.EatError):
+            eat.eat_workspace_size(h_eat, -1)
+    finally:
+        eat.eat_destroy(h_eat)
+        eat.eat_destroy(h_topk)
+
+
+FAKE = 1 << 20          # 16-byte (and 256-byte) aligned fake address, never dereferenced
+
+
+def _fwd(h, **kw):
+    args = dict(x=FAKE, T=4, w_router=FAKE, w1=FAKE, w3=FAKE, w2=FAKE, ws1=None, ws3=None, ws2=None,
+                acc=L.accounts(FAKE, FAKE, FAKE), ppl_trend=None, y=FAKE, mask_out=None,
+                expert_load_out=None, ws=FAKE, ws_bytes=0, stream=0)
+    args.update(kw)
+    eat.eat_moe_forward(h, **args)
+
+
+def test_forward_validation_happens_on_the_host():
+    h = eat.eat_create(_params(), 64)
+    try:
+        need = eat.eat_workspace_size(h, 4)
+        cases = [
+            (dict(x=None, ws_bytes=need), L.EAT_ERR_INVALID_ARG),
+            (dict(w2=None, ws_bytes=need), L.EAT_ERR_INVALID_ARG),
+            (dict(y=None, ws_bytes=need), L.EAT_ERR_INVALID_ARG),
+            (dict(x=FAKE + 4, ws_bytes=need), L.EAT_ERR_INVALID_ARG),          # misaligned
+            (dict(T=65, ws_bytes=need), L.EAT_ERR_INVALID_ARG),                # > max_tokens
+            (dict(T=-1, ws_bytes=need), L.EAT_ERR_INVALID_ARG),
+            (dict(acc=L.accounts(None, FAKE, FAKE), ws_bytes=need), L.EAT_ERR_INVALID_ARG),
+            (dict(ws1=FAKE, ws_bytes=need), L.EAT_ERR_INVALID_ARG),            # no shared expert declared
+            (dict(ws_bytes=need - 1), L.EAT_ERR_WORKSPACE),
+            (dict(ws=None, ws_bytes=need), L.EAT_ERR_WORKSPACE),
+            (dict(ws=FAKE + 16, ws_bytes=need), L.EAT_ERR_INVALID_ARG),        # workspace not 256-aligned
+            (dict(mask_out=FAKE + 4, ws_bytes=need), L.EAT_ERR_INVALID_ARG),
+        ]
+        for kw, status in cases:
+            with pytest.raises(eat.EatError) as ei:
+                _fwd(h, **kw)
+            assert ei.value.status == status, kw
+        # an empty call is valid and launches nothing
+        _fwd(h, T=0, ws=None, ws_bytes=0)
+    finally:
+        eat.eat_destroy(h)
+
+
+def test_shared_expert_pointers_required_when_declared():
+    h = eat.eat_create(_params(d_shared=128), 8)
+    try:
+        with pytest.raises(eat.EatError) as ei:
+            _fwd(h, ws_bytes=eat.eat_workspace_size(h, 4))
+        assert ei.value.status == L.EAT_ERR_INVALID_ARG
+    finally:
+        eat.eat_destroy(h)
+
+
+def test_baseline_modes_need_no_accounts():
+    h = eat.eat_create(_params(mode=eat.EAT_MODE_TOPK), 8)
+    try:
+        # null accounts pass validation in Top-K; the empty call launches nothing
+        _fwd(h, T=0, acc=L.accounts(None, None, None), ws=None)
+    finally:
+        eat.eat_destroy(h)
+
+
+def test_route_validation_happens_on_the_host():
+    h = eat.eat_create(_params(), 16)
+    try:
+        base = dict(x=FAKE, T=4, w_router=FAKE, acc=L.accounts(FAKE, FAKE, FAKE), ppl_trend=None,
+                    mask_out=FAKE, k_out=FAKE, gate_out=FAKE, prob_out=None, stream=0)
+        for kw in (dict(mask_out=None), dict(k_out=None), dict(gate_out=None), dict(x=None),
+                   dict(w_router=FAKE + 8), dict(T=17), dict(acc=L.accounts(FAKE, None, FAKE))):
+            args = dict(base); args.update(kw)
+            with pytest.raises(eat.EatError) as ei:
+                eat.eat_route(h, **args)
+            assert ei.value.status == L.EAT_ERR_INVALID_ARG, kw
+        args = dict(base); args["T"] = 0
+        eat.eat_route(h, **args)
+        with pytest.raises(eat.EatError):
+            eat.eat_reset_accounts(h, L.accounts(None, FAKE, FAKE), 0)
+    finally:
+        eat.eat_destroy(h)
+
+
+def test_status_strings():
+    for s in range(6):
+        assert isinstance(eat.eat_status_string(s), str) and eat.eat_status_string(s)
+    assert eat.eat_status_string(99) == "unknown status"

@@ -13,4 +13,5 @@ from .gmm import (  # noqa: F401
     HiddenStream,
     make_prefill,
     make_trend,
+    make_accounts,
 )

@@ -21,6 +21,8 @@ Recipe (identical for every consumer):
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
+import os
 from dataclasses import dataclass, field
 from typing import Optional, Tuple
 
@@ -79,10 +81,23 @@ SHAPES = {
 def bf16_bits(a: np.ndarray) -> np.ndarray:
     """Round fp32 values to bf16 (round-to-nearest-even) and return the bit
     patterns as uint16.  Used only to produce bf16 input tensors."""
-    a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32)
-    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
-    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    r = u >> np.uint32(16)
+    r &= np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def _parallel(fn, jobs):
+    n = min(16, os.cpu_count() or 1, max(1, len(jobs)))
+    if n == 1 or sum(np.prod(j[3]) for j in jobs) < 4_000_000:
+        for j in jobs:
+            fn(j)
+        return
+    with cf.ThreadPoolExecutor(max_workers=n) as ex:
+        list(ex.map(fn, jobs))
 
 
 def _streams(seed: int, n: int):
@@ -118,12 +133,19 @@ def make_layer_weights(shape: LayerShape, seed: Optional[int] = None, layer: int
     w1 = np.empty((E, F, d), edt)
     w3 = np.empty((E, F, d), edt)
     w2 = np.empty((E, d, F), edt)
-    per_expert = np.random.SeedSequence(int(g_exp.integers(2**63))).spawn(shape.E if E <= shape.E else E)
+    # one child seed per (expert, matrix): values do not depend on E or on
+    # how many threads draw them
+    per_expert = np.random.SeedSequence(int(g_exp.integers(2**63))).spawn(max(E, shape.E))
+    jobs = []
     for e in range(E):
-        g = np.random.Generator(np.random.PCG64(per_expert[e]))
-        w1[e] = pack(_normal(g, (F, d), 1.0 / np.sqrt(d)))
-        w3[e] = pack(_normal(g, (F, d), 1.0 / np.sqrt(d)))
-        w2[e] = pack(_normal(g, (d, F), 1.0 / np.sqrt(F)))
+        s1, s3, s2 = per_expert[e].spawn(3)
+        jobs += [(w1, e, s1, (F, d), d), (w3, e, s3, (F, d), d), (w2, e, s2, (d, F), F)]
+
+    def draw(job):
+        dst, e, seq, shp, fan_in = job
+        dst[e] = pack(_normal(np.random.Generator(np.random.PCG64(seq)), shp, 1.0 / np.sqrt(fan_in)))
+
+    _parallel(draw, jobs)
     out = {"w_router": w_router, "w1": w1, "w3": w3, "w2": w2}
     Fs = shape.F_shared if F_shared is None else F_shared
     if Fs:
@@ -202,3 +224,16 @@ def make_trend(T: int, seed: int, frac_up: float = 0.5) -> np.ndarray:
     u = g.random(T)
     out = np.where(u < frac_up, 1, np.where(u < frac_up + (1 - frac_up) / 2, -1, 0))
     return out.astype(np.int8)
+
+
+def make_accounts(E: int, seed: int, steps: int = 20, tokens: int = 16, c_scale: float = 1.0):
+    """A plausible non-zero account state (N int64, P_total fp32, C_s fp32)
+    with the shapes of the layer's state: N counts as if ``steps`` calls of
+    ``tokens`` tokens had each picked a few experts; P_total a share of N;
+    C_s a positive magnitude of scale ``c_scale``.  Some experts stay at 0."""
+    g = np.random.Generator(np.random.PCG64(seed))
+    n = g.binomial(steps * tokens, 0.2, size=E).astype(np.int64)
+    n[g.random(E) < 0.2] = 0
+    p = (n * g.uniform(0.1, 0.6, size=E)).astype(np.float32)
+    c = np.where(n > 0, g.uniform(0.2, 1.0, size=E) * c_scale, 0.0).astype(np.float32)
+    return n, p, c
