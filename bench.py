@@ -1,0 +1,287 @@
+#!/usr/bin/env python3
+"""Benchmark of the EAT MoE-layer forward on one MI355X.
+
+Workload: the Mixtral-8x7B-shaped MoE layer (d_model 4096, 8 SwiGLU experts
+of width 14336, bf16 experts, fp32 router and accounts, logits scaled by
+1/T with T = 0.5), decode with a batch of 64 tokens per step, hidden states
+from a seeded 16-cluster Gaussian mixture (cluster-sticky per sequence,
+10% re-draw per step), accounts starting at zero.  A step is one whole
+layer forward (route, permute, experts, combine, account update) over one
+batch; all inputs are resident in HBM before timing starts.
+
+Prints one JSON line: EAT tokens/s (``value``), the Top-K (K=2) and Top-P
+(p=0.6) baselines on the same inputs, mean activated experts per token,
+the experts touched per step, the up/gate kernel's achieved HBM bandwidth
+against the MI355X peak (timed per launch with HIP events on the launch
+stream), a batch sweep, and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--batch B] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer tokens/s + activated experts/token (EAT vs Top-K); HBM GB/s % peak"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime (timing events)."""
+
+    def __init__(self):
+        self.hip = C.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [C.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [C.c_void_p]
+        self.owned = []
+
+    def create(self, n: int):
+        out = []
+        for _ in range(n):
+            e = C.c_void_p()
+            assert self.hip.hipEventCreate(C.byref(e)) == 0
+            out.append(e.value)
+        self.owned += out
+        return out
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = C.c_float()
+        assert self.hip.hipEventSynchronize(b) == 0
+        assert self.hip.hipEventElapsedTime(C.byref(ms), a, b) == 0
+        return ms.value
+
+    def close(self):
+        for e in self.owned:
+            self.hip.hipEventDestroy(e)
+        self.owned = []
+
+
+def popcounts(masks: np.ndarray) -> np.ndarray:
+    m = masks.astype(np.uint64)
+    return np.array([[bin(int(v)).count("1") for v in row] for row in m])
+
+
+def union_sizes(masks: np.ndarray) -> np.ndarray:
+    out = []
+    for row in masks.astype(np.uint64):
+        u = 0
+        for v in row:
+            u |= int(v)
+        out.append(bin(u).count("1"))
+    return np.array(out)
+
+
+def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bool):
+    import torch
+
+    from paper_2609_33614_amd import _lib as L
+    from paper_2609_33614_amd.layer import EatLayer
+
+    p = L.eat_params_default(mode=mode, E=shape.E, d_model=shape.d, d_ffn=shape.F, top_k=shape.K,
+                             top_p=0.6, inv_temperature=shape.inv_temp)
+    lay = EatLayer(p, B, wdev)
+    E = shape.E
+    y = torch.empty(B, shape.d, dtype=torch.bfloat16, device="cuda")
+    masks = torch.empty(steps, B, dtype=torch.int64, device="cuda")
+    scratch = torch.empty(B, dtype=torch.int64, device="cuda")
+    # warm-up on a scratch account state, then start from zero accounts
+    for s in range(warmup):
+        lay.forward(xs[s % xs.shape[0]], y=y, mask_out=scratch)
+    lay.reset_accounts()
+    torch.cuda.synchronize()
+
+    stage = [None] * L.EAT_NUM_STAGE_EVENTS
+    evs = ev.create(3 * steps) if profile else []
+    t0, t1 = ev.create(2)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    ev.hip.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
+    ev.hip.hipEventRecord(t0, stream.cuda_stream)
+    for s in range(steps):
+        x = xs[warmup + s]
+        if profile:
+            stage[L.EAT_STAGE_PERMUTED] = evs[3 * s]
+            stage[L.EAT_STAGE_UP] = evs[3 * s + 1]
+            stage[L.EAT_STAGE_DOWN] = evs[3 * s + 2]
+            lay.forward(x, y=y, mask_out=masks[s], events=stage)
+        else:
+            lay.forward(x, y=y, mask_out=masks[s])
+    ev.hip.hipEventRecord(t1, stream.cuda_stream)
+    torch.cuda.synchronize()
+    total_ms = ev.elapsed_ms(t0, t1)
+    up_ms = dn_ms = None
+    if profile:
+        up_ms = np.array([ev.elapsed_ms(evs[3 * s], evs[3 * s + 1]) for s in range(steps)])
+        dn_ms = np.array([ev.elapsed_ms(evs[3 * s + 1], evs[3 * s + 2]) for s in range(steps)])
+    m = masks.cpu().numpy().astype(np.int64).view(np.uint64)
+    k = popcounts(m)
+    U = union_sizes(m)
+    acc = lay.accounts_host()
+    lay.close()
+    return dict(total_ms=total_ms, up_ms=up_ms, dn_ms=dn_ms, k=k, U=U, E=E, accounts=acc)
+
+
+def traffic_up(shape, B, k_row, U):
+    """Algorithmic HBM bytes of one up/gate launch: W1 and W3 rows of every
+    expert in the step's union, the B token rows read, the H rows written."""
+    d, F = shape.d, shape.F
+    return U * 2 * F * d * 2 + B * d * 2 + k_row.sum() * F * 2
+
+
+def traffic_down(shape, k_row, U):
+    """Algorithmic HBM bytes of one down launch: W2 of every expert in the
+    union, the H rows read, one fp32 output row per (token, expert)."""
+    d, F = shape.d, shape.F
+    return U * d * F * 2 + k_row.sum() * F * 2 + k_row.sum() * d * 4
+
+
+def cpu_baseline(shape, w_host, xs_host, B, max_seconds: float):
+    """The oracle, unchanged, on the first steps of the same EAT workload."""
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+        cores = int(max(blas)) if blas else 1
+    except Exception:
+        cores = 1
+    prm = O.Params(mode=O.MODE_EAT, K=shape.K, inv_temp=shape.inv_temp)
+    acc = O.zero_accounts(shape.E)
+    t = time.time()
+    n = 0
+    while True:
+        out = O.moe_step(xs_host[n], w_host, acc, None, prm)
+        acc = out.acc
+        n += 1
+        if time.time() - t >= max_seconds or n >= xs_host.shape[0]:
+            break
+    dt = time.time() - t
+    return {"value": round(n * B / dt, 3), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} EAT decode step(s) of B={B} on the same layer and inputs "
+                      f"({n * B} tokens, {dt:.1f} s; numpy fp64, BLAS threads={cores})"}
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--batch", type=int, default=64)
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    args = ap.parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the EAT layer path here is a single-GPU build "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}).", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2609_33614_amd import _lib as L
+    from paper_2609_33614_amd.layer import to_device
+    from workload import SHAPES, HiddenStream, make_layer_weights
+
+    L.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    shape = SHAPES["mixtral"]
+    B, K, W = args.batch, args.steps, args.warmup
+    log(f"generating weights d={shape.d} E={shape.E} F={shape.F}")
+    t = time.time()
+    w_host = make_layer_weights(shape)
+    wdev = to_device(w_host)
+    log(f"weights ready in {time.time() - t:.1f} s; generating {W + K} steps of B={B}")
+    xs_host = HiddenStream(shape, B).steps(W + K)
+    xs = torch.from_numpy(xs_host).view(torch.bfloat16).cuda()
+    ev = HipEvents()
+
+    results = {}
+    for name in ("eat", "topk", "topp"):
+        log(f"timing {name}: {K} steps (+{W} warm-up)")
+        results[name] = run_mode(L.MODES[name], shape, wdev, xs, B, K, W, ev, profile=True)
+    r = results["eat"]
+    ms_step = r["total_ms"] / K
+    value = B * K / (r["total_ms"] / 1e3)
+
+    up_bytes = np.array([traffic_up(shape, B, r["k"][s], r["U"][s]) for s in range(K)], dtype=np.float64)
+    dn_bytes = np.array([traffic_down(shape, r["k"][s], r["U"][s]) for s in range(K)], dtype=np.float64)
+    up_gbs = up_bytes.sum() / (r["up_ms"].sum() / 1e3) / 1e9
+    dn_gbs = dn_bytes.sum() / (r["dn_ms"].sum() / 1e3) / 1e9
+
+    def summary(res):
+        return {"tokens_per_s": round(B * K / (res["total_ms"] / 1e3), 1),
+                "ms_per_step": round(res["total_ms"] / K, 4),
+                "mean_activated_experts": round(float(res["k"].mean()), 4),
+                "mean_experts_touched_per_step": round(float(res["U"].mean()), 3),
+                "up_gate_us_per_launch": round(float(res["up_ms"].mean() * 1e3), 2),
+                "down_us_per_launch": round(float(res["dn_ms"].mean() * 1e3), 2)}
+
+    sweep = []
+    if not args.no_sweep:
+        for b in (1, 8, 32):
+            xb = torch.from_numpy(HiddenStream(shape, b).steps(W + K)).view(torch.bfloat16).cuda()
+            row = {"batch": b}
+            for name in ("eat", "topk"):
+                log(f"sweep B={b} {name}")
+                rr = run_mode(L.MODES[name], shape, wdev, xb, b, K, W, ev, profile=False)
+                row[name] = {"tokens_per_s": round(b * K / (rr["total_ms"] / 1e3), 1),
+                             "ms_per_step": round(rr["total_ms"] / K, 4),
+                             "mean_activated_experts": round(float(rr["k"].mean()), 4),
+                             "mean_experts_touched_per_step": round(float(rr["U"].mean()), 3)}
+            sweep.append(row)
+            del xb
+    ev.close()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(shape, w_host, xs_host[W:], B, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian-mixture hidden states, random-init weights)",
+        "config": {"workload": "Mixtral-shaped MoE layer decode, EAT routing",
+                   "d_model": shape.d, "experts": shape.E, "d_ffn": shape.F, "top_k": shape.K,
+                   "batch": B, "logit_scale": shape.inv_temp, "router": "fp32", "experts_dtype": "bf16"},
+        "roofline": {"bound": "hbm", "kernel": "expert up/gate (stream_kernel<gated>)",
+                     "achieved": round(up_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(up_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "down_achieved": round(dn_gbs, 1),
+                     "bytes_per_launch": round(float(up_bytes.mean()), 0),
+                     "us_per_launch": round(float(r["up_ms"].mean() * 1e3), 2)},
+        "cpu_baseline": cpu,
+        "modes": {name: summary(res) for name, res in results.items()},
+        "sweep": sweep,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -176,6 +176,33 @@ eat_status_t eat_moe_forward(eat_handle_t h, const void* x, int32_t T, const flo
                              uint64_t* mask_out, int32_t* expert_load_out,
                              void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Stage boundaries of eat_moe_forward, in launch order. */
+typedef enum {
+    EAT_STAGE_BEGIN = 0,      /* before routing                              */
+    EAT_STAGE_ROUTED = 1,     /* routing done, before the permutation        */
+    EAT_STAGE_PERMUTED = 2,   /* before the expert up/gate projection        */
+    EAT_STAGE_UP = 3,         /* up/gate done, before the down projection    */
+    EAT_STAGE_DOWN = 4,       /* down done, before the shared expert         */
+    EAT_STAGE_SHARED = 5,     /* before the combine                          */
+    EAT_STAGE_COMBINED = 6,   /* before the account update                   */
+    EAT_STAGE_END = 7,        /* after the last kernel                       */
+    EAT_NUM_STAGE_EVENTS = 8
+} eat_stage_t;
+
+/* eat_moe_forward that also records events[i] on `stream` at stage boundary
+ * i for every non-null events[i], i < n_events <= EAT_NUM_STAGE_EVENTS, so a
+ * caller can time individual kernels with hipEventElapsedTime.  Events are
+ * created and owned by the caller.  Errors as eat_moe_forward; n_events
+ * outside [0, EAT_NUM_STAGE_EVENTS] or a null array with n_events > 0 is
+ * EAT_ERR_INVALID_ARG. */
+eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, const float* w_router,
+                                      const void* w1, const void* w3, const void* w2,
+                                      const void* ws1, const void* ws3, const void* ws2,
+                                      eat_accounts_t acc, const int8_t* ppl_trend, void* y,
+                                      uint64_t* mask_out, int32_t* expert_load_out,
+                                      void* ws, size_t ws_bytes, hipStream_t stream,
+                                      const hipEvent_t* events, int32_t n_events);
+
 /* Static description of a status code (never NULL). */
 const char* eat_status_string(eat_status_t s);
 

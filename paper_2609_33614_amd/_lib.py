@@ -12,11 +12,13 @@ import os
 from typing import Optional
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libeat.so")
+LIB_PATH = os.environ.get("EAT_LIB_PATH") or os.path.join(_HERE, "libeat.so")
 
 EAT_OK, EAT_ERR_INVALID_ARG, EAT_ERR_UNSUPPORTED, EAT_ERR_WORKSPACE, EAT_ERR_HIP, EAT_ERR_INTERNAL = range(6)
 EAT_MODE_EAT, EAT_MODE_TOPK, EAT_MODE_TOPP = 0, 1, 2
 EAT_F32, EAT_BF16 = 0, 1
+(EAT_STAGE_BEGIN, EAT_STAGE_ROUTED, EAT_STAGE_PERMUTED, EAT_STAGE_UP, EAT_STAGE_DOWN, EAT_STAGE_SHARED,
+ EAT_STAGE_COMBINED, EAT_STAGE_END, EAT_NUM_STAGE_EVENTS) = range(9)
 MODES = {"eat": EAT_MODE_EAT, "topk": EAT_MODE_TOPK, "topp": EAT_MODE_TOPP}
 
 
@@ -65,10 +67,11 @@ def load() -> C.CDLL:
     lib.eat_route.argtypes = [P, P, C.c_int32, P, eat_accounts_t, P, P, P, P, P, P, C.c_size_t, P]
     lib.eat_moe_forward.argtypes = [P, P, C.c_int32, P, P, P, P, P, P, P, eat_accounts_t, P, P, P, P, P,
                                     C.c_size_t, P]
+    lib.eat_moe_forward_profiled.argtypes = lib.eat_moe_forward.argtypes + [P, C.c_int32]
     lib.eat_status_string.argtypes = [C.c_int]
     lib.eat_status_string.restype = C.c_char_p
     for name in ("eat_params_default", "eat_create", "eat_destroy", "eat_workspace_size",
-                 "eat_reset_accounts", "eat_route", "eat_moe_forward"):
+                 "eat_reset_accounts", "eat_route", "eat_moe_forward", "eat_moe_forward_profiled"):
         getattr(lib, name).restype = st
     _lib = lib
     return lib
@@ -152,3 +155,17 @@ def eat_moe_forward(handle: int, x, T: int, w_router, w1, w3, w2, ws1, ws3, ws2,
                                   _ptr(ws1), _ptr(ws3), _ptr(ws2), acc, _ptr(ppl_trend), _ptr(y),
                                   _ptr(mask_out), _ptr(expert_load_out), _ptr(ws), int(ws_bytes),
                                   _stream(stream)), "eat_moe_forward")
+
+
+def eat_moe_forward_profiled(handle: int, x, T: int, w_router, w1, w3, w2, ws1, ws3, ws2,
+                             acc: eat_accounts_t, ppl_trend, y, mask_out, expert_load_out, ws,
+                             ws_bytes: int, stream=None, events=None) -> None:
+    """``events``: sequence of hipEvent_t handles (ints) or None, indexed by
+    stage boundary (EAT_STAGE_*)."""
+    events = list(events or [])
+    arr = (C.c_void_p * max(1, len(events)))(*[e or None for e in events]) if events else None
+    _check(load().eat_moe_forward_profiled(handle, _ptr(x), int(T), _ptr(w_router), _ptr(w1), _ptr(w3),
+                                           _ptr(w2), _ptr(ws1), _ptr(ws3), _ptr(ws2), acc, _ptr(ppl_trend),
+                                           _ptr(y), _ptr(mask_out), _ptr(expert_load_out), _ptr(ws),
+                                           int(ws_bytes), _stream(stream), arr, len(events)),
+           "eat_moe_forward_profiled")

@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <functional>
 #include <new>
 
 #include "eat_internal.h"
@@ -167,12 +168,14 @@ eat_status_t eat_route(eat_handle_t h, const void* x, int32_t T, const float* w_
     return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;
 }
 
-eat_status_t eat_moe_forward(eat_handle_t h, const void* x, int32_t T, const float* w_router,
-                             const void* w1, const void* w3, const void* w2, const void* ws1,
-                             const void* ws3, const void* ws2, eat_accounts_t acc,
-                             const int8_t* ppl_trend, void* y, uint64_t* mask_out,
-                             int32_t* expert_load_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, const float* w_router,
+                                      const void* w1, const void* w3, const void* w2, const void* ws1,
+                                      const void* ws3, const void* ws2, eat_accounts_t acc,
+                                      const int8_t* ppl_trend, void* y, uint64_t* mask_out,
+                                      int32_t* expert_load_out, void* ws, size_t ws_bytes, hipStream_t stream,
+                                      const hipEvent_t* events, int32_t n_events) {
     if (!h || T < 0 || T > h->max_tokens) return EAT_ERR_INVALID_ARG;
+    if (n_events < 0 || n_events > EAT_NUM_STAGE_EVENTS || (n_events > 0 && !events)) return EAT_ERR_INVALID_ARG;
     const eat_params_t& p = h->p;
     if (!x || !w_router || !w1 || !w3 || !w2 || !y) return EAT_ERR_INVALID_ARG;
     const void* a16[] = {x, w_router, w1, w3, w2, y};
@@ -210,22 +213,32 @@ eat_status_t eat_moe_forward(eat_handle_t h, const void* x, int32_t T, const flo
     b.ys = reinterpret_cast<float*>(base + w.ys);
 
     (void)hipGetLastError();
-    hipError_t e = eat::launch_route(p, x, T, w_router, acc, ppl_trend, b.mask, b.k, b.gate, b.prob, stream);
+    hipError_t e = hipSuccess;
+    auto mark = [&](int stage) {
+        if (e == hipSuccess && stage < n_events && events[stage]) e = hipEventRecord(events[stage], stream);
+    };
+    mark(EAT_STAGE_BEGIN);
+    if (e == hipSuccess)
+        e = eat::launch_route(p, x, T, w_router, acc, ppl_trend, b.mask, b.k, b.gate, b.prob, stream);
+    mark(EAT_STAGE_ROUTED);
     if (e == hipSuccess)
         e = eat::launch_permute(p, T, b.mask, b.offsets, b.tok_idx, b.inv, b.row_expert, expert_load_out,
                                 stream);
+    mark(EAT_STAGE_PERMUTED);
     if (e == hipSuccess) {
         if (p.expert_dtype == EAT_BF16)
             e = eat::launch_experts_bf16(p, T, w.rows, static_cast<const uint16_t*>(x),
                                          static_cast<const uint16_t*>(w1), static_cast<const uint16_t*>(w3),
                                          static_cast<const uint16_t*>(w2), b.offsets, b.tok_idx,
-                                         static_cast<uint16_t*>(b.h), b.yp, stream);
+                                         static_cast<uint16_t*>(b.h), b.yp, stream,
+                                         [&]() { mark(EAT_STAGE_UP); });
         else
             e = eat::launch_experts_f32(p, T, w.rows, static_cast<const float*>(x),
                                         static_cast<const float*>(w1), static_cast<const float*>(w3),
                                         static_cast<const float*>(w2), b.offsets, b.tok_idx, b.row_expert,
-                                        static_cast<float*>(b.h), b.yp, stream);
+                                        static_cast<float*>(b.h), b.yp, stream, [&]() { mark(EAT_STAGE_UP); });
     }
+    mark(EAT_STAGE_DOWN);
     const bool shared = p.d_shared > 0;
     if (e == hipSuccess && shared) {
         if (p.expert_dtype == EAT_BF16)
@@ -237,12 +250,24 @@ eat_status_t eat_moe_forward(eat_handle_t h, const void* x, int32_t T, const flo
                                        static_cast<const float*>(ws3), static_cast<const float*>(ws2),
                                        static_cast<float*>(b.hs), b.ys, stream);
     }
+    mark(EAT_STAGE_SHARED);
     if (e == hipSuccess)
         e = eat::launch_combine(p, T, b.mask, b.gate, b.inv, b.yp, shared ? b.ys : nullptr, y, b.nrm, w.splits,
                                 w.rows * p.d_model, stream);
+    mark(EAT_STAGE_COMBINED);
     if (e == hipSuccess && p.mode == EAT_MODE_EAT)
         e = eat::launch_update_accounts(p, b.offsets, b.tok_idx, b.prob, b.nrm, acc, stream);
+    mark(EAT_STAGE_END);
     return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;
+}
+
+eat_status_t eat_moe_forward(eat_handle_t h, const void* x, int32_t T, const float* w_router,
+                             const void* w1, const void* w3, const void* w2, const void* ws1,
+                             const void* ws3, const void* ws2, eat_accounts_t acc,
+                             const int8_t* ppl_trend, void* y, uint64_t* mask_out,
+                             int32_t* expert_load_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+    return eat_moe_forward_profiled(h, x, T, w_router, w1, w3, w2, ws1, ws3, ws2, acc, ppl_trend, y, mask_out,
+                                    expert_load_out, ws, ws_bytes, stream, nullptr, 0);
 }
 
 const char* eat_status_string(eat_status_t s) {

@@ -56,4 +56,12 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 
 __device__ __forceinline__ float silu(float a) { return a / (1.0f + __expf(-a)); }
 
+// Workgroup barrier that only waits for this wave's LDS traffic.  Global
+// loads issued before it stay in flight (__syncthreads() would drain them
+// with a full fence); the "memory" clobber keeps the compiler from moving
+// LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 }  // namespace eat

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <functional>
+
 #include "../../include/eat.h"
 
 struct eat_ctx {
@@ -54,17 +56,21 @@ hipError_t launch_permute(const eat_params_t& p, int32_t T, const uint64_t* mask
                           int32_t* offsets, int32_t* tok_idx, int32_t* inv, int32_t* row_expert,
                           int32_t* expert_load, hipStream_t s);
 
-// Routed experts, fp32 weights and activations (small layers).
+// Routed experts.  `between` runs on the host after the up/gate launch and
+// before the down launch (stage-event hook).
+// fp32 weights and activations (small layers):
 hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap, const float* x,
                               const float* w1, const float* w3, const float* w2,
                               const int32_t* offsets, const int32_t* tok_idx,
-                              const int32_t* row_expert, float* h, float* yp, hipStream_t s);
+                              const int32_t* row_expert, float* h, float* yp, hipStream_t s,
+                              const std::function<void()>& between);
 
-// Routed experts, bf16 weights and activations: MFMA kernels.
+// bf16 weights and activations: MFMA kernels.
 hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_cap,
                                const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
                                const uint16_t* w2, const int32_t* offsets, const int32_t* tok_idx,
-                               uint16_t* h, float* yp, hipStream_t s);
+                               uint16_t* h, float* yp, hipStream_t s,
+                               const std::function<void()>& between);
 
 // Always-on shared expert over all T tokens.
 hipError_t launch_shared_f32(const eat_params_t& p, int32_t T, const float* x, const float* ws1,

@@ -74,11 +74,15 @@ __global__ __launch_bounds__(256) void ffn_down_f32(F32Args a) {
     }
 }
 
-hipError_t launch_f32_pair(F32Args a, int64_t rows_cap, hipStream_t s) {
+hipError_t launch_f32_pair(F32Args a, int64_t rows_cap, hipStream_t s,
+                           const std::function<void()>& between) {
     const int64_t up = rows_cap * a.F, dn = rows_cap * a.d;
     const int gu = static_cast<int>(std::min<int64_t>((up + 255) / 256, 8192));
     const int gd = static_cast<int>(std::min<int64_t>((dn + 255) / 256, 8192));
     if (gu > 0) ffn_up_f32<<<gu, 256, 0, s>>>(a);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    if (between) between();
     if (gd > 0) ffn_down_f32<<<gd, 256, 0, s>>>(a);
     return hipGetLastError();
 }
@@ -102,16 +106,32 @@ __device__ __forceinline__ bf16x8 ld16(const uint16_t* p) {
     return *reinterpret_cast<const bf16x8*>(p);
 }
 
-template <bool GATED, int NSUB>
+// One workgroup = 4 waves = 64 consecutive weight rows (16 per wave) of one
+// expert, applied to one tile of up to 16*NSUB of that expert's tokens.
+// The reduction dimension is walked in chunks of 32*KS:
+//   * the tile's token rows for the next chunk are fetched into registers
+//     and parked in the other half of a double-buffered LDS slab;
+//   * the wave's weight fragments for the next chunk are fetched into a
+//     second register set;
+// both while the MFMAs of the current chunk run, so every wave keeps
+// 16*KS*(GATED ? 2 : 1) bytes per lane of weights in flight.
+// Token sub-tiles beyond the tile's row count are skipped (uniform branch),
+// so a tile of 1 token costs one MFMA per k-step and matrix.
+template <bool GATED, int NSUB, int KS>
 __global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
     constexpr int BN = 16 * NSUB;
+    constexpr int KC = 32 * KS;
+    constexpr int LDS_ROW = KC + 8;                   // +16 B per row against bank conflicts
+    constexpr int VPR = KC / 8;                       // 16-byte vectors per token row per chunk
+    constexpr int RMAX = (BN * VPR + 255) / 256;      // vectors per thread per chunk
+    __shared__ __attribute__((aligned(16))) uint16_t xs[2][BN * LDS_ROW];
     __shared__ int tstart[65];
-    const int lane = lane_id(), wave = threadIdx.x / kWave;
+    const int tid = threadIdx.x;
+    const int lane = lane_id(), wave = tid / kWave;
 
-    // per-group first tile index (prefix over ceil(n_e / BN))
     int ntiles;
     if (a.offsets) {
-        if (threadIdx.x == 0) {
+        if (tid == 0) {
             int acc = 0;
             for (int e = 0; e < a.groups; ++e) {
                 tstart[e] = acc;
@@ -128,7 +148,7 @@ __global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
     const int i = lane & 15, g = lane >> 4;
     const int m0 = blockIdx.x * 64 + wave * 16;
     const int kbeg = blockIdx.z * a.ksplit;
-    const int kend = kbeg + a.ksplit;
+    const int nch = a.ksplit / KC;
 
     for (int tile = blockIdx.y; tile < ntiles; tile += gridDim.y) {
         int e = 0, r0, n;
@@ -140,58 +160,94 @@ __global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
             r0 = tile * BN;
             n = min(BN, a.nrows - r0);
         }
+        const int nsub = (n + 15) >> 4;
         const size_t wrow = (static_cast<size_t>(e) * a.M + m0 + i) * a.K + 8 * g;
         const uint16_t* pa = a.wa + wrow;
         const uint16_t* pb = GATED ? a.wb + wrow : nullptr;
-        const uint16_t* px[NSUB];
-        bool xok[NSUB];
+
+        // token-row vectors this thread moves into LDS each chunk
+        const uint16_t* xsrc[RMAX];
+        int xdst[RMAX];
+        bool xon[RMAX];
 #pragma unroll
-        for (int s = 0; s < NSUB; ++s) {
-            const int c = s * 16 + i;
-            xok[s] = c < n;
-            const int srow = xok[s] ? (a.gather ? a.gather[r0 + c] : r0 + c) : 0;
-            px[s] = a.src + static_cast<size_t>(srow) * a.K + 8 * g;
+        for (int r = 0; r < RMAX; ++r) {
+            const int v = tid + 256 * r;
+            const int row = v / VPR, col = v % VPR;
+            xon[r] = row < n;
+            const int srow = xon[r] ? (a.gather ? a.gather[r0 + row] : r0 + row) : 0;
+            xsrc[r] = a.src + static_cast<size_t>(srow) * a.K + kbeg + 8 * col;
+            xdst[r] = row * LDS_ROW + 8 * col;
         }
+        uint4 xr[RMAX];
+        auto load_x = [&](int c) {
+#pragma unroll
+            for (int r = 0; r < RMAX; ++r)
+                if (xon[r]) xr[r] = *reinterpret_cast<const uint4*>(xsrc[r] + c * KC);
+        };
+        auto store_x = [&](int buf) {
+#pragma unroll
+            for (int r = 0; r < RMAX; ++r)
+                if (xon[r]) *reinterpret_cast<uint4*>(&xs[buf][xdst[r]]) = xr[r];
+        };
+        auto load_w = [&](int c, bf16x8 (&A)[KS], bf16x8 (&B)[KS]) {
+            const int k = kbeg + c * KC;
+#pragma unroll
+            for (int j = 0; j < KS; ++j) {
+                A[j] = ld16(pa + k + 32 * j);
+                if constexpr (GATED) B[j] = ld16(pb + k + 32 * j);
+            }
+        };
+
         f32x4 acc_a[NSUB], acc_b[NSUB];
 #pragma unroll
         for (int s = 0; s < NSUB; ++s) {
             acc_a[s] = f32x4{0.f, 0.f, 0.f, 0.f};
             acc_b[s] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        const bf16x8 zero = {};
-        // groups of U k-steps: all loads of a group are issued before its MFMAs
-        constexpr int U = NSUB >= 4 ? 4 : 8;
-        int k = kbeg;
-        for (; k + 32 * U <= kend; k += 32 * U) {
-            bf16x8 A[U], B[U], X[U][NSUB];
+        auto compute = [&](int buf, const bf16x8 (&A)[KS], const bf16x8 (&B)[KS]) {
+            const uint16_t* xb = xs[buf];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                A[u] = ld16(pa + k + 32 * u);
-                if constexpr (GATED) B[u] = ld16(pb + k + 32 * u);
-#pragma unroll
-                for (int s = 0; s < NSUB; ++s) X[u][s] = xok[s] ? ld16(px[s] + k + 32 * u) : zero;
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u)
+            for (int j = 0; j < KS; ++j) {
 #pragma unroll
                 for (int s = 0; s < NSUB; ++s) {
-                    acc_a[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[u], X[u][s], acc_a[s], 0, 0, 0);
-                    if constexpr (GATED)
-                        acc_b[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(B[u], X[u][s], acc_b[s], 0, 0, 0);
+                    if (s < nsub) {
+                        const bf16x8 X = *reinterpret_cast<const bf16x8*>(xb + (s * 16 + i) * LDS_ROW + 32 * j + 8 * g);
+                        acc_a[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[j], X, acc_a[s], 0, 0, 0);
+                        if constexpr (GATED)
+                            acc_b[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(B[j], X, acc_b[s], 0, 0, 0);
+                    }
                 }
-        }
-        for (; k < kend; k += 32) {
-            const bf16x8 A = ld16(pa + k);
-            bf16x8 B;
-            if constexpr (GATED) B = ld16(pb + k);
-#pragma unroll
-            for (int s = 0; s < NSUB; ++s) {
-                const bf16x8 X = xok[s] ? ld16(px[s] + k) : zero;
-                acc_a[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, X, acc_a[s], 0, 0, 0);
-                if constexpr (GATED)
-                    acc_b[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(B, X, acc_b[s], 0, 0, 0);
             }
+        };
+
+        // Two register sets in ping-pong: while the MFMAs consume one chunk's
+        // weights, the next chunk's are in flight in the other set (no
+        // register copies, so the loads are not waited for early).
+        bf16x8 A0[KS], B0[KS], A1[KS], B1[KS];
+        load_x(0);
+        load_w(0, A0, B0);
+        store_x(0);
+        lds_barrier();
+        for (int c = 0; c < nch; c += 2) {
+            const bool has1 = c + 1 < nch;
+            if (has1) {
+                load_x(c + 1);
+                load_w(c + 1, A1, B1);
+            }
+            compute(0, A0, B0);
+            if (has1) store_x(1);
+            lds_barrier();
+            if (!has1) break;
+            const bool has2 = c + 2 < nch;
+            if (has2) {
+                load_x(c + 2);
+                load_w(c + 2, A0, B0);
+            }
+            compute(1, A1, B1);
+            if (has2) store_x(0);
+            lds_barrier();
         }
+
         // result: lane holds weight rows m0 + 4g + q (q < 4) for token column s*16 + i
 #pragma unroll
         for (int s = 0; s < NSUB; ++s) {
@@ -215,33 +271,92 @@ __global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
     }
 }
 
+// Largest chunk (in 32-wide k-steps) that divides the reduction slice.
+static int pick_ks(int ksplit) {
+    for (int ks : {8, 4, 2, 1})
+        if (ksplit % (32 * ks) == 0) return ks;
+    return 1;
+}
+
+// Chunk depth (k-steps of 32) per variant.  Each wave keeps one chunk of
+// weight fragments in flight, so the bytes in flight per CU are about
+// waves/SIMD x 4 x KS x 1 KB (x2 when gated); the table maximises that
+// product for the register and LDS footprint of each variant, spill-free.
+#ifndef EAT_KS_G1
+#define EAT_KS_G1 4
+#endif
+#ifndef EAT_KS_G2
+#define EAT_KS_G2 4
+#endif
+#ifndef EAT_KS_G4
+#define EAT_KS_G4 4
+#endif
+#ifndef EAT_KS_P1
+#define EAT_KS_P1 8
+#endif
+#ifndef EAT_KS_P2
+#define EAT_KS_P2 8
+#endif
+#ifndef EAT_KS_P4
+#define EAT_KS_P4 4
+#endif
+template <bool GATED, int NSUB>
+constexpr int max_ks() {
+    if (GATED) return NSUB >= 8 ? 1 : NSUB >= 4 ? EAT_KS_G4 : NSUB >= 2 ? EAT_KS_G2 : EAT_KS_G1;
+    return NSUB >= 8 ? 2 : NSUB >= 4 ? EAT_KS_P4 : NSUB >= 2 ? EAT_KS_P2 : EAT_KS_P1;
+}
+
+template <bool GATED, int NSUB, int KS>
+hipError_t launch_stream_k(const StreamArgs& a, dim3 grid, hipStream_t s) {
+    if constexpr (KS <= max_ks<GATED, NSUB>()) {
+        stream_kernel<GATED, NSUB, KS><<<grid, dim3(256), 0, s>>>(a);
+        return hipGetLastError();
+    } else {
+        return hipErrorInvalidValue;
+    }
+}
+
+template <bool GATED, int NSUB>
+hipError_t launch_stream_n(const StreamArgs& a, int tiles_y, int splits, hipStream_t s) {
+    const dim3 grid(a.M / 64, tiles_y, splits);
+    const int ks = std::min(pick_ks(a.ksplit), max_ks<GATED, NSUB>());
+    switch (ks) {
+        case 8: return launch_stream_k<GATED, NSUB, 8>(a, grid, s);
+        case 4: return launch_stream_k<GATED, NSUB, 4>(a, grid, s);
+        case 2: return launch_stream_k<GATED, NSUB, 2>(a, grid, s);
+        default: return launch_stream_k<GATED, NSUB, 1>(a, grid, s);
+    }
+}
+
 template <bool GATED>
 hipError_t launch_stream(const StreamArgs& a, int nsub, int tiles_y, int splits, hipStream_t s) {
-    const dim3 grid(a.M / 64, tiles_y, splits), block(256);
     switch (nsub) {
-        case 1: stream_kernel<GATED, 1><<<grid, block, 0, s>>>(a); break;
-        case 2: stream_kernel<GATED, 2><<<grid, block, 0, s>>>(a); break;
-        default: stream_kernel<GATED, 4><<<grid, block, 0, s>>>(a); break;
+        case 1: return launch_stream_n<GATED, 1>(a, tiles_y, splits, s);
+        case 2: return launch_stream_n<GATED, 2>(a, tiles_y, splits, s);
+        case 4: return launch_stream_n<GATED, 4>(a, tiles_y, splits, s);
+        default: return launch_stream_n<GATED, 8>(a, tiles_y, splits, s);
     }
-    return hipGetLastError();
 }
 
 }  // namespace
 
-// Token sub-tiles per stream tile: enough to cover the expected tokens per
-// expert in one pass over the weights, at most 4 (64 tokens).
-static int pick_nsub(int64_t rows_expected_per_group) {
-    if (rows_expected_per_group <= 16) return 1;
-    if (rows_expected_per_group <= 32) return 2;
-    return 4;
+// Token sub-tiles per stream tile: one tile holds every token an expert
+// can receive in a call of T tokens (at most T), up to 128; beyond that an
+// expert's tokens take several tiles.
+static int pick_nsub(int64_t T) {
+    if (T <= 16) return 1;
+    if (T <= 32) return 2;
+    if (T <= 64) return 4;
+    return 8;
 }
 
 int down_splits(const eat_params_t& p, int32_t T) {
     if (p.expert_dtype != EAT_BF16) return 1;
     // Split the down projection's reduction dimension while the number of
-    // 16-row wave tiles over the likely-active experts is below ~2048.
+    // 16-row wave tiles is below ~2048, counting only K active experts: the
+    // union of a call can be that small (EAT concentrates its picks).
     const int64_t assign = std::max<int64_t>(1, static_cast<int64_t>(T) * p.top_k);
-    const int64_t active = std::min<int64_t>(p.E, assign);
+    const int64_t active = std::min<int64_t>({static_cast<int64_t>(p.E), assign, static_cast<int64_t>(p.top_k)});
     const int64_t waves = static_cast<int64_t>(p.d_model / 16) * active;
     int s = 1;
     while (s < 8 && p.d_ffn % (64 * s) == 0 && waves * s < 2048) s *= 2;
@@ -251,29 +366,29 @@ int down_splits(const eat_params_t& p, int32_t T) {
 hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap, const float* x,
                               const float* w1, const float* w3, const float* w2,
                               const int32_t* offsets, const int32_t* tok_idx,
-                              const int32_t* row_expert, float* h, float* yp, hipStream_t s) {
+                              const int32_t* row_expert, float* h, float* yp, hipStream_t s,
+                              const std::function<void()>& between) {
     F32Args a{x, w1, w3, w2, tok_idx, row_expert, offsets + p.E, 0, p.d_model, p.d_ffn, h, yp};
     (void)T;
-    return launch_f32_pair(a, rows_cap, s);
+    return launch_f32_pair(a, rows_cap, s, between);
 }
 
 hipError_t launch_shared_f32(const eat_params_t& p, int32_t T, const float* x, const float* ws1,
                              const float* ws3, const float* ws2, float* hs, float* ys,
                              hipStream_t s) {
     F32Args a{x, ws1, ws3, ws2, nullptr, nullptr, nullptr, T, p.d_model, p.d_shared, hs, ys};
-    return launch_f32_pair(a, T, s);
+    return launch_f32_pair(a, T, s, nullptr);
 }
 
 hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_cap, const uint16_t* x,
                                const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
                                const int32_t* offsets, const int32_t* tok_idx, uint16_t* h,
-                               float* yp, hipStream_t s) {
-    // Expected rows per active expert: T*K spread over min(E, T*K) experts.
-    const int64_t assign = static_cast<int64_t>(T) * p.top_k;
-    const int64_t active = std::max<int64_t>(1, std::min<int64_t>(p.E, assign));
-    const int nsub = pick_nsub((assign + active - 1) / active);
+                               float* yp, hipStream_t s, const std::function<void()>& between) {
+    const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;
-    const int64_t max_tiles = std::min<int64_t>(rows_cap, (rows_cap + bn - 1) / bn + p.E);
+    // no expert holds more than T rows, so it needs at most ceil(T / bn) tiles
+    const int64_t per_expert = (T + bn - 1) / bn;
+    const int64_t max_tiles = std::min<int64_t>({rows_cap, per_expert * p.E, (rows_cap + bn - 1) / bn + p.E});
     // keep roughly 8 workgroups per CU in flight; extra tiles loop
     const int cap_up = std::max(1, 2048 / std::max(1, p.d_ffn / 64));
     const int tiles_up = static_cast<int>(std::min<int64_t>(max_tiles, cap_up));
@@ -284,6 +399,7 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     up.out = h;
     hipError_t err = launch_stream<true>(up, nsub, tiles_up, 1, s);
     if (err != hipSuccess) return err;
+    if (between) between();
 
     const int splits = down_splits(p, T);
     const int cap_dn = std::max(1, 2048 / std::max(1, (p.d_model / 64) * splits));
@@ -298,7 +414,7 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
 hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* x, const uint16_t* ws1,
                               const uint16_t* ws3, const uint16_t* ws2, uint16_t* hs, float* ys,
                               hipStream_t s) {
-    const int nsub = T <= 16 ? 1 : (T <= 32 ? 2 : 4);
+    const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;
     const int tiles = (T + bn - 1) / bn;
     StreamArgs up{};

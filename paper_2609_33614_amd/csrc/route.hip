@@ -1,11 +1,11 @@
 // Router + EAT selection kernel (gfx950).
 //
-// One workgroup of 4 waves routes a tile of 16 tokens:
+// One workgroup of 16 waves routes a tile of 16 tokens:
 //   1. history score S_h for every expert from the account snapshot
 //      (Sec. 3.2, Eq. 1), in fp64, once per workgroup;
 //   2. router logits for the 16 tokens x E experts with fp32 MFMA
-//      (v_mfma_f32_16x16x4_f32); the four waves split d and their partial
-//      tiles are added in a fixed order;
+//      (v_mfma_f32_16x16x4_f32); the 16 waves take interleaved 16-wide
+//      k-steps of d and their partial tiles are added in wave order;
 //   3. one wave per token, one lane per expert: softmax (Sec. 3.1), then
 //      the mode's selection (EAT: Eq. 2-6 and Sec. 3.3; Top-K; Top-P) and
 //      the renormalisation of Eq. 7-8.
@@ -20,7 +20,7 @@ namespace eat {
 namespace {
 
 constexpr int kTok = 16;            // tokens per workgroup
-constexpr int kWaves = 4;
+constexpr int kWaves = 16;
 
 struct RouteArgs {
     const void* x;
@@ -62,7 +62,7 @@ __device__ __forceinline__ float value_at_rank(float v, int rank, int r, bool va
 }
 
 template <typename XT, int NT>
-__global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
+__global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
     __shared__ float part[kWaves][kTok][NT * 16];
     __shared__ float sh[64];
 
@@ -95,8 +95,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
         const bool row_ok = row < a.T;
         const XT* xrow = x + static_cast<size_t>(row_ok ? row : 0) * a.d;
         const int kq = 4 * (lane >> 4);        // this lane's 4 k values in a 16-k group
-        const int kw = a.d / kWaves;
-        const int kbeg = wave * kw, kend = kbeg + kw;
+        const int nsteps = a.d / 16;            // 16-wide k-steps, dealt round-robin to the waves
         f32x4 acc[NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -108,7 +107,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
             e_ok[nt] = e < E;
             wrow[nt] = a.w_router + static_cast<size_t>(e_ok[nt] ? e : 0) * a.d;
         }
-        auto step = [&](int k, const float (&xv)[4], const float4 (&wv)[NT]) {
+        auto step = [&](const float (&xv)[4], const float4 (&wv)[NT]) {
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
                 acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[0], wv[nt].x, acc[nt], 0, 0, 0);
@@ -125,21 +124,21 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
                 wv[nt] = e_ok[nt] ? *reinterpret_cast<const float4*>(wrow[nt] + k + kq)
                                   : make_float4(0.f, 0.f, 0.f, 0.f);
         };
-        // groups of 4 k-steps (64 k): loads first, then the MFMAs
-        int k = kbeg;
-        for (; k + 64 <= kend; k += 64) {
+        // groups of 4 of this wave's k-steps: loads first, then the MFMAs
+        int st = wave;
+        for (; st + 3 * kWaves < nsteps; st += 4 * kWaves) {
             float xv[4][4];
             float4 wv[4][NT];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) load(k + 16 * u, xv[u], wv[u]);
+            for (int u = 0; u < 4; ++u) load(16 * (st + u * kWaves), xv[u], wv[u]);
 #pragma unroll
-            for (int u = 0; u < 4; ++u) step(k + 16 * u, xv[u], wv[u]);
+            for (int u = 0; u < 4; ++u) step(xv[u], wv[u]);
         }
-        for (; k < kend; k += 16) {
+        for (; st < nsteps; st += kWaves) {
             float xv[4];
             float4 wv[NT];
-            load(k, xv, wv);
-            step(k, xv, wv);
+            load(16 * st, xv, wv);
+            step(xv, wv);
         }
         // result layout: lane holds tokens 4*(lane/16)+i, expert nt*16 + lane%16
 #pragma unroll
@@ -156,8 +155,10 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
         if (t >= a.T) break;
         float z = -INFINITY;
         if (valid) {
-            const float s = ((part[0][tl][lane] + part[1][tl][lane]) + part[2][tl][lane]) + part[3][tl][lane];
-            z = s * a.inv_temp;
+            float sum = 0.f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) sum += part[w][tl][lane];
+            z = sum * a.inv_temp;
         }
         const float zmax = wave_max(z);
         const float ez = valid ? expf(z - zmax) : 0.f;
@@ -257,6 +258,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
 template <typename XT>
 hipError_t launch_route_t(const RouteArgs& a, hipStream_t s) {
     const dim3 grid((a.T + kTok - 1) / kTok), block(kWaves * kWave);
+    static_assert(kTok == kWaves, "one selection wave per token of the tile");
     const int nt = (a.E + 15) / 16;
     switch (nt) {
         case 1: route_kernel<XT, 1><<<grid, block, 0, s>>>(a); break;

@@ -53,15 +53,18 @@ class EatLayer:
     # calls ---------------------------------------------------------------
     def forward(self, x: torch.Tensor, trend: Optional[torch.Tensor] = None, y: Optional[torch.Tensor] = None,
                 mask_out: Optional[torch.Tensor] = None, load_out: Optional[torch.Tensor] = None,
-                stream=None) -> torch.Tensor:
+                stream=None, events=None) -> torch.Tensor:
         T = x.shape[0]
         if y is None:
             y = torch.empty_like(x)
         ws = self.workspace(T)
         w = self.w
-        L.eat_moe_forward(self.handle, x, T, w["w_router"], w["w1"], w["w3"], w["w2"],
-                          w.get("ws1"), w.get("ws3"), w.get("ws2"), self.acc, trend, y, mask_out,
-                          load_out, ws, ws.numel(), stream)
+        args = (self.handle, x, T, w["w_router"], w["w1"], w["w3"], w["w2"], w.get("ws1"), w.get("ws3"),
+                w.get("ws2"), self.acc, trend, y, mask_out, load_out, ws, ws.numel(), stream)
+        if events is None:
+            L.eat_moe_forward(*args)
+        else:
+            L.eat_moe_forward_profiled(*args, events=events)
         return y
 
     def route(self, x: torch.Tensor, trend: Optional[torch.Tensor] = None, stream=None):
