@@ -185,6 +185,10 @@ def main(argv=None) -> int:
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--modes", default="eat,topk,topp", help="routing modes to time (eat first)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="also run 4 plain device copies of MIB MiB (a known-size kernel for "
+                         "calibrating HBM byte counters)")
     args = ap.parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -211,8 +215,21 @@ def main(argv=None) -> int:
     xs = torch.from_numpy(xs_host).view(torch.bfloat16).cuda()
     ev = HipEvents()
 
+    if args.calibrate_copy:
+        n = args.calibrate_copy * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"copy calibration: 4 x {args.calibrate_copy} MiB read + written")
+
     results = {}
-    for name in ("eat", "topk", "topp"):
+    modes = [m for m in args.modes.split(",") if m]
+    assert modes and modes[0] == "eat", "the headline mode (eat) is timed first"
+    for name in modes:
         log(f"timing {name}: {K} steps (+{W} warm-up)")
         results[name] = run_mode(L.MODES[name], shape, wdev, xs, B, K, W, ev, profile=True)
     r = results["eat"]

@@ -56,6 +56,7 @@ Workspace plan_workspace(const eat_ctx& c, int32_t T) {
     const size_t es = p.expert_dtype == EAT_BF16 ? 2 : 4;
     w.rows = static_cast<int64_t>(T) * c.kmax;
     w.splits = down_splits(p, T);
+    w.up_splits = up_splits(p, T);
     const size_t rows = static_cast<size_t>(w.rows);
     size_t off = 0;
     auto take = [&](size_t bytes) { const size_t at = off; off += align256(bytes); return at; };
@@ -68,6 +69,7 @@ Workspace plan_workspace(const eat_ctx& c, int32_t T) {
     w.inv = take(t * E * 4);
     w.row_expert = take(rows * 4);
     w.h = take(rows * p.d_ffn * es);
+    w.gu = take(w.up_splits > 1 ? 2 * static_cast<size_t>(w.up_splits) * rows * p.d_ffn * 4 : 0);
     w.yp = take(static_cast<size_t>(w.splits) * rows * p.d_model * 4);
     w.nrm = take(rows * 4);
     w.hs = take(p.d_shared ? t * p.d_shared * es : 0);
@@ -207,6 +209,7 @@ eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, 
     b.inv = reinterpret_cast<int32_t*>(base + w.inv);
     b.row_expert = reinterpret_cast<int32_t*>(base + w.row_expert);
     b.h = base + w.h;
+    b.gu = reinterpret_cast<float*>(base + w.gu);
     b.yp = reinterpret_cast<float*>(base + w.yp);
     b.nrm = reinterpret_cast<float*>(base + w.nrm);
     b.hs = base + w.hs;
@@ -230,7 +233,7 @@ eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, 
             e = eat::launch_experts_bf16(p, T, w.rows, static_cast<const uint16_t*>(x),
                                          static_cast<const uint16_t*>(w1), static_cast<const uint16_t*>(w3),
                                          static_cast<const uint16_t*>(w2), b.offsets, b.tok_idx,
-                                         static_cast<uint16_t*>(b.h), b.yp, stream,
+                                         static_cast<uint16_t*>(b.h), b.gu, b.yp, stream,
                                          [&]() { mark(EAT_STAGE_UP); });
         else
             e = eat::launch_experts_f32(p, T, w.rows, static_cast<const float*>(x),

@@ -20,10 +20,11 @@ namespace eat {
 // Offsets (bytes) of the workspace regions for T tokens.  Every region
 // starts on a 256-byte boundary.
 struct Workspace {
-    size_t prob, gate, mask, k, offsets, tok_idx, inv, row_expert, h, yp, nrm, hs, ys;
+    size_t prob, gate, mask, k, offsets, tok_idx, inv, row_expert, h, gu, yp, nrm, hs, ys;
     size_t total;
     int64_t rows;            // capacity in (token, expert) rows = T * kmax
     int splits;              // down-projection slices held in yp
+    int up_splits;           // up/gate slices held in gu (1: gu unused)
 };
 Workspace plan_workspace(const eat_ctx& c, int32_t T);
 
@@ -38,6 +39,7 @@ struct Buffers {
     int32_t* inv;            // [T][E] row of (t, e), valid where selected
     int32_t* row_expert;     // [rows] expert of each row
     void* h;                 // [rows][F] SwiGLU hidden (bf16 or fp32)
+    float* gu;               // [2][up_splits][rows][F] gate / up partial sums
     float* yp;               // [splits][rows][d] un-gated expert outputs (partials)
     float* nrm;              // [rows] ||yp row||_2
     void* hs;                // [T][F_sh] shared-expert hidden
@@ -69,7 +71,7 @@ hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap
 hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_cap,
                                const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
                                const uint16_t* w2, const int32_t* offsets, const int32_t* tok_idx,
-                               uint16_t* h, float* yp, hipStream_t s,
+                               uint16_t* h, float* gu, float* yp, hipStream_t s,
                                const std::function<void()>& between);
 
 // Always-on shared expert over all T tokens.
@@ -90,6 +92,9 @@ hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask
 // Number of reduction-dimension slices the bf16 down projection uses for T
 // tokens (1 for fp32 layers).
 int down_splits(const eat_params_t& p, int32_t T);
+// Slices of the bf16 up/gate projection; above 1 the gate and up sums go
+// through fp32 partial buffers (workspace region gu) and a reduce kernel.
+int up_splits(const eat_params_t& p, int32_t T);
 
 hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets,
                                   const int32_t* tok_idx, const float* prob, const float* nrm,

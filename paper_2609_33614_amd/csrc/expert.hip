@@ -98,8 +98,11 @@ struct StreamArgs {
     int nrows;                 // rows of the single group when offsets is null
     int groups, M, K;
     int ksplit;                // reduction length per gridDim.z slice
-    int64_t split_stride;      // elements between split slices of out
-    void* out;                 // gated: bf16 [rows][M]; plain: fp32 [split][rows][M]
+    int64_t split_stride;      // elements between split slices of out / out2
+    void* out;                 // gated: bf16 H [rows][M], or fp32 G partials
+                               // [split][rows][M] when `partial`; plain: fp32 [split][rows][M]
+    float* out2;               // gated + partial: fp32 U partials [split][rows][M]
+    int partial;               // gated: write G/U partial sums instead of H
 };
 
 __device__ __forceinline__ bf16x8 ld16(const uint16_t* p) {
@@ -178,18 +181,21 @@ __global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
             xsrc[r] = a.src + static_cast<size_t>(srow) * a.K + kbeg + 8 * col;
             xdst[r] = row * LDS_ROW + 8 * col;
         }
-        uint4 xr[RMAX];
-        auto load_x = [&](int c) {
+        // Every lane loads (rows past the tile read a valid row and are not
+        // stored), so xr stays in registers instead of private memory.
+        // (native vector type: HIP's uint4 struct would be copied with
+        // memcpy and kept in private memory)
+        bf16x8 xr[RMAX];
+        auto load_x = [&](int c) __attribute__((always_inline)) {
+#pragma unroll
+            for (int r = 0; r < RMAX; ++r) xr[r] = ld16(xsrc[r] + c * KC);
+        };
+        auto store_x = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
             for (int r = 0; r < RMAX; ++r)
-                if (xon[r]) xr[r] = *reinterpret_cast<const uint4*>(xsrc[r] + c * KC);
+                if (xon[r]) *reinterpret_cast<bf16x8*>(&xs[buf][xdst[r]]) = xr[r];
         };
-        auto store_x = [&](int buf) {
-#pragma unroll
-            for (int r = 0; r < RMAX; ++r)
-                if (xon[r]) *reinterpret_cast<uint4*>(&xs[buf][xdst[r]]) = xr[r];
-        };
-        auto load_w = [&](int c, bf16x8 (&A)[KS], bf16x8 (&B)[KS]) {
+        auto load_w = [&](int c, bf16x8 (&A)[KS], bf16x8 (&B)[KS]) __attribute__((always_inline)) {
             const int k = kbeg + c * KC;
 #pragma unroll
             for (int j = 0; j < KS; ++j) {
@@ -204,7 +210,7 @@ __global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
             acc_a[s] = f32x4{0.f, 0.f, 0.f, 0.f};
             acc_b[s] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        auto compute = [&](int buf, const bf16x8 (&A)[KS], const bf16x8 (&B)[KS]) {
+        auto compute = [&](int buf, const bf16x8 (&A)[KS], const bf16x8 (&B)[KS]) __attribute__((always_inline)) {
             const uint16_t* xb = xs[buf];
 #pragma unroll
             for (int j = 0; j < KS; ++j) {
@@ -254,7 +260,13 @@ __global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
             const int c = s * 16 + i;
             if (c >= n) continue;
             const size_t o = static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g;
-            if constexpr (GATED) {
+            if (GATED && a.partial) {
+                const size_t po = blockIdx.z * a.split_stride + o;
+                *reinterpret_cast<float4*>(static_cast<float*>(a.out) + po) =
+                    make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
+                *reinterpret_cast<float4*>(a.out2 + po) =
+                    make_float4(acc_b[s][0], acc_b[s][1], acc_b[s][2], acc_b[s][3]);
+            } else if constexpr (GATED) {
                 uint16_t hv[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) hv[q] = f32_to_bf16(silu(acc_a[s][q]) * acc_b[s][q]);
@@ -268,6 +280,34 @@ __global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
                     make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
             }
         }
+    }
+}
+
+// H[r][f] = bf16(silu(sum_s G[s][r][f]) * sum_s U[s][r][f]) over the rows
+// in use (offsets[groups] of them), slices added in slice order.
+__global__ __launch_bounds__(256) void swiglu_reduce_kernel(const float* __restrict__ gp,
+                                                            const float* __restrict__ up,
+                                                            const int32_t* __restrict__ rows_dev, int M,
+                                                            int splits, int64_t split_stride,
+                                                            uint16_t* __restrict__ h) {
+    const int64_t total = static_cast<int64_t>(*rows_dev) * (M / 4);
+    for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < total;
+         v += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t o = 4 * v;
+        float4 gs = *reinterpret_cast<const float4*>(gp + o);
+        float4 us = *reinterpret_cast<const float4*>(up + o);
+        for (int sp = 1; sp < splits; ++sp) {
+            const float4 ga = *reinterpret_cast<const float4*>(gp + sp * split_stride + o);
+            const float4 ua = *reinterpret_cast<const float4*>(up + sp * split_stride + o);
+            gs.x += ga.x; gs.y += ga.y; gs.z += ga.z; gs.w += ga.w;
+            us.x += ua.x; us.y += ua.y; us.z += ua.z; us.w += ua.w;
+        }
+        uint2 pk;
+        pk.x = static_cast<uint32_t>(f32_to_bf16(silu(gs.x) * us.x)) |
+               (static_cast<uint32_t>(f32_to_bf16(silu(gs.y) * us.y)) << 16);
+        pk.y = static_cast<uint32_t>(f32_to_bf16(silu(gs.z) * us.z)) |
+               (static_cast<uint32_t>(f32_to_bf16(silu(gs.w) * us.w)) << 16);
+        *reinterpret_cast<uint2*>(h + o) = pk;
     }
 }
 
@@ -350,17 +390,44 @@ static int pick_nsub(int64_t T) {
     return 8;
 }
 
-int down_splits(const eat_params_t& p, int32_t T) {
-    if (p.expert_dtype != EAT_BF16) return 1;
-    // Split the down projection's reduction dimension while the number of
-    // 16-row wave tiles is below ~2048, counting only K active experts: the
-    // union of a call can be that small (EAT concentrates its picks).
+// Reduction-dimension slices of a stream launch: double them while the
+// number of 16-row wave tiles over the experts a call may be left with is
+// below EAT_SPLIT_WAVES.  Only K experts are counted (the union of a call
+// can be that small: EAT concentrates its picks), so short launches still
+// spread over the whole chip and end without a long tail.
+#ifndef EAT_SPLIT_WAVES
+#define EAT_SPLIT_WAVES 4096
+#endif
+// The gated projection pays for its slices with fp32 partials and a reduce
+// pass, so it only splits grids that would leave most of the chip idle.
+#ifndef EAT_UP_SPLIT_WAVES
+#define EAT_UP_SPLIT_WAVES 1024
+#endif
+#ifndef EAT_UP_SPLIT_MAX
+#define EAT_UP_SPLIT_MAX 4
+#endif
+static int pick_nsub(int64_t T);
+
+static int stream_splits(int64_t rows_m, int kdim, const eat_params_t& p, int32_t T, int max_splits,
+                         int64_t threshold) {
     const int64_t assign = std::max<int64_t>(1, static_cast<int64_t>(T) * p.top_k);
     const int64_t active = std::min<int64_t>({static_cast<int64_t>(p.E), assign, static_cast<int64_t>(p.top_k)});
-    const int64_t waves = static_cast<int64_t>(p.d_model / 16) * active;
+    const int64_t bn = 16 * pick_nsub(T);
+    const int64_t tiles = std::max<int64_t>(active, (assign + bn - 1) / bn);
+    const int64_t waves = (rows_m / 16) * tiles;
     int s = 1;
-    while (s < 8 && p.d_ffn % (64 * s) == 0 && waves * s < 2048) s *= 2;
+    while (s < max_splits && kdim % (64 * s) == 0 && waves * s < threshold) s *= 2;
     return s;
+}
+
+int down_splits(const eat_params_t& p, int32_t T) {
+    if (p.expert_dtype != EAT_BF16) return 1;
+    return stream_splits(p.d_model, p.d_ffn, p, T, 8, EAT_SPLIT_WAVES);
+}
+
+int up_splits(const eat_params_t& p, int32_t T) {
+    if (p.expert_dtype != EAT_BF16) return 1;
+    return stream_splits(p.d_ffn, p.d_model, p, T, EAT_UP_SPLIT_MAX, EAT_UP_SPLIT_WAVES);
 }
 
 hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap, const float* x,
@@ -383,7 +450,7 @@ hipError_t launch_shared_f32(const eat_params_t& p, int32_t T, const float* x, c
 hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_cap, const uint16_t* x,
                                const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
                                const int32_t* offsets, const int32_t* tok_idx, uint16_t* h,
-                               float* yp, hipStream_t s, const std::function<void()>& between) {
+                               float* gu, float* yp, hipStream_t s, const std::function<void()>& between) {
     const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;
     // no expert holds more than T rows, so it needs at most ceil(T / bn) tiles
@@ -393,12 +460,23 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     const int cap_up = std::max(1, 2048 / std::max(1, p.d_ffn / 64));
     const int tiles_up = static_cast<int>(std::min<int64_t>(max_tiles, cap_up));
 
+    const int usplits = up_splits(p, T);
     StreamArgs up{};
     up.wa = w1; up.wb = w3; up.src = x; up.gather = tok_idx; up.offsets = offsets;
-    up.groups = p.E; up.M = p.d_ffn; up.K = p.d_model; up.ksplit = p.d_model; up.split_stride = 0;
-    up.out = h;
-    hipError_t err = launch_stream<true>(up, nsub, tiles_up, 1, s);
+    up.groups = p.E; up.M = p.d_ffn; up.K = p.d_model; up.ksplit = p.d_model / usplits;
+    up.split_stride = rows_cap * p.d_ffn;
+    up.partial = usplits > 1;
+    up.out = up.partial ? static_cast<void*>(gu) : static_cast<void*>(h);
+    up.out2 = up.partial ? gu + usplits * up.split_stride : nullptr;
+    hipError_t err = launch_stream<true>(up, nsub, tiles_up, usplits, s);
     if (err != hipSuccess) return err;
+    if (up.partial) {
+        const int64_t vec = rows_cap * (p.d_ffn / 4);
+        const int grid = static_cast<int>(std::min<int64_t>((vec + 255) / 256, 4096));
+        swiglu_reduce_kernel<<<grid, 256, 0, s>>>(gu, up.out2, offsets + p.E, p.d_ffn, usplits, up.split_stride, h);
+        err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
     if (between) between();
 
     const int splits = down_splits(p, T);

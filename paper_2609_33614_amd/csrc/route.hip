@@ -107,7 +107,7 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
             e_ok[nt] = e < E;
             wrow[nt] = a.w_router + static_cast<size_t>(e_ok[nt] ? e : 0) * a.d;
         }
-        auto step = [&](const float (&xv)[4], const float4 (&wv)[NT]) {
+        auto step = [&](const float (&xv)[4], const float4 (&wv)[NT]) __attribute__((always_inline)) {
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
                 acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[0], wv[nt].x, acc[nt], 0, 0, 0);
@@ -116,7 +116,7 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
                 acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[3], wv[nt].w, acc[nt], 0, 0, 0);
             }
         };
-        auto load = [&](int k, float (&xv)[4], float4 (&wv)[NT]) {
+        auto load = [&](int k, float (&xv)[4], float4 (&wv)[NT]) __attribute__((always_inline)) {
             xv[0] = xv[1] = xv[2] = xv[3] = 0.f;
             if (row_ok) load_x4<XT>(xrow, k + kq, xv);
 #pragma unroll
