@@ -151,6 +151,21 @@ def traffic_down(shape, k_row, U):
     return U * d * F * 2 + k_row.sum() * F * 2 + k_row.sum() * d * 4
 
 
+def measured_traffic(name: str):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary profiles/<name>.traffic.txt, or None when it is missing or was
+    measured on a different version of the expert kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", name + ".traffic.txt")
+    src = os.path.join(ROOT, "paper_2609_33614_amd", "csrc", "expert.hip")
+    if not os.path.exists(path):
+        return None
+    kv = dict(line.split(": ", 1) for line in open(path).read().splitlines() if ": " in line)
+    if kv.get("source_sha1") != hashlib.sha1(open(src, "rb").read()).hexdigest():
+        return None
+    return float(kv["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(shape, w_host, xs_host, B, max_seconds: float):
     """The oracle, unchanged, on the first steps of the same EAT workload."""
     import oracle as O
@@ -288,7 +303,9 @@ def main(argv=None) -> int:
                    "batch": B, "logit_scale": shape.inv_temp, "router": "fp32", "experts_dtype": "bf16"},
         "roofline": {"bound": "hbm", "kernel": "expert up/gate (stream_kernel<gated>)",
                      "achieved": round(up_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(up_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(up_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("up_gate_mixtral_decode_b64_eat")
+                     if (B == 64 and K == 256 and W == 16) else None,
                      "down_achieved": round(dn_gbs, 1),
                      "bytes_per_launch": round(float(up_bytes.mean()), 0),
                      "us_per_launch": round(float(r["up_ms"].mean() * 1e3), 2)},

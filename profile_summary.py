@@ -1,0 +1,127 @@
+#!/usr/bin/env python3
+"""Summarise rocprofv3 output of bench.py into profiles/.
+
+Inputs (directories written by the commands below, CSV output format):
+  TRACE   rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run --
+              python3 bench.py --no-sweep --no-cpu-baseline --modes eat
+  FETCH   rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH -o run --
+              python3 bench.py --no-sweep --no-cpu-baseline --modes eat --calibrate-copy 1024
+  WRITE   the same with --pmc WRITE_SIZE
+
+Writes profiles/<name>.md (kernel table, the dominant kernel's per-launch
+duration and HBM traffic) and profiles/<name>.traffic.txt (key: value lines
+that bench.py reads for roofline.traffic, with the SHA-1 of the expert
+kernel source they were measured on).
+
+    python profile_summary.py --trace T --fetch F --write W --bench-json B.json --name NAME
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+import statistics
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_33614_amd", "csrc", "expert.hip")
+DOMINANT = "stream_kernel<true"
+COPY = "__amd_rocclr_copyBuffer"
+
+
+def source_sha1() -> str:
+    return hashlib.sha1(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+
+
+def counter_rows(d):
+    return list(csv.DictReader(open(os.path.join(d, "run_counter_collection.csv"))))
+
+
+def copy_factor(rows, mib: int, expect_bytes: float) -> float:
+    """Bytes a known-size copy really moves / what the counter reports for it."""
+    vals = [float(r["Counter_Value"]) * 1024 for r in rows
+            if COPY in r["Kernel_Name"] and int(r["Grid_Size"]) >= 65536]
+    assert vals, "no calibration copy dispatch found"
+    return expect_bytes / statistics.mean(vals)
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--fetch", required=True)
+    ap.add_argument("--write", required=True)
+    ap.add_argument("--bench-json", required=True, help="JSON line printed by the traced bench run")
+    ap.add_argument("--name", required=True)
+    ap.add_argument("--copy-mib", type=int, default=1024)
+    ap.add_argument("--steps", type=int, default=256)
+    args = ap.parse_args(argv)
+
+    bench = json.loads(open(args.bench_json).read().strip().splitlines()[-1])
+    stats = list(csv.DictReader(open(os.path.join(args.trace, "run_kernel_stats.csv"))))
+    trace = list(csv.DictReader(open(os.path.join(args.trace, "run_kernel_trace.csv"))))
+    dom = [r for r in trace if DOMINANT in r["Kernel_Name"]]
+    dom.sort(key=lambda r: int(r["Start_Timestamp"]))
+    timed = dom[-args.steps:]
+    dur_us = statistics.mean((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in timed)
+
+    # counters: the copy kernel is a (split) 1 GiB read + 1 GiB write in 512 MiB dispatches
+    fetch, write = counter_rows(args.fetch), counter_rows(args.write)
+    copy_disp = [r for r in fetch if COPY in r["Kernel_Name"] and int(r["Grid_Size"]) >= 65536]
+    per_copy = args.copy_mib * (1 << 20) * 4 / len(copy_disp)       # bytes each dispatch moves
+    f_fac = copy_factor(fetch, args.copy_mib, per_copy)
+    w_fac = copy_factor(write, args.copy_mib, per_copy)
+    fd = [float(r["Counter_Value"]) * 1024 * f_fac for r in fetch if DOMINANT in r["Kernel_Name"]][-args.steps:]
+    wd = [float(r["Counter_Value"]) * 1024 * w_fac for r in write if DOMINANT in r["Kernel_Name"]][-args.steps:]
+    fetch_b, write_b = statistics.mean(fd), statistics.mean(wd)
+    alg = bench["roofline"]["bytes_per_launch"]
+    ev_us = bench["roofline"]["us_per_launch"]
+
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    md = os.path.join(ROOT, "profiles", args.name + ".md")
+    with open(md, "w") as f:
+        f.write(f"# {args.name}\n\n")
+        f.write(f"Workload: {bench['config']['workload']}, batch {bench['config']['batch']}, "
+                f"{bench['steps']} timed steps (+{bench['warmup']} warm-up), MI355X.\n\n")
+        f.write("Commands (from the repository root):\n\n```\n")
+        f.write("rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run -- "
+                "python3 bench.py --no-sweep --no-cpu-baseline --modes eat\n")
+        f.write("rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH -o run -- "
+                "python3 bench.py --no-sweep --no-cpu-baseline --modes eat --calibrate-copy 1024\n")
+        f.write("rocprofv3 --pmc WRITE_SIZE --output-format csv -d WRITE -o run -- "
+                "python3 bench.py --no-sweep --no-cpu-baseline --modes eat --calibrate-copy 1024\n")
+        f.write(f"python3 profile_summary.py --trace TRACE --fetch FETCH --write WRITE "
+                f"--bench-json TRACED_BENCH.json --name {args.name}\n```\n\n")
+        f.write("## Kernel time (rocprofv3 --stats, whole traced run incl. warm-up)\n\n")
+        f.write("| kernel | calls | avg us | % time |\n|---|---|---|---|\n")
+        for r in stats[:10]:
+            name = r["Name"].replace("(anonymous namespace)::", "").split("(")[0]
+            f.write(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} |\n")
+        f.write("\n## Dominant kernel: expert up/gate (`stream_kernel<true, ...>`)\n\n")
+        f.write(f"- average duration over the {len(timed)} timed launches (trace): **{dur_us:.2f} us**\n")
+        f.write(f"- average duration measured in bench.py with HIP events (same run): {ev_us:.2f} us\n")
+        f.write(f"- algorithmic bytes per launch (weights of the experts touched + token rows + H): "
+                f"{alg / 1e6:.1f} MB -> {alg / dur_us / 1e3:.1f} GB/s = "
+                f"{alg / dur_us / 1e3 / 8000 * 100:.1f}% of 8 TB/s\n")
+        f.write(f"- HBM traffic per launch (FETCH_SIZE x {f_fac:.3f} + WRITE_SIZE x {w_fac:.3f}, the factors "
+                f"that make a {args.copy_mib} MiB device copy read and write its size): "
+                f"{fetch_b / 1e6:.1f} MB read + {write_b / 1e6:.1f} MB written = "
+                f"{(fetch_b + write_b) / alg:.3f} x algorithmic\n")
+    txt = os.path.join(ROOT, "profiles", args.name + ".traffic.txt")
+    with open(txt, "w") as f:
+        f.write(f"kernel: {DOMINANT}\n")
+        f.write(f"source_sha1: {source_sha1()}\n")
+        f.write(f"steps: {len(timed)}\n")
+        f.write(f"fetch_factor: {f_fac:.6f}\n")
+        f.write(f"write_factor: {w_fac:.6f}\n")
+        f.write(f"fetch_bytes_per_launch: {fetch_b:.0f}\n")
+        f.write(f"write_bytes_per_launch: {write_b:.0f}\n")
+        f.write(f"traffic_bytes_per_launch: {fetch_b + write_b:.0f}\n")
+        f.write(f"algorithmic_bytes_per_launch: {alg:.0f}\n")
+        f.write(f"trace_us_per_launch: {dur_us:.3f}\n")
+    print(open(md).read())
+    return 0
+
+
+if __name__ == "__main__":
+    raise SystemExit(main())
