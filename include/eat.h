@@ -138,6 +138,11 @@ eat_status_t eat_workspace_size(eat_handle_t h, int32_t T, size_t* bytes);
  * in a graph). */
 eat_status_t eat_reset_accounts(eat_handle_t h, eat_accounts_t acc, hipStream_t stream);
 
+/* Bytes of device workspace eat_route needs for T tokens (the partial router
+ * scores of its d slices).  Always <= eat_workspace_size(h, T), so a
+ * forward workspace also serves routing. */
+eat_status_t eat_route_workspace_size(eat_handle_t h, int32_t T, size_t* bytes);
+
 /* Routing only (Sec. 3.1-3.4, no experts, accounts read but not updated).
  *   x          [T][d_model] act_dtype, device
  *   w_router   [E][d_model] fp32, device
@@ -147,7 +152,8 @@ eat_status_t eat_reset_accounts(eat_handle_t h, eat_accounts_t acc, hipStream_t 
  *              token's sequence (tau x ppl_up), anything else tau x ppl_down
  *   mask_out   [T] uint64, k_out [T] int32, gate_out [T][E] fp32: required
  *   prob_out   [T][E] fp32 router probabilities, or NULL
- *   ws         device workspace of at least eat_workspace_size(h, T) bytes
+ *   ws         device workspace of at least eat_route_workspace_size(h, T)
+ *              bytes, 256-byte aligned (EAT_ERR_WORKSPACE otherwise)
  */
 eat_status_t eat_route(eat_handle_t h, const void* x, int32_t T, const float* w_router,
                        eat_accounts_t acc, const int8_t* ppl_trend,

@@ -64,15 +64,18 @@ def load() -> C.CDLL:
     lib.eat_destroy.argtypes = [P]
     lib.eat_workspace_size.argtypes = [P, C.c_int32, C.POINTER(C.c_size_t)]
     lib.eat_reset_accounts.argtypes = [P, eat_accounts_t, P]
+    if hasattr(lib, "eat_route_workspace_size"):
+        lib.eat_route_workspace_size.argtypes = [P, C.c_int32, C.POINTER(C.c_size_t)]
     lib.eat_route.argtypes = [P, P, C.c_int32, P, eat_accounts_t, P, P, P, P, P, P, C.c_size_t, P]
     lib.eat_moe_forward.argtypes = [P, P, C.c_int32, P, P, P, P, P, P, P, eat_accounts_t, P, P, P, P, P,
                                     C.c_size_t, P]
     lib.eat_moe_forward_profiled.argtypes = lib.eat_moe_forward.argtypes + [P, C.c_int32]
     lib.eat_status_string.argtypes = [C.c_int]
     lib.eat_status_string.restype = C.c_char_p
-    for name in ("eat_params_default", "eat_create", "eat_destroy", "eat_workspace_size",
+    for name in ("eat_params_default", "eat_create", "eat_destroy", "eat_workspace_size", "eat_route_workspace_size",
                  "eat_reset_accounts", "eat_route", "eat_moe_forward", "eat_moe_forward_profiled"):
-        getattr(lib, name).restype = st
+        if hasattr(lib, name):
+            getattr(lib, name).restype = st
     _lib = lib
     return lib
 
@@ -135,6 +138,12 @@ def eat_destroy(handle: int) -> None:
 def eat_workspace_size(handle: int, T: int) -> int:
     b = C.c_size_t()
     _check(load().eat_workspace_size(handle, int(T), C.byref(b)), "eat_workspace_size")
+    return b.value
+
+
+def eat_route_workspace_size(handle: int, T: int) -> int:
+    b = C.c_size_t()
+    _check(load().eat_route_workspace_size(handle, int(T), C.byref(b)), "eat_route_workspace_size")
     return b.value
 
 

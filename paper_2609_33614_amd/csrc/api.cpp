@@ -60,6 +60,8 @@ Workspace plan_workspace(const eat_ctx& c, int32_t T) {
     const size_t rows = static_cast<size_t>(w.rows);
     size_t off = 0;
     auto take = [&](size_t bytes) { const size_t at = off; off += align256(bytes); return at; };
+    w.lpart = take(static_cast<size_t>(T > 0 ? route_slices(p, T) : 1) * t * E * 4);
+    w.route_total = off;
     w.prob = take(t * E * 4);
     w.gate = take(t * E * 4);
     w.mask = take(t * 8);
@@ -71,7 +73,7 @@ Workspace plan_workspace(const eat_ctx& c, int32_t T) {
     w.h = take(rows * p.d_ffn * es);
     w.gu = take(w.up_splits > 1 ? 2 * static_cast<size_t>(w.up_splits) * rows * p.d_ffn * 4 : 0);
     w.yp = take(static_cast<size_t>(w.splits) * rows * p.d_model * 4);
-    w.nrm = take(rows * 4);
+    w.nrm = take(rows * static_cast<size_t>(combine_chunks(p)) * 4);
     w.hs = take(p.d_shared ? t * p.d_shared * es : 0);
     w.ys = take(p.d_shared ? t * p.d_model * 4 : 0);
     w.total = off;
@@ -150,12 +152,16 @@ static eat_status_t check_accounts(const eat_ctx& c, const eat_accounts_t& acc) 
     return EAT_OK;
 }
 
+eat_status_t eat_route_workspace_size(eat_handle_t h, int32_t T, size_t* bytes) {
+    if (!h || !bytes || T < 0 || T > h->max_tokens) return EAT_ERR_INVALID_ARG;
+    *bytes = eat::plan_workspace(*h, T).route_total;
+    return EAT_OK;
+}
+
 eat_status_t eat_route(eat_handle_t h, const void* x, int32_t T, const float* w_router,
                        eat_accounts_t acc, const int8_t* ppl_trend, uint64_t* mask_out,
                        int32_t* k_out, float* gate_out, float* prob_out, void* ws, size_t ws_bytes,
                        hipStream_t stream) {
-    (void)ws;
-    (void)ws_bytes;  // routing alone needs no workspace
     if (!h || T < 0 || T > h->max_tokens) return EAT_ERR_INVALID_ARG;
     if (!x || !w_router || !mask_out || !k_out || !gate_out) return EAT_ERR_INVALID_ARG;
     if (!aligned(x, 16) || !aligned(w_router, 16) || !aligned(mask_out, 8) || !aligned(k_out, 4) ||
@@ -163,10 +169,14 @@ eat_status_t eat_route(eat_handle_t h, const void* x, int32_t T, const float* w_
         return EAT_ERR_INVALID_ARG;
     const eat_status_t st = check_accounts(*h, acc);
     if (st != EAT_OK) return st;
+    const eat::Workspace w = eat::plan_workspace(*h, T);
+    if (T > 0 && (!ws || ws_bytes < w.route_total)) return EAT_ERR_WORKSPACE;
+    if (ws && !aligned(ws, 256)) return EAT_ERR_INVALID_ARG;
     if (T == 0) return EAT_OK;
     (void)hipGetLastError();
-    const hipError_t e = eat::launch_route(h->p, x, T, w_router, acc, ppl_trend, mask_out, k_out, gate_out,
-                                           prob_out, stream);
+    const hipError_t e = eat::launch_route(h->p, x, T, w_router, acc, ppl_trend,
+                                           reinterpret_cast<float*>(static_cast<char*>(ws) + w.lpart), mask_out,
+                                           k_out, gate_out, prob_out, stream);
     return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;
 }
 
@@ -200,6 +210,7 @@ eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, 
 
     char* base = static_cast<char*>(ws);
     eat::Buffers b;
+    b.lpart = reinterpret_cast<float*>(base + w.lpart);
     b.prob = reinterpret_cast<float*>(base + w.prob);
     b.gate = reinterpret_cast<float*>(base + w.gate);
     b.mask = mask_out ? mask_out : reinterpret_cast<uint64_t*>(base + w.mask);
@@ -211,7 +222,7 @@ eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, 
     b.h = base + w.h;
     b.gu = reinterpret_cast<float*>(base + w.gu);
     b.yp = reinterpret_cast<float*>(base + w.yp);
-    b.nrm = reinterpret_cast<float*>(base + w.nrm);
+    b.nrm2 = reinterpret_cast<float*>(base + w.nrm);
     b.hs = base + w.hs;
     b.ys = reinterpret_cast<float*>(base + w.ys);
 
@@ -222,7 +233,7 @@ eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, 
     };
     mark(EAT_STAGE_BEGIN);
     if (e == hipSuccess)
-        e = eat::launch_route(p, x, T, w_router, acc, ppl_trend, b.mask, b.k, b.gate, b.prob, stream);
+        e = eat::launch_route(p, x, T, w_router, acc, ppl_trend, b.lpart, b.mask, b.k, b.gate, b.prob, stream);
     mark(EAT_STAGE_ROUTED);
     if (e == hipSuccess)
         e = eat::launch_permute(p, T, b.mask, b.offsets, b.tok_idx, b.inv, b.row_expert, expert_load_out,
@@ -255,11 +266,11 @@ eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, 
     }
     mark(EAT_STAGE_SHARED);
     if (e == hipSuccess)
-        e = eat::launch_combine(p, T, b.mask, b.gate, b.inv, b.yp, shared ? b.ys : nullptr, y, b.nrm, w.splits,
+        e = eat::launch_combine(p, T, b.mask, b.gate, b.inv, b.yp, shared ? b.ys : nullptr, y, b.nrm2, w.splits,
                                 w.rows * p.d_model, stream);
     mark(EAT_STAGE_COMBINED);
     if (e == hipSuccess && p.mode == EAT_MODE_EAT)
-        e = eat::launch_update_accounts(p, b.offsets, b.tok_idx, b.prob, b.nrm, acc, stream);
+        e = eat::launch_update_accounts(p, b.offsets, b.tok_idx, b.prob, b.nrm2, acc, stream);
     mark(EAT_STAGE_END);
     return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;
 }

@@ -20,7 +20,8 @@ namespace eat {
 // Offsets (bytes) of the workspace regions for T tokens.  Every region
 // starts on a 256-byte boundary.
 struct Workspace {
-    size_t prob, gate, mask, k, offsets, tok_idx, inv, row_expert, h, gu, yp, nrm, hs, ys;
+    size_t lpart, prob, gate, mask, k, offsets, tok_idx, inv, row_expert, h, gu, yp, nrm, hs, ys;
+    size_t route_total;      // bytes eat_route needs (the leading lpart region)
     size_t total;
     int64_t rows;            // capacity in (token, expert) rows = T * kmax
     int splits;              // down-projection slices held in yp
@@ -30,6 +31,7 @@ Workspace plan_workspace(const eat_ctx& c, int32_t T);
 
 // Pointers into a workspace for one call.
 struct Buffers {
+    float* lpart;            // [route_slices][T][E] partial router scores
     float* prob;             // [T][E] router probabilities
     float* gate;             // [T][E] renormalised gates
     uint64_t* mask;          // [T]
@@ -41,7 +43,7 @@ struct Buffers {
     void* h;                 // [rows][F] SwiGLU hidden (bf16 or fp32)
     float* gu;               // [2][up_splits][rows][F] gate / up partial sums
     float* yp;               // [splits][rows][d] un-gated expert outputs (partials)
-    float* nrm;              // [rows] ||yp row||_2
+    float* nrm2;             // [rows][combine_chunks] partial sums of squares of yp rows
     void* hs;                // [T][F_sh] shared-expert hidden
     float* ys;               // [T][d] shared-expert output
 };
@@ -50,9 +52,13 @@ struct Buffers {
 
 hipError_t launch_reset_accounts(const eat_params_t& p, eat_accounts_t acc, hipStream_t s);
 
+// Routing: partial router scores per (token tile, d slice) into `part`
+// ([route_slices][T][E] fp32), then one selection wave per token.
 hipError_t launch_route(const eat_params_t& p, const void* x, int32_t T, const float* w_router,
-                        eat_accounts_t acc, const int8_t* trend, uint64_t* mask, int32_t* k,
+                        eat_accounts_t acc, const int8_t* trend, float* part, uint64_t* mask, int32_t* k,
                         float* gate, float* prob, hipStream_t s);
+int route_token_tiles(int32_t T);                  // 16-token MFMA tiles per logits workgroup
+int route_slices(const eat_params_t& p, int32_t T);  // d slices of the logits kernel
 
 hipError_t launch_permute(const eat_params_t& p, int32_t T, const uint64_t* mask,
                           int32_t* offsets, int32_t* tok_idx, int32_t* inv, int32_t* row_expert,
@@ -86,8 +92,10 @@ hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* 
 // floats apart; they are added in slice order.
 hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask,
                           const float* gate, const int32_t* inv, const float* yp,
-                          const float* ys, void* y, float* nrm, int splits,
+                          const float* ys, void* y, float* nrm2, int splits,
                           int64_t split_stride, hipStream_t s);
+// 1024-element slices of d the combine works in (and nrm2 holds per row).
+int combine_chunks(const eat_params_t& p);
 
 // Number of reduction-dimension slices the bf16 down projection uses for T
 // tokens (1 for fp32 layers).
@@ -97,7 +105,7 @@ int down_splits(const eat_params_t& p, int32_t T);
 int up_splits(const eat_params_t& p, int32_t T);
 
 hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets,
-                                  const int32_t* tok_idx, const float* prob, const float* nrm,
+                                  const int32_t* tok_idx, const float* prob, const float* nrm2,
                                   eat_accounts_t acc, hipStream_t s);
 
 }  // namespace eat

@@ -1,17 +1,23 @@
-// Router + EAT selection kernel (gfx950).
+// Router + EAT selection kernels (gfx950).
 //
-// One workgroup of 16 waves routes a tile of 16 tokens:
-//   1. history score S_h for every expert from the account snapshot
-//      (Sec. 3.2, Eq. 1), in fp64, once per workgroup;
-//   2. router logits for the 16 tokens x E experts with fp32 MFMA
-//      (v_mfma_f32_16x16x4_f32); the 16 waves take interleaved 16-wide
-//      k-steps of d and their partial tiles are added in wave order;
-//   3. one wave per token, one lane per expert: softmax (Sec. 3.1), then
-//      the mode's selection (EAT: Eq. 2-6 and Sec. 3.3; Top-K; Top-P) and
-//      the renormalisation of Eq. 7-8.
+// logits_kernel: one workgroup of 4 waves per (tile of 16*TT tokens,
+// slice of d).  Router scores x W_r^T for the tile's tokens and all E
+// experts over its slice, fp32 MFMA (v_mfma_f32_16x16x4_f32, fp32 router
+// weights); the waves take interleaved 16-wide k-steps of the slice and add
+// their tiles in wave order; the slice's partial scores go to the workspace.
+// Spreading d over many workgroups keeps the router-weight reads (E*d*4
+// bytes per token tile) off a single CU.
+//
+// select_kernel: one wave per token, one lane per expert.  Adds the slice
+// partials in slice order, then softmax (Sec. 3.1) and the mode's selection
+// (EAT: history score S_h from the account snapshot in fp64 (Eq. 1),
+// importance (Eq. 2), threshold (Eq. 3-5, Sec. 3.3), activation set (Eq. 6);
+// Top-K; Top-P) and the renormalisation of Eq. 7-8.
 // All reductions use fixed butterfly or sequential orders, so results are
 // bit-reproducible run to run.
 #include <math.h>
+
+#include <algorithm>
 
 #include "eat_device.h"
 #include "eat_internal.h"
@@ -19,8 +25,7 @@
 namespace eat {
 namespace {
 
-constexpr int kTok = 16;            // tokens per workgroup
-constexpr int kWaves = 16;
+constexpr int kLogitWaves = 4;
 
 struct RouteArgs {
     const void* x;
@@ -29,11 +34,12 @@ struct RouteArgs {
     const float* acc_p;
     const float* acc_c;
     const int8_t* trend;
+    float* part;               // [slices][T][E] partial router scores
     uint64_t* mask;
     int32_t* k;
     float* gate;
     float* prob;
-    int T, d, E, K, mode, cs_mode, top_p_cap;
+    int T, d, E, K, mode, cs_mode, top_p_cap, slices;
     float top_p, w1, w2, w3, beta, alpha1, alpha2, kappa1, kappa2, ppl_up, ppl_down, q_lo, q_hi,
         eps, inv_temp;
 };
@@ -61,17 +67,107 @@ __device__ __forceinline__ float value_at_rank(float v, int rank, int r, bool va
     return read_lane(v, __builtin_ctzll(b));
 }
 
-template <typename XT, int NT>
-__global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
-    __shared__ float part[kWaves][kTok][NT * 16];
-    __shared__ float sh[64];
-
+template <typename XT, int NT, int TT>
+__global__ __launch_bounds__(256) void logits_kernel(RouteArgs a) {
+    __shared__ float red[kLogitWaves][TT * 16][NT * 16];
     const int lane = lane_id();
     const int wave = threadIdx.x / kWave;
-    const int t0 = blockIdx.x * kTok;
+    const int t0 = blockIdx.x * 16 * TT;
+    const int E = a.E;
+    const XT* x = static_cast<const XT*>(a.x);
+    const int kq = 4 * (lane >> 4);          // this lane's 4 k values in a 16-wide k-step
+    const int nsteps = a.d / 16;
+    const int per = nsteps / a.slices;
+    const int sbeg = blockIdx.y * per, send = sbeg + per;
+
+    const XT* xrow[TT];
+    bool row_ok[TT];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+        const int row = t0 + tt * 16 + (lane & 15);
+        row_ok[tt] = row < a.T;
+        xrow[tt] = x + static_cast<size_t>(row_ok[tt] ? row : 0) * a.d;
+    }
+    const float* wrow[NT];
+    bool e_ok[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        const int e = nt * 16 + (lane & 15);
+        e_ok[nt] = e < E;
+        wrow[nt] = a.w_router + static_cast<size_t>(e_ok[nt] ? e : 0) * a.d;
+    }
+    f32x4 acc[TT][NT];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[tt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto load = [&](int k, float (&xv)[TT][4], float4 (&wv)[NT]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt) {
+            xv[tt][0] = xv[tt][1] = xv[tt][2] = xv[tt][3] = 0.f;
+            if (row_ok[tt]) load_x4<XT>(xrow[tt], k + kq, xv[tt]);
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+            wv[nt] = e_ok[nt] ? *reinterpret_cast<const float4*>(wrow[nt] + k + kq) : make_float4(0.f, 0.f, 0.f, 0.f);
+    };
+    auto step = [&](const float (&xv)[TT][4], const float4 (&wv)[NT]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                acc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[tt][0], wv[nt].x, acc[tt][nt], 0, 0, 0);
+                acc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[tt][1], wv[nt].y, acc[tt][nt], 0, 0, 0);
+                acc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[tt][2], wv[nt].z, acc[tt][nt], 0, 0, 0);
+                acc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[tt][3], wv[nt].w, acc[tt][nt], 0, 0, 0);
+            }
+    };
+    // groups of G of this wave's k-steps: all loads of a group, then its MFMAs
+    constexpr int G = TT * NT <= 2 ? 4 : 2;
+    int st = sbeg + wave;
+    for (; st + (G - 1) * kLogitWaves < send; st += G * kLogitWaves) {
+        float xv[G][TT][4];
+        float4 wv[G][NT];
+#pragma unroll
+        for (int u = 0; u < G; ++u) load(16 * (st + u * kLogitWaves), xv[u], wv[u]);
+#pragma unroll
+        for (int u = 0; u < G; ++u) step(xv[u], wv[u]);
+    }
+    for (; st < send; st += kLogitWaves) {
+        float xv[TT][4];
+        float4 wv[NT];
+        load(16 * st, xv, wv);
+        step(xv, wv);
+    }
+    // lane holds tokens tt*16 + 4*(lane/16) + i, expert nt*16 + lane%16
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) red[wave][tt * 16 + 4 * (lane >> 4) + i][nt * 16 + (lane & 15)] = acc[tt][nt][i];
+    __syncthreads();
+    for (int v = threadIdx.x; v < TT * 16 * E; v += 256) {
+        const int tl = v / E, e = v % E;
+        const int t = t0 + tl;
+        if (t >= a.T) continue;
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < kLogitWaves; ++w) sum += red[w][tl][e];
+        a.part[(static_cast<size_t>(blockIdx.y) * a.T + t) * E + e] = sum;
+    }
+}
+
+constexpr int kSelWaves = 4;
+
+__global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
+    __shared__ float sh[64];
+    const int lane = lane_id();
+    const int wave = threadIdx.x / kWave;
     const int E = a.E;
 
-    // ---- 1. history score from the account snapshot (Eq. 1) ----------
+    // ---- history score from the account snapshot (Eq. 1) --------------
     if (a.mode == EAT_MODE_EAT && wave == 0) {
         const bool valid = lane < E;
         const double n = valid ? static_cast<double>(a.acc_n[lane]) : 0.0;
@@ -87,77 +183,28 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
         }
         sh[lane] = static_cast<float>(a.w1 * t1 + a.w2 * t2 + a.w3 * t3);
     }
-
-    // ---- 2. router logits: MFMA 16 tokens x 16 experts x 4 k -----------
-    {
-        const XT* x = static_cast<const XT*>(a.x);
-        const int row = t0 + (lane & 15);
-        const bool row_ok = row < a.T;
-        const XT* xrow = x + static_cast<size_t>(row_ok ? row : 0) * a.d;
-        const int kq = 4 * (lane >> 4);        // this lane's 4 k values in a 16-k group
-        const int nsteps = a.d / 16;            // 16-wide k-steps, dealt round-robin to the waves
-        f32x4 acc[NT];
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        const float* wrow[NT];
-        bool e_ok[NT];
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            const int e = nt * 16 + (lane & 15);
-            e_ok[nt] = e < E;
-            wrow[nt] = a.w_router + static_cast<size_t>(e_ok[nt] ? e : 0) * a.d;
-        }
-        auto step = [&](const float (&xv)[4], const float4 (&wv)[NT]) __attribute__((always_inline)) {
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[0], wv[nt].x, acc[nt], 0, 0, 0);
-                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[1], wv[nt].y, acc[nt], 0, 0, 0);
-                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[2], wv[nt].z, acc[nt], 0, 0, 0);
-                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[3], wv[nt].w, acc[nt], 0, 0, 0);
-            }
-        };
-        auto load = [&](int k, float (&xv)[4], float4 (&wv)[NT]) __attribute__((always_inline)) {
-            xv[0] = xv[1] = xv[2] = xv[3] = 0.f;
-            if (row_ok) load_x4<XT>(xrow, k + kq, xv);
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-                wv[nt] = e_ok[nt] ? *reinterpret_cast<const float4*>(wrow[nt] + k + kq)
-                                  : make_float4(0.f, 0.f, 0.f, 0.f);
-        };
-        // groups of 4 of this wave's k-steps: loads first, then the MFMAs
-        int st = wave;
-        for (; st + 3 * kWaves < nsteps; st += 4 * kWaves) {
-            float xv[4][4];
-            float4 wv[4][NT];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) load(16 * (st + u * kWaves), xv[u], wv[u]);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) step(xv[u], wv[u]);
-        }
-        for (; st < nsteps; st += kWaves) {
-            float xv[4];
-            float4 wv[NT];
-            load(16 * st, xv, wv);
-            step(xv, wv);
-        }
-        // result layout: lane holds tokens 4*(lane/16)+i, expert nt*16 + lane%16
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) part[wave][4 * (lane >> 4) + i][nt * 16 + (lane & 15)] = acc[nt][i];
-    }
     __syncthreads();
 
-    // ---- 3. per-token softmax, selection, renormalisation --------------
+    // ---- per-token softmax, selection, renormalisation ----------------
     const bool valid = lane < E;
-    for (int tl = wave; tl < kTok; tl += kWaves) {
-        const int t = t0 + tl;
-        if (t >= a.T) break;
+    {
+        const int t = blockIdx.x * kSelWaves + wave;
+        if (t >= a.T) return;
         float z = -INFINITY;
         if (valid) {
+            // slices added in slice order; loads issued 8 at a time
+            const float* src = a.part + static_cast<size_t>(t) * E + lane;
+            const size_t stride = static_cast<size_t>(a.T) * E;
             float sum = 0.f;
+            int sl = 0;
+            for (; sl + 8 <= a.slices; sl += 8) {
+                float v[8];
 #pragma unroll
-            for (int w = 0; w < kWaves; ++w) sum += part[w][tl][lane];
+                for (int u = 0; u < 8; ++u) v[u] = src[(sl + u) * stride];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) sum += v[u];
+            }
+            for (; sl < a.slices; ++sl) sum += src[sl * stride];
             z = sum * a.inv_temp;
         }
         const float zmax = wave_max(z);
@@ -255,26 +302,49 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
     }
 }
 
+template <typename XT, int NT>
+hipError_t launch_logits_n(const RouteArgs& a, int tt, dim3 grid, hipStream_t s) {
+    if (tt == 4) logits_kernel<XT, NT, 4><<<grid, 256, 0, s>>>(a);
+    else logits_kernel<XT, NT, 1><<<grid, 256, 0, s>>>(a);
+    return hipGetLastError();
+}
+
 template <typename XT>
 hipError_t launch_route_t(const RouteArgs& a, hipStream_t s) {
-    const dim3 grid((a.T + kTok - 1) / kTok), block(kWaves * kWave);
-    static_assert(kTok == kWaves, "one selection wave per token of the tile");
-    const int nt = (a.E + 15) / 16;
-    switch (nt) {
-        case 1: route_kernel<XT, 1><<<grid, block, 0, s>>>(a); break;
-        case 2: route_kernel<XT, 2><<<grid, block, 0, s>>>(a); break;
-        case 3: route_kernel<XT, 3><<<grid, block, 0, s>>>(a); break;
-        default: route_kernel<XT, 4><<<grid, block, 0, s>>>(a); break;
+    const int tt = route_token_tiles(a.T);
+    const dim3 grid((a.T + 16 * tt - 1) / (16 * tt), a.slices);
+    hipError_t err;
+    switch ((a.E + 15) / 16) {
+        case 1: err = launch_logits_n<XT, 1>(a, tt, grid, s); break;
+        case 2: err = launch_logits_n<XT, 2>(a, tt, grid, s); break;
+        case 3: err = launch_logits_n<XT, 3>(a, tt, grid, s); break;
+        default: err = launch_logits_n<XT, 4>(a, tt, grid, s); break;
     }
+    if (err != hipSuccess) return err;
+    select_kernel<<<(a.T + kSelWaves - 1) / kSelWaves, kSelWaves * kWave, 0, s>>>(a);
     return hipGetLastError();
 }
 
 }  // namespace
 
+int route_token_tiles(int32_t T) { return T >= 1024 ? 4 : 1; }
+
+int route_slices(const eat_params_t& p, int32_t T) {
+    // enough (token tile, d slice) workgroups to spread the router weights
+    // over the chip: about 512, each wave keeping at least one k-step
+    const int tiles = (T + 16 * route_token_tiles(T) - 1) / (16 * route_token_tiles(T));
+    const int nsteps = p.d_model / 16;
+    int sl = 1;
+    while (2 * sl * tiles <= 512 && nsteps % (2 * sl) == 0 && nsteps / (2 * sl) >= kLogitWaves) sl *= 2;
+    return sl;
+}
+
 hipError_t launch_route(const eat_params_t& p, const void* x, int32_t T, const float* w_router,
-                        eat_accounts_t acc, const int8_t* trend, uint64_t* mask, int32_t* k,
+                        eat_accounts_t acc, const int8_t* trend, float* part, uint64_t* mask, int32_t* k,
                         float* gate, float* prob, hipStream_t s) {
     RouteArgs a;
+    a.part = part;
+    a.slices = route_slices(p, T);
     a.x = x; a.w_router = w_router;
     a.acc_n = acc.n; a.acc_p = acc.p_total; a.acc_c = acc.c_s;
     a.trend = trend; a.mask = mask; a.k = k; a.gate = gate; a.prob = prob;

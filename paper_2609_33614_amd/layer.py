@@ -74,8 +74,9 @@ class EatLayer:
         k = torch.empty(T, dtype=torch.int32, device=self.device)
         gate = torch.empty(T, E, dtype=torch.float32, device=self.device)
         prob = torch.empty(T, E, dtype=torch.float32, device=self.device)
+        ws = self.workspace(T)
         L.eat_route(self.handle, x, T, self.w["w_router"], self.acc, trend, mask, k, gate, prob,
-                    None, 0, stream)
+                    ws, ws.numel(), stream)
         return mask, k, gate, prob
 
     def close(self) -> None:

@@ -191,15 +191,23 @@ def test_baseline_modes_need_no_accounts():
 def test_route_validation_happens_on_the_host():
     h = eat.eat_create(_params(), 16)
     try:
+        need = eat.eat_route_workspace_size(h, 4)
+        assert 0 < need <= eat.eat_workspace_size(h, 4)
         base = dict(x=FAKE, T=4, w_router=FAKE, acc=L.accounts(FAKE, FAKE, FAKE), ppl_trend=None,
-                    mask_out=FAKE, k_out=FAKE, gate_out=FAKE, prob_out=None, stream=0)
+                    mask_out=FAKE, k_out=FAKE, gate_out=FAKE, prob_out=None, ws=FAKE, ws_bytes=need, stream=0)
+        for kw, status in ((dict(ws=None), L.EAT_ERR_WORKSPACE), (dict(ws_bytes=need - 1), L.EAT_ERR_WORKSPACE),
+                           (dict(ws=FAKE + 64), L.EAT_ERR_INVALID_ARG)):
+            args = dict(base); args.update(kw)
+            with pytest.raises(eat.EatError) as ei:
+                eat.eat_route(h, **args)
+            assert ei.value.status == status, kw
         for kw in (dict(mask_out=None), dict(k_out=None), dict(gate_out=None), dict(x=None),
                    dict(w_router=FAKE + 8), dict(T=17), dict(acc=L.accounts(FAKE, None, FAKE))):
             args = dict(base); args.update(kw)
             with pytest.raises(eat.EatError) as ei:
                 eat.eat_route(h, **args)
             assert ei.value.status == L.EAT_ERR_INVALID_ARG, kw
-        args = dict(base); args["T"] = 0
+        args = dict(base); args.update(T=0, ws=None, ws_bytes=0)
         eat.eat_route(h, **args)
         with pytest.raises(eat.EatError):
             eat.eat_reset_accounts(h, L.accounts(None, FAKE, FAKE), 0)
