@@ -351,3 +351,41 @@ def test_full_shared_sampled(T):
     err = PT.row_rel_err(_y_host(y)[sample], lo.y[sample])
     PT.report(f"full shared T={T}", borderline=int(border.sum()), max_rel_y=f"{err.max():.2e}")
     assert (err <= PT.TOL_Y_BF16).all()
+
+
+# --------------------------------------------- prefill-sized (tile kernels) --
+
+TILE_CASES = {
+    # 1024-1500 tokens over 8 experts, K=2: 2+ token tiles per expert, ragged tails
+    "mixtral_tiles": dict(shape="mixtral", d=512, F=768, E=8, Fs=0),
+    # shared expert of width 384 over 600 tokens goes through the tile kernel
+    "shared_tiles": dict(shape="shared", d=256, F=192, E=60, Fs=384),
+}
+
+
+@pytest.mark.parametrize("mode", ["eat", "topk", "topp"])
+@pytest.mark.parametrize("case,T", [("mixtral_tiles", 1024), ("mixtral_tiles", 1500), ("shared_tiles", 600)])
+def test_forward_parity_prefill_tiles(case, T, mode):
+    c = TILE_CASES[case]
+    shape, w, lay, prm = _layer(c, mode, max_tokens=T)
+    x = make_prefill(shape, tokens=T, seqs=4, d=c["d"])
+    acc = make_accounts(c["E"], seed=T, c_scale=0.05)
+    if mode == "eat":
+        lay.load_accounts(*acc)
+    mask = torch.empty(T, dtype=torch.int64, device="cuda")
+    y = lay.forward(_x_dev(x), mask_out=mask)
+    torch.cuda.synchronize()
+    ref = O.moe_step(x, w, acc if mode == "eat" else None, None, prm)
+    border = PT.borderline(ref.routing, prm)
+    gm = PT.masks_to_list(mask)
+    bad = [t for t in range(T) if not border[t] and gm[t] != ref.routing.masks[t]]
+    err = PT.row_rel_err(_y_host(y), ref.y)
+    ok = ~border
+    PT.report(f"tiles {case} {mode} T={T}", borderline=int(border.sum()), mask_mismatch=len(bad),
+              max_rel_y=f"{err[ok].max():.2e}")
+    assert not bad
+    assert (err[ok] <= PT.TOL_Y_BF16).all()
+    if mode == "eat" and not border.any():
+        n, pt, cs = lay.accounts_host()
+        np.testing.assert_array_equal(n, ref.acc[0])
+        np.testing.assert_allclose(cs, ref.acc[2], rtol=PT.TOL_C_BF16, atol=1e-6)
