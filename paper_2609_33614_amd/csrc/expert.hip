@@ -493,13 +493,211 @@ __global__ __launch_bounds__(256) void tile_kernel(StreamArgs a) {
     }
 }
 
+// tile_dma_kernel: the same tiling with a 3-stage LDS ring fed by direct
+// global->LDS loads (global_load_lds_dwordx4), so two chunks of loads stay in
+// flight without holding registers.  One wave instruction fills one 1 KB
+// block of 8 rows x 128 B; the lane for (row r, slot s) fetches the row's
+// 16-byte vector s ^ ((r >> 1) & 7), an XOR swizzle under which every
+// 16-lane group of an MFMA operand read hits 16 distinct bank groups.  The
+// stages are separate LDS arrays and the ring is unrolled, so each wait
+// names only the stage about to be read.
+constexpr int kStageTok = kTM * kTK * 2;                // bytes of token rows per stage
+
+__device__ __forceinline__ int swz_off(int r, int v) {  // byte offset of (row, 16-B vector) in a region
+    return (r >> 3) * 1024 + (r & 7) * 128 + ((v ^ ((r >> 1) & 7)) << 4);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    // vmcnt(N) with expcnt / lgkmcnt left unconstrained (gfx9 encoding)
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <bool GATED>
+__global__ __launch_bounds__(256) void tile_dma_kernel(StreamArgs a) {
+    constexpr int NMAT = GATED ? 2 : 1;
+    constexpr int STAGE = kStageTok * (1 + NMAT);         // bytes per stage
+    constexpr int NB = 16 * (1 + NMAT);                   // 1 KB blocks per stage
+    constexpr int BPW = NB / 4;                           // blocks per wave per stage
+    __shared__ __attribute__((aligned(1024))) uint8_t st0[STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t st1[STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t st2[STAGE];
+    __shared__ int tstart[65];
+    const int tid = threadIdx.x;
+    const int lane = lane_id(), wave = tid / kWave;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    int ntiles;
+    if (a.offsets) {
+        if (tid == 0) {
+            int acc = 0;
+            for (int e = 0; e < a.groups; ++e) {
+                tstart[e] = acc;
+                acc += (a.offsets[e + 1] - a.offsets[e] + kTM - 1) / kTM;
+            }
+            tstart[a.groups] = acc;
+        }
+        __syncthreads();
+        ntiles = tstart[a.groups];
+    } else {
+        ntiles = (a.nrows + kTM - 1) / kTM;
+    }
+    const int nx = a.M / kTN;
+    const int work = ntiles * nx;
+    const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+    const int per_xcd_blocks = gridDim.x / kXcds;
+    const int chunk = (work + kXcds - 1) / kXcds;
+    const int wbeg = xcd * chunk, wend = min(work, wbeg + chunk);
+    const int nch = a.K / kTK;
+    const int l32 = lane & 31, lh = lane >> 5;
+    const int lrow = lane >> 3, lslot = lane & 7;        // lane's row within a DMA block and its slot
+
+    for (int wid = wbeg + slot; wid < wend; wid += per_xcd_blocks) {
+        const int tile = wid / nx, xt = wid % nx;
+        int e = 0, r0, n;
+        if (a.offsets) {
+            while (tstart[e + 1] <= tile) ++e;
+            r0 = a.offsets[e] + (tile - tstart[e]) * kTM;
+            n = min(kTM, a.offsets[e + 1] - r0);
+        } else {
+            r0 = tile * kTM;
+            n = min(kTM, a.nrows - r0);
+        }
+        const int m0 = xt * kTN;
+        // this lane's source vector for each block the wave fills
+        const uint16_t* src[BPW];
+        int dst[BPW];
+#pragma unroll
+        for (int j = 0; j < BPW; ++j) {
+            const int b = wave + 4 * j;                  // block index within the stage
+            const int rb = b & 15;                       // 8-row block within its region
+            const int r = rb * 8 + lrow;                 // row within the 128-row region
+            const int v = lslot ^ ((r >> 1) & 7);        // global vector this lane fetches
+            if (b < 16) {
+                const int srow = r < n ? (a.gather ? a.gather[r0 + r] : r0 + r) : (a.gather ? a.gather[r0] : r0);
+                src[j] = a.src + static_cast<size_t>(srow) * a.K + 8 * v;
+            } else {
+                const int mt = (b >> 4) - 1;
+                const uint16_t* base = mt == 0 ? a.wa : a.wb;
+                src[j] = base + (static_cast<size_t>(e) * a.M + m0 + r) * a.K + 8 * v;
+            }
+            dst[j] = b * 1024;
+        }
+        // Issued through asm so that the compiler inserts no waits of its
+        // own for these loads (it would merge the ring's stages and wait for
+        // all of them); the ring's explicit vmcnt waits + barriers order them.
+        auto issue = [&](uint8_t* st, int c) __attribute__((always_inline)) {
+#pragma unroll
+            for (int j = 0; j < BPW; ++j) {
+                const uint32_t lds = __builtin_amdgcn_readfirstlane(
+                    static_cast<uint32_t>(reinterpret_cast<uintptr_t>(st + dst[j])));
+                asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                             :: "v"(src[j] + c * kTK), "s"(lds) : "memory", "m0");
+            }
+        };
+
+        f32x16 acc[NMAT][2][2];
+#pragma unroll
+        for (int mt = 0; mt < NMAT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) acc[mt][i][j] = f32x16{};
+
+        auto compute = [&](const uint8_t* st) __attribute__((always_inline)) {
+#pragma unroll
+            for (int ks = 0; ks < kTK / 16; ++ks) {
+                const int v = 2 * ks + lh;
+                bf16x8 Bt[2], Aw[NMAT][2];
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    Bt[j] = *reinterpret_cast<const bf16x8*>(st + swz_off(wm * 64 + j * 32 + l32, v));
+#pragma unroll
+                for (int mt = 0; mt < NMAT; ++mt)
+#pragma unroll
+                    for (int i = 0; i < 2; ++i)
+                        Aw[mt][i] = *reinterpret_cast<const bf16x8*>(
+                            st + kStageTok * (1 + mt) + swz_off(wn * 64 + i * 32 + l32, v));
+#pragma unroll
+                for (int mt = 0; mt < NMAT; ++mt)
+#pragma unroll
+                    for (int i = 0; i < 2; ++i)
+#pragma unroll
+                        for (int j = 0; j < 2; ++j)
+                            acc[mt][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Aw[mt][i], Bt[j], acc[mt][i][j], 0, 0, 0);
+            }
+        };
+        // one ring step: wait for stage `cur` (later stages may stay in
+        // flight), barrier, refill the stage read last step, compute `cur`
+        auto step = [&](int c, uint8_t* cur, uint8_t* refill) __attribute__((always_inline)) {
+            if (c + 1 < nch) wait_vm<BPW>(); else wait_vm<0>();
+            lds_barrier();
+            if (c + 2 < nch) issue(refill, c + 2);
+            compute(cur);
+        };
+
+        // the previous tile's last reads must finish before the ring refills
+        lds_barrier();
+        issue(st0, 0);
+        if (nch > 1) issue(st1, 1);
+        int c = 0;
+        for (; c + 3 <= nch; c += 3) {
+            step(c, st0, st2);
+            step(c + 1, st1, st0);
+            step(c + 2, st2, st1);
+        }
+        if (c < nch) step(c, st0, st2);
+        if (c + 1 < nch) step(c + 1, st1, st0);
+
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int c = wm * 64 + j * 32 + l32;
+            if (c >= n) continue;
+            const size_t orow = static_cast<size_t>(r0 + c) * a.M;
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+#pragma unroll
+                for (int qb = 0; qb < 4; ++qb) {
+                    const int f = m0 + wn * 64 + i * 32 + 8 * qb + 4 * lh;
+                    if constexpr (GATED) {
+                        uint16_t hv[4];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            hv[q] = f32_to_bf16(silu(acc[0][i][j][4 * qb + q]) * acc[1][i][j][4 * qb + q]);
+                        uint2 pk;
+                        pk.x = static_cast<uint32_t>(hv[0]) | (static_cast<uint32_t>(hv[1]) << 16);
+                        pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
+                        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + orow + f) = pk;
+                    } else {
+                        *reinterpret_cast<float4*>(static_cast<float*>(a.out) + orow + f) =
+                            make_float4(acc[0][i][j][4 * qb + 0], acc[0][i][j][4 * qb + 1],
+                                        acc[0][i][j][4 * qb + 2], acc[0][i][j][4 * qb + 3]);
+                    }
+                }
+            }
+        }
+    }
+}
+
+// The gated projection uses the DMA ring (its register-staged version is
+// limited to one workgroup per CU anyway); the plain one keeps register
+// staging, which fits two workgroups per CU.
+#ifndef EAT_TILE_DMA_GATED
+#define EAT_TILE_DMA_GATED 1
+#endif
+#ifndef EAT_TILE_DMA_PLAIN
+#define EAT_TILE_DMA_PLAIN 0
+#endif
+
 template <bool GATED>
 hipError_t launch_tile(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
     // persistent: at most one workgroup per CU and XCD slot, a multiple of 8
     const int64_t work = max_tiles * (a.M / kTN);
     int64_t blocks = std::min<int64_t>(work, GATED ? 256 : 512);
     blocks = std::max<int64_t>(kXcds, (blocks + kXcds - 1) / kXcds * kXcds);
-    tile_kernel<GATED><<<static_cast<int>(blocks), 256, 0, s>>>(a);
+    if (GATED ? EAT_TILE_DMA_GATED : EAT_TILE_DMA_PLAIN) tile_dma_kernel<GATED><<<static_cast<int>(blocks), 256, 0, s>>>(a);
+    else tile_kernel<GATED><<<static_cast<int>(blocks), 256, 0, s>>>(a);
     return hipGetLastError();
 }
 
