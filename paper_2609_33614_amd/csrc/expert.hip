@@ -120,13 +120,14 @@ __device__ __forceinline__ bf16x8 ld16(const uint16_t* p) {
 // 16*KS*(GATED ? 2 : 1) bytes per lane of weights in flight.
 // Token sub-tiles beyond the tile's row count are skipped (uniform branch),
 // so a tile of 1 token costs one MFMA per k-step and matrix.
-template <bool GATED, int NSUB, int KS>
-__global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
+template <bool GATED, int NSUB, int KS, int WPB>
+__global__ __launch_bounds__(WPB * 64) void stream_kernel(StreamArgs a) {
+    constexpr int NT = WPB * 64;                      // threads per workgroup
     constexpr int BN = 16 * NSUB;
     constexpr int KC = 32 * KS;
     constexpr int LDS_ROW = KC + 8;                   // +16 B per row against bank conflicts
     constexpr int VPR = KC / 8;                       // 16-byte vectors per token row per chunk
-    constexpr int RMAX = (BN * VPR + 255) / 256;      // vectors per thread per chunk
+    constexpr int RMAX = (BN * VPR + NT - 1) / NT;    // vectors per thread per chunk
     __shared__ __attribute__((aligned(16))) uint16_t xs[2][BN * LDS_ROW];
     __shared__ int tstart[65];
     const int tid = threadIdx.x;
@@ -149,7 +150,7 @@ __global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
     }
 
     const int i = lane & 15, g = lane >> 4;
-    const int m0 = blockIdx.x * 64 + wave * 16;
+    const int m0 = blockIdx.x * (16 * WPB) + wave * 16;
     const int kbeg = blockIdx.z * a.ksplit;
     const int nch = a.ksplit / KC;
 
@@ -174,7 +175,7 @@ __global__ __launch_bounds__(256) void stream_kernel(StreamArgs a) {
         bool xon[RMAX];
 #pragma unroll
         for (int r = 0; r < RMAX; ++r) {
-            const int v = tid + 256 * r;
+            const int v = tid + NT * r;
             const int row = v / VPR, col = v % VPR;
             xon[r] = row < n;
             const int srow = xon[r] ? (a.gather ? a.gather[r0 + row] : r0 + row) : 0;
@@ -736,10 +737,21 @@ constexpr int max_ks() {
     return NSUB >= 8 ? 2 : NSUB >= 4 ? EAT_KS_P4 : NSUB >= 2 ? EAT_KS_P2 : EAT_KS_P1;
 }
 
+// Waves per workgroup: the down projection with 64+-token tiles shares one
+// token slab between 8 waves (half the slab traffic per weight byte); the
+// gated kernel is faster with 4 (measured on the Mixtral-shaped layer).
+template <bool GATED, int NSUB>
+constexpr int stream_wpb() { return (!GATED && NSUB >= 4) ? 8 : 4; }
+
 template <bool GATED, int NSUB, int KS>
 hipError_t launch_stream_k(const StreamArgs& a, dim3 grid, hipStream_t s) {
     if constexpr (KS <= max_ks<GATED, NSUB>()) {
-        stream_kernel<GATED, NSUB, KS><<<grid, dim3(256), 0, s>>>(a);
+        if (stream_wpb<GATED, NSUB>() == 8 && a.M % 128 == 0) {
+            grid.x = a.M / 128;
+            stream_kernel<GATED, NSUB, KS, 8><<<grid, dim3(512), 0, s>>>(a);
+        } else {
+            stream_kernel<GATED, NSUB, KS, 4><<<grid, dim3(256), 0, s>>>(a);
+        }
         return hipGetLastError();
     } else {
         return hipErrorInvalidValue;
