@@ -37,7 +37,7 @@ eat_status_t check_params(const eat_params_t& p) {
         (p.expert_dtype != EAT_F32 && p.expert_dtype != EAT_BF16))
         return EAT_ERR_INVALID_ARG;
     // supported shapes and dtype pairs
-    if (p.E > 64) return EAT_ERR_UNSUPPORTED;
+    if (p.E > eat::kMaxExperts) return EAT_ERR_UNSUPPORTED;
     if (p.d_model % 64 || p.d_ffn % 64 || p.d_shared % 64) return EAT_ERR_UNSUPPORTED;
     if (p.act_dtype != p.expert_dtype) return EAT_ERR_UNSUPPORTED;
     return EAT_OK;

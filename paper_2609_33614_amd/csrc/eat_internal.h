@@ -5,6 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <functional>
 
 #include "../../include/eat.h"
@@ -16,6 +17,8 @@ struct eat_ctx {
 };
 
 namespace eat {
+
+constexpr int kMaxExperts = 64;    // one 64-bit selection mask per token
 
 // Offsets (bytes) of the workspace regions for T tokens.  Every region
 // starts on a 256-byte boundary.
@@ -103,6 +106,16 @@ int down_splits(const eat_params_t& p, int32_t T);
 // Slices of the bf16 up/gate projection; above 1 the gate and up sums go
 // through fp32 partial buffers (workspace region gu) and a reduce kernel.
 int up_splits(const eat_params_t& p, int32_t T);
+
+// Grouped bf16 GEMM with 256 x 256 tiles for prefill-sized calls (wide.hip):
+// gated = H = bf16(silu(x W1^T) * (x W3^T)) over 128-feature tiles, plain =
+// fp32 out = src W^T over 256-row tiles.  Rows are the expert segments given
+// by offsets (gather maps them to source rows), or nrows identity rows when
+// offsets is null.  wide_fits tells whether M and K suit the tiling.
+bool wide_fits(bool gated, int M, int K);
+hipError_t launch_wide(bool gated, const uint16_t* wa, const uint16_t* wb, const uint16_t* src,
+                       const int32_t* gather, const int32_t* offsets, int groups, int nrows, int M,
+                       int K, void* out, int64_t rows_cap, hipStream_t s);
 
 hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets,
                                   const int32_t* tok_idx, const float* prob, const float* nrm2,

@@ -10,6 +10,8 @@
 // read from HBM exactly once per token tile, which is what bounds decode.
 // The down projection may split its reduction dimension over gridDim.z;
 // the partial tiles are added, in split order, by the combine kernel.
+// Prefill-sized calls (hundreds of rows per expert) go to the wide MFMA
+// tiles of wide.hip instead.
 //
 // fp32 path: plain dot products, one thread per output element, for layers
 // whose weights are fp32 (small correctness-sized layers).
@@ -312,396 +314,6 @@ __global__ __launch_bounds__(256) void swiglu_reduce_kernel(const float* __restr
     }
 }
 
-// ---------------------------------------------------------- bf16 tiles --
-//
-// Prefill-sized calls (hundreds of tokens per expert) are bound by the
-// matrix cores, not by HBM.  tile_kernel is a grouped GEMM over the experts'
-// row segments: a workgroup owns a tile of 128 tokens x 128 weight rows (the
-// gated kernel holds 128 rows of both W1 and W3), walks the reduction
-// dimension in 64-wide chunks staged through double-buffered LDS, and its 4
-// waves (2 x 2) each compute 64 tokens x 64 rows per matrix with
-// v_mfma_f32_32x32x16_bf16 (weights as the A operand, tokens as B, so a lane
-// ends with 4 consecutive output features of one token).  LDS rows are
-// padded to 144 bytes, which keeps every 16-lane group of ds_read_b128
-// conflict-free.  The grid is persistent: each XCD (workgroups are dealt to
-// the 8 XCDs round-robin) walks one contiguous eighth of the work list,
-// ordered token tile by token tile, so an expert's weight tiles are reused
-// inside one XCD's L2.
-
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-
-constexpr int kTM = 128;                 // tokens per tile
-constexpr int kTN = 128;                 // weight rows per tile (per matrix)
-constexpr int kTK = 64;                  // reduction chunk
-constexpr int kTPitch = kTK + 8;         // LDS row pitch (bf16 elements)
-constexpr int kXcds = 8;
-
-template <bool GATED>
-__global__ __launch_bounds__(256) void tile_kernel(StreamArgs a) {
-    constexpr int NMAT = GATED ? 2 : 1;
-    constexpr int WROWS = NMAT * kTN;                    // weight rows staged per chunk
-    __shared__ __attribute__((aligned(16))) uint16_t ws_lds[2][WROWS * kTPitch];
-    __shared__ __attribute__((aligned(16))) uint16_t xs_lds[2][kTM * kTPitch];
-    __shared__ int tstart[65];
-    const int tid = threadIdx.x;
-    const int lane = lane_id(), wave = tid / kWave;
-    const int wm = wave >> 1, wn = wave & 1;             // wave's 64-token / 64-row quadrant
-
-    int ntiles;
-    if (a.offsets) {
-        if (tid == 0) {
-            int acc = 0;
-            for (int e = 0; e < a.groups; ++e) {
-                tstart[e] = acc;
-                acc += (a.offsets[e + 1] - a.offsets[e] + kTM - 1) / kTM;
-            }
-            tstart[a.groups] = acc;
-        }
-        __syncthreads();
-        ntiles = tstart[a.groups];
-    } else {
-        ntiles = (a.nrows + kTM - 1) / kTM;
-    }
-    const int nx = a.M / kTN;
-    const int work = ntiles * nx;
-    // XCD-contiguous share of the work list
-    const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
-    const int per_xcd_blocks = gridDim.x / kXcds;
-    const int chunk = (work + kXcds - 1) / kXcds;
-    const int wbeg = xcd * chunk, wend = min(work, wbeg + chunk);
-    const int nch = a.K / kTK;
-
-    // global -> LDS mapping: each row is 8 vectors of 16 B; 256 threads
-    // cover 32 rows per round
-    const int vcol = tid & 7, vrow = tid >> 3;
-    const int l32 = lane & 31, lh = lane >> 5;
-
-    for (int wid = wbeg + slot; wid < wend; wid += per_xcd_blocks) {
-        const int tile = wid / nx, xt = wid % nx;
-        int e = 0, r0, n;
-        if (a.offsets) {
-            while (tstart[e + 1] <= tile) ++e;
-            r0 = a.offsets[e] + (tile - tstart[e]) * kTM;
-            n = min(kTM, a.offsets[e + 1] - r0);
-        } else {
-            r0 = tile * kTM;
-            n = min(kTM, a.nrows - r0);
-        }
-        const int m0 = xt * kTN;
-        // sources of this thread's 4 token rows and 4 (x NMAT) weight rows
-        const uint16_t* xsrc[4];
-        const uint16_t* wsrc[4 * NMAT];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = vrow + 32 * r;
-            const int srow = row < n ? (a.gather ? a.gather[r0 + row] : r0 + row) : (a.gather ? a.gather[r0] : r0);
-            xsrc[r] = a.src + static_cast<size_t>(srow) * a.K + 8 * vcol;
-#pragma unroll
-            for (int mt = 0; mt < NMAT; ++mt) {
-                const uint16_t* base = mt == 0 ? a.wa : a.wb;
-                wsrc[mt * 4 + r] = base + (static_cast<size_t>(e) * a.M + m0 + row) * a.K + 8 * vcol;
-            }
-        }
-        bf16x8 xr[4], wr[4 * NMAT];
-        auto load = [&](int c) __attribute__((always_inline)) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) xr[r] = ld16(xsrc[r] + c * kTK);
-#pragma unroll
-            for (int r = 0; r < 4 * NMAT; ++r) wr[r] = ld16(wsrc[r] + c * kTK);
-        };
-        auto store = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                *reinterpret_cast<bf16x8*>(&xs_lds[buf][(vrow + 32 * r) * kTPitch + 8 * vcol]) = xr[r];
-#pragma unroll
-            for (int mt = 0; mt < NMAT; ++mt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    *reinterpret_cast<bf16x8*>(&ws_lds[buf][(mt * kTN + vrow + 32 * r) * kTPitch + 8 * vcol]) =
-                        wr[mt * 4 + r];
-        };
-
-        f32x16 acc[NMAT][2][2];                           // [matrix][row tile][token tile]
-#pragma unroll
-        for (int mt = 0; mt < NMAT; ++mt)
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j) acc[mt][i][j] = f32x16{};
-
-        load(0);
-        store(0);
-        lds_barrier();
-        for (int c = 0; c < nch; ++c) {
-            const bool more = c + 1 < nch;
-            if (more) load(c + 1);
-            const uint16_t* wb = ws_lds[c & 1];
-            const uint16_t* xb = xs_lds[c & 1];
-#pragma unroll
-            for (int ks = 0; ks < kTK / 16; ++ks) {
-                const int kk = ks * 16 + 8 * lh;
-                bf16x8 Bt[2], Aw[NMAT][2];
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    Bt[j] = *reinterpret_cast<const bf16x8*>(xb + (wm * 64 + j * 32 + l32) * kTPitch + kk);
-#pragma unroll
-                for (int mt = 0; mt < NMAT; ++mt)
-#pragma unroll
-                    for (int i = 0; i < 2; ++i)
-                        Aw[mt][i] = *reinterpret_cast<const bf16x8*>(
-                            wb + (mt * kTN + wn * 64 + i * 32 + l32) * kTPitch + kk);
-#pragma unroll
-                for (int mt = 0; mt < NMAT; ++mt)
-#pragma unroll
-                    for (int i = 0; i < 2; ++i)
-#pragma unroll
-                        for (int j = 0; j < 2; ++j)
-                            acc[mt][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Aw[mt][i], Bt[j], acc[mt][i][j], 0, 0, 0);
-            }
-            if (more) store((c + 1) & 1);
-            lds_barrier();
-        }
-
-        // result: lane holds weight rows 8*(q/4) + 4*(lane/32) + q%4 of each
-        // 32-row tile for token column lane%32 of each 32-token tile
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int c = wm * 64 + j * 32 + l32;
-            if (c >= n) continue;
-            const size_t orow = static_cast<size_t>(r0 + c) * a.M;
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-#pragma unroll
-                for (int qb = 0; qb < 4; ++qb) {
-                    const int f = m0 + wn * 64 + i * 32 + 8 * qb + 4 * lh;
-                    if constexpr (GATED) {
-                        uint16_t hv[4];
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            hv[q] = f32_to_bf16(silu(acc[0][i][j][4 * qb + q]) * acc[1][i][j][4 * qb + q]);
-                        uint2 pk;
-                        pk.x = static_cast<uint32_t>(hv[0]) | (static_cast<uint32_t>(hv[1]) << 16);
-                        pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
-                        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + orow + f) = pk;
-                    } else {
-                        *reinterpret_cast<float4*>(static_cast<float*>(a.out) + orow + f) =
-                            make_float4(acc[0][i][j][4 * qb + 0], acc[0][i][j][4 * qb + 1],
-                                        acc[0][i][j][4 * qb + 2], acc[0][i][j][4 * qb + 3]);
-                    }
-                }
-            }
-        }
-    }
-}
-
-// tile_dma_kernel: the same tiling with a 3-stage LDS ring fed by direct
-// global->LDS loads (global_load_lds_dwordx4), so two chunks of loads stay in
-// flight without holding registers.  One wave instruction fills one 1 KB
-// block of 8 rows x 128 B; the lane for (row r, slot s) fetches the row's
-// 16-byte vector s ^ ((r >> 1) & 7), an XOR swizzle under which every
-// 16-lane group of an MFMA operand read hits 16 distinct bank groups.  The
-// stages are separate LDS arrays and the ring is unrolled, so each wait
-// names only the stage about to be read.
-constexpr int kStageTok = kTM * kTK * 2;                // bytes of token rows per stage
-
-__device__ __forceinline__ int swz_off(int r, int v) {  // byte offset of (row, 16-B vector) in a region
-    return (r >> 3) * 1024 + (r & 7) * 128 + ((v ^ ((r >> 1) & 7)) << 4);
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-    // vmcnt(N) with expcnt / lgkmcnt left unconstrained (gfx9 encoding)
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-template <bool GATED>
-__global__ __launch_bounds__(256) void tile_dma_kernel(StreamArgs a) {
-    constexpr int NMAT = GATED ? 2 : 1;
-    constexpr int STAGE = kStageTok * (1 + NMAT);         // bytes per stage
-    constexpr int NB = 16 * (1 + NMAT);                   // 1 KB blocks per stage
-    constexpr int BPW = NB / 4;                           // blocks per wave per stage
-    __shared__ __attribute__((aligned(1024))) uint8_t st0[STAGE];
-    __shared__ __attribute__((aligned(1024))) uint8_t st1[STAGE];
-    __shared__ __attribute__((aligned(1024))) uint8_t st2[STAGE];
-    __shared__ int tstart[65];
-    const int tid = threadIdx.x;
-    const int lane = lane_id(), wave = tid / kWave;
-    const int wm = wave >> 1, wn = wave & 1;
-
-    int ntiles;
-    if (a.offsets) {
-        if (tid == 0) {
-            int acc = 0;
-            for (int e = 0; e < a.groups; ++e) {
-                tstart[e] = acc;
-                acc += (a.offsets[e + 1] - a.offsets[e] + kTM - 1) / kTM;
-            }
-            tstart[a.groups] = acc;
-        }
-        __syncthreads();
-        ntiles = tstart[a.groups];
-    } else {
-        ntiles = (a.nrows + kTM - 1) / kTM;
-    }
-    const int nx = a.M / kTN;
-    const int work = ntiles * nx;
-    const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
-    const int per_xcd_blocks = gridDim.x / kXcds;
-    const int chunk = (work + kXcds - 1) / kXcds;
-    const int wbeg = xcd * chunk, wend = min(work, wbeg + chunk);
-    const int nch = a.K / kTK;
-    const int l32 = lane & 31, lh = lane >> 5;
-    const int lrow = lane >> 3, lslot = lane & 7;        // lane's row within a DMA block and its slot
-
-    for (int wid = wbeg + slot; wid < wend; wid += per_xcd_blocks) {
-        const int tile = wid / nx, xt = wid % nx;
-        int e = 0, r0, n;
-        if (a.offsets) {
-            while (tstart[e + 1] <= tile) ++e;
-            r0 = a.offsets[e] + (tile - tstart[e]) * kTM;
-            n = min(kTM, a.offsets[e + 1] - r0);
-        } else {
-            r0 = tile * kTM;
-            n = min(kTM, a.nrows - r0);
-        }
-        const int m0 = xt * kTN;
-        // this lane's source vector for each block the wave fills
-        const uint16_t* src[BPW];
-        int dst[BPW];
-#pragma unroll
-        for (int j = 0; j < BPW; ++j) {
-            const int b = wave + 4 * j;                  // block index within the stage
-            const int rb = b & 15;                       // 8-row block within its region
-            const int r = rb * 8 + lrow;                 // row within the 128-row region
-            const int v = lslot ^ ((r >> 1) & 7);        // global vector this lane fetches
-            if (b < 16) {
-                const int srow = r < n ? (a.gather ? a.gather[r0 + r] : r0 + r) : (a.gather ? a.gather[r0] : r0);
-                src[j] = a.src + static_cast<size_t>(srow) * a.K + 8 * v;
-            } else {
-                const int mt = (b >> 4) - 1;
-                const uint16_t* base = mt == 0 ? a.wa : a.wb;
-                src[j] = base + (static_cast<size_t>(e) * a.M + m0 + r) * a.K + 8 * v;
-            }
-            dst[j] = b * 1024;
-        }
-        // Issued through asm so that the compiler inserts no waits of its
-        // own for these loads (it would merge the ring's stages and wait for
-        // all of them); the ring's explicit vmcnt waits + barriers order them.
-        auto issue = [&](uint8_t* st, int c) __attribute__((always_inline)) {
-#pragma unroll
-            for (int j = 0; j < BPW; ++j) {
-                const uint32_t lds = __builtin_amdgcn_readfirstlane(
-                    static_cast<uint32_t>(reinterpret_cast<uintptr_t>(st + dst[j])));
-                asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-                             :: "v"(src[j] + c * kTK), "s"(lds) : "memory", "m0");
-            }
-        };
-
-        f32x16 acc[NMAT][2][2];
-#pragma unroll
-        for (int mt = 0; mt < NMAT; ++mt)
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j) acc[mt][i][j] = f32x16{};
-
-        auto compute = [&](const uint8_t* st) __attribute__((always_inline)) {
-#pragma unroll
-            for (int ks = 0; ks < kTK / 16; ++ks) {
-                const int v = 2 * ks + lh;
-                bf16x8 Bt[2], Aw[NMAT][2];
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    Bt[j] = *reinterpret_cast<const bf16x8*>(st + swz_off(wm * 64 + j * 32 + l32, v));
-#pragma unroll
-                for (int mt = 0; mt < NMAT; ++mt)
-#pragma unroll
-                    for (int i = 0; i < 2; ++i)
-                        Aw[mt][i] = *reinterpret_cast<const bf16x8*>(
-                            st + kStageTok * (1 + mt) + swz_off(wn * 64 + i * 32 + l32, v));
-#pragma unroll
-                for (int mt = 0; mt < NMAT; ++mt)
-#pragma unroll
-                    for (int i = 0; i < 2; ++i)
-#pragma unroll
-                        for (int j = 0; j < 2; ++j)
-                            acc[mt][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Aw[mt][i], Bt[j], acc[mt][i][j], 0, 0, 0);
-            }
-        };
-        // one ring step: wait for stage `cur` (later stages may stay in
-        // flight), barrier, refill the stage read last step, compute `cur`
-        auto step = [&](int c, uint8_t* cur, uint8_t* refill) __attribute__((always_inline)) {
-            if (c + 1 < nch) wait_vm<BPW>(); else wait_vm<0>();
-            lds_barrier();
-            if (c + 2 < nch) issue(refill, c + 2);
-            compute(cur);
-        };
-
-        // the previous tile's last reads must finish before the ring refills
-        lds_barrier();
-        issue(st0, 0);
-        if (nch > 1) issue(st1, 1);
-        int c = 0;
-        for (; c + 3 <= nch; c += 3) {
-            step(c, st0, st2);
-            step(c + 1, st1, st0);
-            step(c + 2, st2, st1);
-        }
-        if (c < nch) step(c, st0, st2);
-        if (c + 1 < nch) step(c + 1, st1, st0);
-
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int c = wm * 64 + j * 32 + l32;
-            if (c >= n) continue;
-            const size_t orow = static_cast<size_t>(r0 + c) * a.M;
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-#pragma unroll
-                for (int qb = 0; qb < 4; ++qb) {
-                    const int f = m0 + wn * 64 + i * 32 + 8 * qb + 4 * lh;
-                    if constexpr (GATED) {
-                        uint16_t hv[4];
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            hv[q] = f32_to_bf16(silu(acc[0][i][j][4 * qb + q]) * acc[1][i][j][4 * qb + q]);
-                        uint2 pk;
-                        pk.x = static_cast<uint32_t>(hv[0]) | (static_cast<uint32_t>(hv[1]) << 16);
-                        pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
-                        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + orow + f) = pk;
-                    } else {
-                        *reinterpret_cast<float4*>(static_cast<float*>(a.out) + orow + f) =
-                            make_float4(acc[0][i][j][4 * qb + 0], acc[0][i][j][4 * qb + 1],
-                                        acc[0][i][j][4 * qb + 2], acc[0][i][j][4 * qb + 3]);
-                    }
-                }
-            }
-        }
-    }
-}
-
-// The gated projection uses the DMA ring (its register-staged version is
-// limited to one workgroup per CU anyway); the plain one keeps register
-// staging, which fits two workgroups per CU.
-#ifndef EAT_TILE_DMA_GATED
-#define EAT_TILE_DMA_GATED 1
-#endif
-#ifndef EAT_TILE_DMA_PLAIN
-#define EAT_TILE_DMA_PLAIN 0
-#endif
-
-template <bool GATED>
-hipError_t launch_tile(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
-    // persistent: at most one workgroup per CU and XCD slot, a multiple of 8
-    const int64_t work = max_tiles * (a.M / kTN);
-    int64_t blocks = std::min<int64_t>(work, GATED ? 256 : 512);
-    blocks = std::max<int64_t>(kXcds, (blocks + kXcds - 1) / kXcds * kXcds);
-    if (GATED ? EAT_TILE_DMA_GATED : EAT_TILE_DMA_PLAIN) tile_dma_kernel<GATED><<<static_cast<int>(blocks), 256, 0, s>>>(a);
-    else tile_kernel<GATED><<<static_cast<int>(blocks), 256, 0, s>>>(a);
-    return hipGetLastError();
-}
-
 // Largest chunk (in 32-wide k-steps) that divides the reduction slice.
 static int pick_ks(int ksplit) {
     for (int ks : {8, 4, 2, 1})
@@ -822,24 +434,24 @@ static int stream_splits(int64_t rows_m, int kdim, const eat_params_t& p, int32_
     return s;
 }
 
-// Prefill-sized calls (two or more 128-token tiles per expert on average)
-// go through the MFMA tile kernel, which needs 128-multiple output widths.
-bool use_tiles(const eat_params_t& p, int32_t T) {
-    return p.expert_dtype == EAT_BF16 && static_cast<int64_t>(T) * p.top_k >= 2LL * 128 * p.E &&
-           p.d_ffn % 128 == 0 && p.d_model % 128 == 0;
+// Prefill-sized calls (256 or more rows per expert on average; the
+// always-on expert from 384 tokens) go through the wide MFMA tiles.
+static bool use_wide(const eat_params_t& p, int32_t T) {
+    return p.expert_dtype == EAT_BF16 && static_cast<int64_t>(T) * p.top_k >= 256LL * p.E &&
+           wide_fits(true, p.d_ffn, p.d_model) && wide_fits(false, p.d_model, p.d_ffn);
 }
-
-static bool shared_tiles(const eat_params_t& p, int32_t T) {
-    return T >= 512 && p.d_shared % 128 == 0 && p.d_model % 128 == 0;
+static bool shared_wide(const eat_params_t& p, int32_t T) {
+    return T >= 384 && p.d_shared > 0 && wide_fits(true, p.d_shared, p.d_model) &&
+           wide_fits(false, p.d_model, p.d_shared);
 }
 
 int down_splits(const eat_params_t& p, int32_t T) {
-    if (p.expert_dtype != EAT_BF16 || use_tiles(p, T)) return 1;
+    if (p.expert_dtype != EAT_BF16 || use_wide(p, T)) return 1;
     return stream_splits(p.d_model, p.d_ffn, p, T, 8, EAT_SPLIT_WAVES);
 }
 
 int up_splits(const eat_params_t& p, int32_t T) {
-    if (p.expert_dtype != EAT_BF16 || use_tiles(p, T)) return 1;
+    if (p.expert_dtype != EAT_BF16 || use_wide(p, T)) return 1;
     return stream_splits(p.d_ffn, p.d_model, p, T, EAT_UP_SPLIT_MAX, EAT_UP_SPLIT_WAVES);
 }
 
@@ -873,18 +485,11 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     const int cap_up = std::max(1, 2048 / std::max(1, p.d_ffn / 64));
     const int tiles_up = static_cast<int>(std::min<int64_t>(max_tiles, cap_up));
 
-    if (use_tiles(p, T)) {
-        const int64_t tiles = std::min<int64_t>(rows_cap, (rows_cap + kTM - 1) / kTM + p.E);
-        StreamArgs up{};
-        up.wa = w1; up.wb = w3; up.src = x; up.gather = tok_idx; up.offsets = offsets;
-        up.groups = p.E; up.M = p.d_ffn; up.K = p.d_model; up.ksplit = p.d_model; up.out = h;
-        hipError_t err = launch_tile<true>(up, tiles, s);
+    if (use_wide(p, T)) {
+        hipError_t err = launch_wide(true, w1, w3, x, tok_idx, offsets, p.E, 0, p.d_ffn, p.d_model, h, rows_cap, s);
         if (err != hipSuccess) return err;
         if (between) between();
-        StreamArgs dn{};
-        dn.wa = w2; dn.src = h; dn.offsets = offsets;
-        dn.groups = p.E; dn.M = p.d_model; dn.K = p.d_ffn; dn.ksplit = p.d_ffn; dn.out = yp;
-        return launch_tile<false>(dn, tiles, s);
+        return launch_wide(false, w2, nullptr, h, nullptr, offsets, p.E, 0, p.d_model, p.d_ffn, yp, rows_cap, s);
     }
     const int usplits = up_splits(p, T);
     StreamArgs up{};
@@ -918,17 +523,10 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
 hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* x, const uint16_t* ws1,
                               const uint16_t* ws3, const uint16_t* ws2, uint16_t* hs, float* ys,
                               hipStream_t s) {
-    if (shared_tiles(p, T)) {
-        const int64_t tiles = (T + kTM - 1) / kTM;
-        StreamArgs up{};
-        up.wa = ws1; up.wb = ws3; up.src = x; up.nrows = T;
-        up.groups = 1; up.M = p.d_shared; up.K = p.d_model; up.ksplit = p.d_model; up.out = hs;
-        hipError_t err = launch_tile<true>(up, tiles, s);
+    if (shared_wide(p, T)) {
+        hipError_t err = launch_wide(true, ws1, ws3, x, nullptr, nullptr, 1, T, p.d_shared, p.d_model, hs, T, s);
         if (err != hipSuccess) return err;
-        StreamArgs dn{};
-        dn.wa = ws2; dn.src = hs; dn.nrows = T;
-        dn.groups = 1; dn.M = p.d_model; dn.K = p.d_shared; dn.ksplit = p.d_shared; dn.out = ys;
-        return launch_tile<false>(dn, tiles, s);
+        return launch_wide(false, ws2, nullptr, hs, nullptr, nullptr, 1, T, p.d_model, p.d_shared, ys, T, s);
     }
     const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;

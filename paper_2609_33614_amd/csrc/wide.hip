@@ -1,0 +1,254 @@
+// Wide MFMA tiles for prefill-sized grouped GEMMs (gfx950).
+//
+// At prefill sizes (hundreds of rows per expert) the expert projections are
+// dense contractions whose speed is set by how fast each CU can pull operand
+// bytes from L2 into LDS.  Measured on this part, that rate grows with the
+// number of waves issuing loads (about 20 B/clk per CU with 4 waves, 46 with
+// 8, 80 with 16), not with the loads each wave keeps in flight; and lines
+// that miss L2 come at roughly HBM speed whatever their pattern.  So a
+// workgroup here is 16 waves (4 per SIMD) that own a 256-token x 256-row tile
+// (the gated projection: 128 rows of W1 and the matching 128 of W3) -- half
+// the bytes per flop of a 128 x 128 tile -- all of them loading the stages
+// of a double-buffered LDS ring (64-wide reduction chunks, 128-byte rows,
+// direct global->LDS loads) and each computing 64 tokens x 64 weight rows
+// with v_mfma_f32_32x32x16_bf16 (weights as A, tokens as B: a lane ends with
+// 4 consecutive output features of one token).  Four waves per SIMD hide
+// each other's LDS and barrier latency without hand scheduling.  The waves
+// of a SIMD cover the four token quarters of the tile, so when a tile holds
+// fewer rows of its expert, the waves of the empty quarters skip their
+// MFMAs and every SIMD's work shrinks with the tile.
+//
+// The grid is persistent: the work list (token tile x weight tile, token
+// tiles of one expert adjacent) is cut into 8 contiguous parts, one per XCD
+// (workgroups are dealt to XCDs round-robin), so the workgroups that share an
+// expert's weight tiles share one L2.
+#include "eat_device.h"
+#include "eat_internal.h"
+
+namespace eat {
+namespace {
+
+constexpr int kWM = 256;                  // token rows per tile
+constexpr int kWN = 256;                  // weight rows per tile
+constexpr int kWK = 64;                   // reduction chunk (bf16 elements): 128-byte rows
+constexpr int kWaves = 16;                // 4 token quarters x 4 weight quarters
+constexpr int kThreads = kWaves * kWave;
+constexpr int kRegion = kWM * kWK * 2;    // bytes of one operand's rows per stage (32 KB)
+constexpr int kStage = 2 * kRegion;       // tokens then weights (64 KB)
+constexpr int kXcd = 8;
+static_assert(kWN * kWK * 2 == kRegion, "token and weight regions have the same size");
+
+struct WideArgs {
+    const uint16_t* wa;        // [groups][M][K]  (W1, or W2 for the plain projection)
+    const uint16_t* wb;        // [groups][M][K]  (W3, gated only)
+    const uint16_t* src;       // activation rows, K wide
+    const int32_t* gather;     // row -> source row, or null (identity)
+    const int32_t* offsets;    // [groups+1] expert-major row offsets, or null
+    int groups, nrows, M, K;
+    void* out;                 // gated: bf16 H [rows][M]; plain: fp32 [rows][M]
+};
+
+// Byte offset of 16-byte vector v (0..7) of row r in a region of 128-byte
+// rows; the XOR spreads the rows that one LDS cycle serves for an MFMA
+// operand read (consecutive rows, same vector) over distinct banks.
+__device__ __forceinline__ int wswz(int r, int v) {
+    return r * 128 + ((v ^ ((r >> 1) & 7)) << 4);
+}
+
+template <bool GATED>
+__device__ __forceinline__ void wide_tile(const WideArgs& a, uint8_t* ring, int e, int r0, int n, int m0) {
+    constexpr int NB = (kWM + kWN) / 8;       // 1 KB DMA blocks (8 rows each) per stage
+    constexpr int BPW = NB / kWaves;          // per wave
+    static_assert(NB % kWaves == 0, "blocks split evenly over the waves");
+    const int lane = lane_id(), wave = threadIdx.x / kWave;
+    const int l32 = lane & 31, lh = lane >> 5;
+    const int wm = wave >> 2, wn = wave & 3;  // token quarter, weight quarter (SIMD = wave % 4)
+
+    // Lane l of a DMA instruction writes LDS bytes [16 l, 16 l + 16) of its
+    // 1 KB block = row l / 8, slot l % 8; it fetches the global vector that
+    // belongs in that slot under the swizzle.
+    const uint16_t* srcp[BPW];
+    int dst[BPW];
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+        const int b = wave + kWaves * j;
+        const int slot = lane & 7;
+        if (b < kWM / 8) {
+            const int r = 8 * b + (lane >> 3);
+            const int v = slot ^ ((r >> 1) & 7);
+            // rows past the expert's segment load a valid row (results unused)
+            const int srow = r < n ? (a.gather ? a.gather[r0 + r] : r0 + r) : (a.gather ? a.gather[r0] : r0);
+            srcp[j] = a.src + static_cast<size_t>(srow) * a.K + 8 * v;
+            dst[j] = 1024 * b;
+        } else {
+            const int r = 8 * (b - kWM / 8) + (lane >> 3);
+            const int v = slot ^ ((r >> 1) & 7);
+            const uint16_t* base = GATED && r >= kWN / 2 ? a.wb : a.wa;
+            const int row = m0 + (GATED ? (r & (kWN / 2 - 1)) : r);
+            srcp[j] = base + (static_cast<size_t>(e) * a.M + row) * a.K + 8 * v;
+            dst[j] = kRegion + 1024 * (b - kWM / 8);
+        }
+    }
+    // asm keeps the compiler from adding waits of its own for these loads;
+    // the ring's waits and barriers order them.
+    auto issue = [&](uint8_t* st, int c) __attribute__((always_inline)) {
+        const int kc = c * kWK;
+#pragma unroll
+        for (int j = 0; j < BPW; ++j) {
+            const uint32_t lds = __builtin_amdgcn_readfirstlane(
+                static_cast<uint32_t>(reinterpret_cast<uintptr_t>(st + dst[j])));
+            asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                         :: "v"(srcp[j] + kc), "s"(lds) : "memory", "m0");
+        }
+    };
+
+    f32x16 acc[2][2];                         // [weight fragment][token fragment]
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+    // this wave's token quarter holds rows of the expert
+    const bool active = 64 * wm < n;
+    const int brow = 64 * wm;
+    const int arow0 = GATED ? 32 * wn : 64 * wn;
+    const int arow1 = GATED ? kWN / 2 + 32 * wn : 64 * wn + 32;
+    auto compute = [&](const uint8_t* st) __attribute__((always_inline)) {
+#pragma unroll
+        for (int ks = 0; ks < kWK / 16; ++ks) {
+            const int v = 2 * ks + lh;
+            bf16x8 B[2], A[2];
+            B[0] = *reinterpret_cast<const bf16x8*>(st + wswz(brow + l32, v));
+            B[1] = *reinterpret_cast<const bf16x8*>(st + wswz(brow + 32 + l32, v));
+            A[0] = *reinterpret_cast<const bf16x8*>(st + kRegion + wswz(arow0 + l32, v));
+            A[1] = *reinterpret_cast<const bf16x8*>(st + kRegion + wswz(arow1 + l32, v));
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[i], B[j], acc[i][j], 0, 0, 0);
+        }
+    };
+    const int nch = a.K / kWK;               // a multiple of 2 (K % 128 == 0)
+    uint8_t* st0 = ring;
+    uint8_t* st1 = ring + kStage;
+    // One ring step: wait for this wave's loads of chunk c, barrier (every
+    // wave's loads have landed and every wave is done with the other stage),
+    // refill the other stage with chunk c + 1, compute chunk c.
+    auto step = [&](int c, uint8_t* cur, uint8_t* nxt) __attribute__((always_inline)) {
+        wait_vm<0>();
+        lds_barrier();
+        if (c + 1 < nch) issue(nxt, c + 1);
+        if (active) compute(cur);
+    };
+
+    // the previous tile's last reads must finish before the ring refills
+    lds_barrier();
+    issue(st0, 0);
+    for (int c = 0; c < nch; c += 2) {
+        step(c, st0, st1);
+        step(c + 1, st1, st0);
+    }
+    if (!active) return;
+
+    // lane holds weight rows 8 (q / 4) + 4 lh + q % 4 of each 32-row
+    // fragment, for token row brow + 32 j + l32
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int t = brow + 32 * j + l32;
+        if (t >= n) continue;
+        const size_t orow = static_cast<size_t>(r0 + t) * a.M;
+        if constexpr (GATED) {
+#pragma unroll
+            for (int qb = 0; qb < 4; ++qb) {
+                const int f = m0 + 32 * wn + 8 * qb + 4 * lh;
+                uint16_t hv[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    hv[q] = f32_to_bf16(silu(acc[0][j][4 * qb + q]) * acc[1][j][4 * qb + q]);
+                uint2 pk;
+                pk.x = static_cast<uint32_t>(hv[0]) | (static_cast<uint32_t>(hv[1]) << 16);
+                pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
+                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + orow + f) = pk;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int qb = 0; qb < 4; ++qb) {
+                    const int f = m0 + 64 * wn + 32 * i + 8 * qb + 4 * lh;
+                    *reinterpret_cast<float4*>(static_cast<float*>(a.out) + orow + f) =
+                        make_float4(acc[i][j][4 * qb + 0], acc[i][j][4 * qb + 1],
+                                    acc[i][j][4 * qb + 2], acc[i][j][4 * qb + 3]);
+                }
+        }
+    }
+}
+
+template <bool GATED>
+__global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
+    __shared__ __attribute__((aligned(1024))) uint8_t ring[2 * kStage];
+    __shared__ int tstart[kMaxExperts + 1];
+    const int tid = threadIdx.x;
+
+    int ntiles;
+    if (a.offsets) {
+        if (tid == 0) {
+            int acc = 0;
+            for (int g = 0; g < a.groups; ++g) {
+                tstart[g] = acc;
+                acc += (a.offsets[g + 1] - a.offsets[g] + kWM - 1) / kWM;
+            }
+            tstart[a.groups] = acc;
+        }
+        __syncthreads();
+        ntiles = tstart[a.groups];
+    } else {
+        ntiles = (a.nrows + kWM - 1) / kWM;
+    }
+    constexpr int kOut = GATED ? kWN / 2 : kWN;     // output features per tile
+    const int nx = a.M / kOut;
+    const int work = ntiles * nx;
+    const int xcd = blockIdx.x % kXcd, slot = blockIdx.x / kXcd;
+    const int per_xcd = gridDim.x / kXcd;
+    const int part = (work + kXcd - 1) / kXcd;
+    const int wbeg = xcd * part, wend = min(work, wbeg + part);
+
+    for (int wid = wbeg + slot; wid < wend; wid += per_xcd) {
+        const int tile = wid / nx, xt = wid % nx;
+        int e = 0, r0, n;
+        if (a.offsets) {
+            while (tstart[e + 1] <= tile) ++e;
+            r0 = a.offsets[e] + (tile - tstart[e]) * kWM;
+            n = min(kWM, a.offsets[e + 1] - r0);
+        } else {
+            r0 = tile * kWM;
+            n = min(kWM, a.nrows - r0);
+        }
+        wide_tile<GATED>(a, ring, e, r0, n, xt * kOut);
+    }
+}
+
+}  // namespace
+
+bool wide_fits(bool gated, int M, int K) {
+    return M % (gated ? kWN / 2 : kWN) == 0 && K % (2 * kWK) == 0;
+}
+
+hipError_t launch_wide(bool gated, const uint16_t* wa, const uint16_t* wb, const uint16_t* src,
+                       const int32_t* gather, const int32_t* offsets, int groups, int nrows, int M, int K,
+                       void* out, int64_t rows_cap, hipStream_t s) {
+    WideArgs a{wa, wb, src, gather, offsets, groups, nrows, M, K, out};
+    // every group may end in a partial tile
+    const int64_t tiles = offsets ? std::min<int64_t>(rows_cap, (rows_cap + kWM - 1) / kWM + groups)
+                                  : (nrows + kWM - 1) / kWM;
+    const int64_t work = tiles * (M / (gated ? kWN / 2 : kWN));
+    // persistent: one workgroup per CU (the ring takes 128 KB of LDS and the
+    // 16 waves fill the SIMDs), a multiple of the XCD count
+    int64_t blocks = std::min<int64_t>(work, 256);
+    blocks = std::max<int64_t>(kXcd, (blocks + kXcd - 1) / kXcd * kXcd);
+    if (gated) wide_kernel<true><<<static_cast<int>(blocks), kThreads, 0, s>>>(a);
+    else wide_kernel<false><<<static_cast<int>(blocks), kThreads, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace eat

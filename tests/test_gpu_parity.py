@@ -356,15 +356,21 @@ def test_full_shared_sampled(T):
 # --------------------------------------------- prefill-sized (tile kernels) --
 
 TILE_CASES = {
-    # 1024-1500 tokens over 8 experts, K=2: 2+ token tiles per expert, ragged tails
+    # 1024-1500 tokens over 8 experts, K=2: 256-375 rows per expert, so the
+    # wide tiles run with partly filled token quarters and ragged tails
     "mixtral_tiles": dict(shape="mixtral", d=512, F=768, E=8, Fs=0),
-    # shared expert of width 384 over 600 tokens goes through the tile kernel
+    # shared expert of width 384 over 600 tokens goes through the wide tiles
+    # (two full 256-token tiles and an 88-token half-height one)
     "shared_tiles": dict(shape="shared", d=256, F=192, E=60, Fs=384),
+    # 2048-3000 tokens over 8 experts, K=2: 512-750 rows per expert, full
+    # 256-token tiles plus ragged last ones
+    "mixtral_wide": dict(shape="mixtral", d=512, F=768, E=8, Fs=0),
 }
 
 
 @pytest.mark.parametrize("mode", ["eat", "topk", "topp"])
-@pytest.mark.parametrize("case,T", [("mixtral_tiles", 1024), ("mixtral_tiles", 1500), ("shared_tiles", 600)])
+@pytest.mark.parametrize("case,T", [("mixtral_tiles", 1024), ("mixtral_tiles", 1500), ("shared_tiles", 600),
+                                    ("mixtral_wide", 2048), ("mixtral_wide", 3000)])
 def test_forward_parity_prefill_tiles(case, T, mode):
     c = TILE_CASES[case]
     shape, w, lay, prm = _layer(c, mode, max_tokens=T)
