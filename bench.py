@@ -14,6 +14,11 @@ Prints one JSON line: EAT tokens/s (``value``), the Top-K (K=2) and Top-P
 the experts touched per step, the up/gate kernel's achieved HBM bandwidth
 against the MI355X peak (timed per launch with HIP events on the launch
 stream), a batch sweep, and the CPU oracle timed on a bounded sample.
+A ``prefill`` object adds the MFMA-bound side: one prefill call of the
+fine-grained layer (4096 tokens, 64 experts of width 1024, K=8) and of the
+shared-expert layer (8192 tokens, 60 experts of width 1408 + an always-on
+expert of width 5632, K=4), each starting from zero accounts, with the
+expert stages' achieved bf16 TFLOP/s against the dense MFMA peak.
 
     python bench.py [--steps K] [--warmup W] [--batch B] [--gpus 1]
 """
@@ -34,6 +39,7 @@ if ROOT not in sys.path:
 
 METRIC = "MoE-layer tokens/s + activated experts/token (EAT vs Top-K); HBM GB/s % peak"
 HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0          # MI355X dense bf16 MFMA
 
 
 def log(msg: str) -> None:
@@ -137,6 +143,63 @@ def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bo
     return dict(total_ms=total_ms, up_ms=up_ms, dn_ms=dn_ms, k=k, U=U, E=E, accounts=acc)
 
 
+def run_prefill(shape_name: str, reps: int, ev: HipEvents, modes=("eat", "topk")):
+    """One prefill call of a layer (its prompt tokens, zero accounts) timed
+    per stage with HIP events, `reps` times after 2 untimed calls; returns
+    per-mode tokens/s, activated experts and the expert stages' TFLOP/s."""
+    import torch
+
+    from paper_2609_33614_amd import _lib as L
+    from paper_2609_33614_amd.layer import EatLayer, to_device
+    from workload import SHAPES, make_layer_weights, make_prefill
+
+    shape = SHAPES[shape_name]
+    T = shape.prefill_tokens
+    wdev = to_device(make_layer_weights(shape))
+    x = torch.from_numpy(make_prefill(shape)).view(torch.bfloat16).cuda()
+    y = torch.empty(T, shape.d, dtype=torch.bfloat16, device="cuda")
+    mask = torch.empty(T, dtype=torch.int64, device="cuda")
+    d, F, Fs, E = shape.d, shape.F, shape.F_shared, shape.E
+    out = {"workload": f"{shape_name} layer prefill", "tokens": T, "d_model": d, "experts": E, "d_ffn": F,
+           "d_shared": Fs, "top_k": shape.K}
+    for mode in modes:
+        p = L.eat_params_default(mode=L.MODES[mode], E=E, d_model=d, d_ffn=F, top_k=shape.K,
+                                 top_p=shape.top_p or 0.6, inv_temperature=shape.inv_temp, d_shared=Fs)
+        lay = EatLayer(p, T, wdev)
+        stage = ev.create(L.EAT_NUM_STAGE_EVENTS)
+        tot, up, dn, sh = [], [], [], []
+        for it in range(2 + reps):
+            lay.reset_accounts()
+            lay.forward(x, y=y, mask_out=mask, events=stage)
+            torch.cuda.synchronize()
+            if it >= 2:
+                tot.append(ev.elapsed_ms(stage[L.EAT_STAGE_BEGIN], stage[L.EAT_STAGE_END]))
+                up.append(ev.elapsed_ms(stage[L.EAT_STAGE_PERMUTED], stage[L.EAT_STAGE_UP]))
+                dn.append(ev.elapsed_ms(stage[L.EAT_STAGE_UP], stage[L.EAT_STAGE_DOWN]))
+                sh.append(ev.elapsed_ms(stage[L.EAT_STAGE_DOWN], stage[L.EAT_STAGE_SHARED]))
+        lay.close()
+        sk = float(popcounts(mask.cpu().numpy().astype(np.int64).view(np.uint64)[None]).sum())
+        t_ms, up_ms, dn_ms, sh_ms = (float(np.median(v)) for v in (tot, up, dn, sh))
+        fl_up, fl_dn = 4.0 * d * F * sk, 2.0 * d * F * sk
+        fl_sh = 6.0 * d * Fs * T
+        fl_all = 2.0 * T * d * E + fl_up + fl_dn + fl_sh
+        tf = lambda fl, ms: fl / (ms * 1e-3) / 1e12
+        r = {"tokens_per_s": round(T / (t_ms * 1e-3), 1), "ms": round(t_ms, 4),
+             "mean_activated_experts": round(sk / T, 4),
+             "up_gate": {"us": round(up_ms * 1e3, 1), "tflops": round(tf(fl_up, up_ms), 1),
+                         "frac": round(tf(fl_up, up_ms) / BF16_PEAK_TFLOPS, 4)},
+             "down": {"us": round(dn_ms * 1e3, 1), "tflops": round(tf(fl_dn, dn_ms), 1),
+                      "frac": round(tf(fl_dn, dn_ms) / BF16_PEAK_TFLOPS, 4)},
+             "layer_tflops": round(tf(fl_all, t_ms), 1)}
+        if Fs:
+            r["shared"] = {"us": round(sh_ms * 1e3, 1), "tflops": round(tf(fl_sh, sh_ms), 1),
+                           "frac": round(tf(fl_sh, sh_ms) / BF16_PEAK_TFLOPS, 4)}
+        out[mode] = r
+    del wdev
+    torch.cuda.empty_cache()
+    return out
+
+
 def traffic_up(shape, B, k_row, U):
     """Algorithmic HBM bytes of one up/gate launch: W1 and W3 rows of every
     expert in the step's union, the B token rows read, the H rows written."""
@@ -201,6 +264,11 @@ def main(argv=None) -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--modes", default="eat,topk,topp", help="routing modes to time (eat first)")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the prefill (MFMA-bound) measurement")
+    ap.add_argument("--prefill-reps", type=int, default=10)
+    ap.add_argument("--only-prefill", default="", metavar="LAYER",
+                    help="time only the prefill of LAYER (finegrained or shared) in --modes and print "
+                         "its JSON object (for kernel traces of the MFMA-bound path)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run 4 plain device copies of MIB MiB (a known-size kernel for "
                          "calibrating HBM byte counters)")
@@ -219,6 +287,12 @@ def main(argv=None) -> int:
 
     L.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.only_prefill:
+        ev = HipEvents()
+        res = run_prefill(args.only_prefill, args.prefill_reps, ev, modes=[m for m in args.modes.split(",") if m])
+        ev.close()
+        print(json.dumps({"prefill": [res]}), flush=True)
+        return 0
     shape = SHAPES["mixtral"]
     B, K, W = args.batch, args.steps, args.warmup
     log(f"generating weights d={shape.d} E={shape.E} F={shape.F}")
@@ -278,6 +352,13 @@ def main(argv=None) -> int:
                              "mean_experts_touched_per_step": round(float(rr["U"].mean()), 3)}
             sweep.append(row)
             del xb
+    prefill = []
+    if not args.no_prefill:
+        del wdev
+        torch.cuda.empty_cache()
+        for name in ("finegrained", "shared"):
+            log(f"prefill {name}: {args.prefill_reps} timed calls per mode")
+            prefill.append(run_prefill(name, args.prefill_reps, ev))
     ev.close()
 
     cpu = None
@@ -312,6 +393,7 @@ def main(argv=None) -> int:
         "cpu_baseline": cpu,
         "modes": {name: summary(res) for name, res in results.items()},
         "sweep": sweep,
+        "prefill": prefill,
     }
     print(json.dumps(out), flush=True)
     return 0

@@ -14,6 +14,13 @@ that bench.py reads for roofline.traffic, with the SHA-1 of the expert
 kernel source they were measured on).
 
     python profile_summary.py --trace T --fetch F --write W --bench-json B.json --name NAME
+
+Prefill (MFMA-bound) summary of the wide tile kernels, from a trace of
+
+  TRACE   rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run --
+              python3 bench.py --only-prefill LAYER --modes topk
+
+    python profile_summary.py --prefill --trace T --bench-json B.json --name NAME
 """
 from __future__ import annotations
 
@@ -46,16 +53,78 @@ def copy_factor(rows, mib: int, expect_bytes: float) -> float:
     return expect_bytes / statistics.mean(vals)
 
 
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def prefill_summary(args) -> int:
+    """Per-launch duration and achieved bf16 TFLOP/s of the wide tile kernels
+    (gated up/gate and plain down) of one traced prefill configuration."""
+    bench = json.loads(open(args.bench_json).read().strip().splitlines()[-1])
+    pf = bench["prefill"][0]
+    modes = [m for m in ("eat", "topk", "topp") if m in pf]
+    assert len(modes) == 1, "trace one routing mode at a time"
+    r = pf[modes[0]]
+    T, d, F = pf["tokens"], pf["d_model"], pf["d_ffn"]
+    sk = r["mean_activated_experts"] * T
+    stats = list(csv.DictReader(open(os.path.join(args.trace, "run_kernel_stats.csv"))))
+    trace = list(csv.DictReader(open(os.path.join(args.trace, "run_kernel_trace.csv"))))
+    trace.sort(key=lambda x: int(x["Start_Timestamp"]))
+
+    def launches(key):
+        return [(int(x["End_Timestamp"]) - int(x["Start_Timestamp"])) / 1e3 for x in trace if key in x["Kernel_Name"]]
+
+    rows = []
+    shared = pf.get("d_shared", 0)
+    per_fwd = 2 if shared else 1          # routed (+ always-on) launches per forward
+    for key, label, fl, ev_us in (("wide_kernel<true>", "up/gate (gated)", 4.0 * d * F * sk, r["up_gate"]["us"]),
+                                  ("wide_kernel<false>", "down (plain)", 2.0 * d * F * sk, r["down"]["us"])):
+        durs = launches(key)
+        routed = durs[0::per_fwd][-args.reps:]
+        us = statistics.mean(routed)
+        rows.append((key, label, len(durs), us, fl, ev_us))
+    md = os.path.join(ROOT, "profiles", args.name + ".md")
+    with open(md, "w") as f:
+        f.write(f"# {args.name}\n\n")
+        f.write(f"Workload: {pf['workload']}, {T} tokens, d_model {d}, {pf['experts']} experts of width {F}"
+                f"{', always-on expert of width ' + str(shared) if shared else ''}, K={pf['top_k']}, "
+                f"{modes[0]} routing from zero accounts (mean {r['mean_activated_experts']} experts per token), "
+                f"MI355X.\n\n")
+        f.write("Commands (from the repository root):\n\n```\n")
+        f.write(f"rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run -- "
+                f"python3 bench.py --only-prefill {pf['workload'].split()[0]} --modes {modes[0]}\n")
+        f.write(f"python3 profile_summary.py --prefill --trace TRACE --bench-json TRACED_BENCH.json --name {args.name}\n```\n\n")
+        f.write("## Kernel time (rocprofv3 --stats, whole traced run incl. warm-up)\n\n")
+        f.write("| kernel | calls | avg us | % time |\n|---|---|---|---|\n")
+        for x in stats[:10]:
+            name = x["Name"].replace("(anonymous namespace)::", "").split("(")[0]
+            f.write(f"| `{name}` | {x['Calls']} | {float(x['AverageNs']) / 1e3:.2f} | {float(x['Percentage']):.1f} |\n")
+        f.write(f"\n## Routed expert GEMMs (last {args.reps} launches of each)\n\n")
+        f.write("| kernel | stage | avg us (trace) | us (bench events) | algorithmic GFLOP | TFLOP/s | % of 2.5 PF bf16 |\n")
+        f.write("|---|---|---|---|---|---|---|\n")
+        for key, label, n, us, fl, ev_us in rows:
+            f.write(f"| `{key}` | {label} | {us:.1f} | {ev_us:.1f} | {fl / 1e9:.1f} | {fl / us / 1e6:.1f} | "
+                    f"{fl / us / 1e6 / BF16_PEAK_TFLOPS * 100:.1f} |\n")
+        f.write("\nAlgorithmic flops: up/gate 4 d F sum(k), down 2 d F sum(k), sum(k) = the call's "
+                "(token, expert) assignments; padding rows of partly filled tiles are not counted.\n")
+    print(open(md).read())
+    return 0
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", required=True)
-    ap.add_argument("--fetch", required=True)
-    ap.add_argument("--write", required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
     ap.add_argument("--bench-json", required=True, help="JSON line printed by the traced bench run")
     ap.add_argument("--name", required=True)
     ap.add_argument("--copy-mib", type=int, default=1024)
     ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--prefill", action="store_true", help="summarise a prefill trace (wide tile kernels)")
+    ap.add_argument("--reps", type=int, default=10, help="timed prefill calls in the traced run")
     args = ap.parse_args(argv)
+    if args.prefill:
+        return prefill_summary(args)
+    assert args.fetch and args.write, "--fetch and --write are needed for the decode summary"
 
     bench = json.loads(open(args.bench_json).read().strip().splitlines()[-1])
     stats = list(csv.DictReader(open(os.path.join(args.trace, "run_kernel_stats.csv"))))
