@@ -21,7 +21,8 @@ Where the paper is silent or ambiguous, the readings listed in ``Params``
 
 Pins: every function here is checked by ``tests/test_oracle_*.py`` against a
 hand-computed three-step sequence, brute-force enumeration on E <= 8,
-library routines (softmax, quantile, std, top-k, SiLU) and closed forms.
+library routines (softmax, quantile, std, top-k, SiLU, RMSNorm, bf16
+conversion) and closed forms.
 """
 from __future__ import annotations
 
@@ -392,3 +393,49 @@ def moe_step(x, weights: dict, acc, trend, prm: Params, sequential: bool = False
     lo = layer_outputs(x, weights, r, prm)
     new_acc = account_update(acc, r.masks, r.p, lo.norms, prm) if prm.mode == MODE_EAT else acc
     return StepOut(y=lo.y, routing=r, norms=lo.norms, acc=new_acc)
+
+
+# ------------------------------------------- stacked layers (evaluation) --
+#
+# The 16-layer evaluation workload composes MoE layers, each with its own
+# account state: layer l reads u = RMSNorm(h_l) (unit weight), and the next
+# layer's input is h_{l+1} = (h_l + MoE_l(u)) M_l^T with a d x d mixing
+# matrix.  Activations are bf16 between the steps, rounded once at each of
+# the three points below from the exact (here fp64) value.
+
+def round_bf16(a) -> np.ndarray:
+    """Nearest bf16 value (ties to even) of each element, as float64:
+    8 significant bits, quantum 2**(e - 8) for a value in [2**(e-1), 2**e),
+    never finer than the smallest subnormal step 2**-133."""
+    a = np.asarray(a, dtype=np.float64)
+    _, e = np.frexp(a)
+    q = np.ldexp(1.0, np.maximum(e, -125) - 8)
+    out = np.rint(a / q) * q                       # rint rounds halves to even
+    return np.where(np.abs(out) > 3.3895313892515355e38, np.copysign(np.inf, a), out)
+
+
+def rms_norm(h, eps: float = 1e-6) -> np.ndarray:
+    """Row-wise h / sqrt(mean(h^2) + eps) (unit gain)."""
+    h = widen(h)
+    return h / np.sqrt(np.mean(h * h, axis=1, keepdims=True) + eps)
+
+
+@dataclass
+class StackOut:
+    h: np.ndarray              # [T, d] bf16 values (float64) after the last layer
+    layers: List[StepOut]      # per layer: routing, outputs, new accounts
+
+
+def stack_step(x, layers: Sequence[dict], mixes: Sequence[np.ndarray], accs: Sequence[tuple], trend,
+               prms: Sequence[Params], eps: float = 1e-6) -> StackOut:
+    """One decode step through the stacked layers:
+    u_l = bf16(RMSNorm(h_l)), r_l = bf16(h_l + MoE_l(u_l)), h_{l+1} = bf16(r_l M_l^T)."""
+    h = widen(x)
+    outs = []
+    for w, m, acc, prm in zip(layers, mixes, accs, prms):
+        u = round_bf16(rms_norm(h, eps))
+        o = moe_step(u, w, acc, trend, prm)
+        r = round_bf16(h + o.y)
+        h = round_bf16(r @ widen(m).T)
+        outs.append(o)
+    return StackOut(h=h, layers=outs)

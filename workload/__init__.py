@@ -10,6 +10,7 @@ from .gmm import (  # noqa: F401
     SHAPES,
     bf16_bits,
     make_layer_weights,
+    make_mixing,
     HiddenStream,
     make_prefill,
     make_trend,

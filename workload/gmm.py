@@ -17,7 +17,9 @@ Recipe (identical for every consumer):
   * cluster means mu_c ~ N(0, 2 I_d) (variance 2); x = mu_c + N(0, I_d);
   * each sequence keeps its cluster across steps; with probability
     ``redraw`` per step it draws a new one (uniform, or Zipf(s) over
-    cluster ranks when ``zipf`` is set).
+    cluster ranks when ``zipf`` is set);
+  * stacked layers: layer l's weights come from root seed + 7919 l, and its
+    d x d mixing matrix M_l ~ N(0, 1/d) (bf16) from a stream of its own.
 """
 from __future__ import annotations
 
@@ -153,6 +155,15 @@ def make_layer_weights(shape: LayerShape, seed: Optional[int] = None, layer: int
         out["ws3"] = pack(_normal(g_shared, (Fs, d), 1.0 / np.sqrt(d)))
         out["ws2"] = pack(_normal(g_shared, (d, Fs), 1.0 / np.sqrt(Fs)))
     return out
+
+
+def make_mixing(shape: LayerShape, layer: int, seed: Optional[int] = None, d: Optional[int] = None) -> np.ndarray:
+    """The d x d residual mixing matrix applied after stacked layer ``layer``:
+    N(0, 1/d) entries from the layer's own stream, bf16 bits."""
+    d = shape.d if d is None else d
+    root = (1000 + shape.index if seed is None else seed) + 7919 * layer
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([root, 0x6d6978])))
+    return bf16_bits(_normal(g, (d, d), 1.0 / np.sqrt(d)))
 
 
 @dataclass
