@@ -62,6 +62,7 @@ class Params:
     inv_temp: float = 1.0      # router logit scale (1 = plain softmax)
     cs_mode: int = 0           # 0: C_s used as is in Eq. 1; 1: C_s / sum(C_s)
     shared: bool = False       # always-on shared expert added with weight 1
+    round_h: bool = False      # round the experts' hidden activation to bf16 (R27)
 
 
 # ---------------------------------------------------------------- inputs --
@@ -285,11 +286,15 @@ def silu(a: np.ndarray) -> np.ndarray:
     return a / (1.0 + np.exp(-a))
 
 
-def swiglu(x: np.ndarray, w1: np.ndarray, w3: np.ndarray, w2: np.ndarray) -> np.ndarray:
+def swiglu(x: np.ndarray, w1: np.ndarray, w3: np.ndarray, w2: np.ndarray, round_h: bool = False) -> np.ndarray:
     """One expert FFN applied to rows of x: W2 (silu(W1 x) * (W3 x)), no
-    biases.  x [n, d]; w1, w3 [F, d]; w2 [d, F]; returns [n, d]."""
+    biases.  x [n, d]; w1, w3 [F, d]; w2 [d, F]; returns [n, d].  With
+    ``round_h`` the hidden activation is rounded to bf16 before W2, the
+    precision at which a bf16 layer stores it (reading R27)."""
     x = widen(x)
     h = silu(x @ widen(w1).T) * (x @ widen(w3).T)
+    if round_h:
+        h = round_bf16(h)
     return h @ widen(w2).T
 
 
@@ -313,12 +318,12 @@ def layer_outputs(x, weights: dict, r: Routing, prm: Params, tokens: Optional[Se
         rows = [t for t in toks if (r.masks[t] >> e) & 1]
         if not rows:
             continue
-        o = swiglu(xw[rows], weights["w1"][e], weights["w3"][e], weights["w2"][e])
+        o = swiglu(xw[rows], weights["w1"][e], weights["w3"][e], weights["w2"][e], prm.round_h)
         for j, t in enumerate(rows):
             norms[t, e] = math.sqrt(float(np.dot(o[j], o[j])))
             y[t] += r.g_norm[t, e] * o[j]
     if prm.shared and "ws1" in weights:
-        o = swiglu(xw[toks], weights["ws1"], weights["ws3"], weights["ws2"])
+        o = swiglu(xw[toks], weights["ws1"], weights["ws3"], weights["ws2"], prm.round_h)
         for j, t in enumerate(toks):
             y[t] += o[j]
     return LayerOut(y=y, norms=norms)

@@ -62,6 +62,14 @@ def test_swiglu_matches_torch_silu_reference():
         * torch.nn.functional.linear(X, torch.from_numpy(w3)),
         torch.from_numpy(w2))
     np.testing.assert_allclose(O.swiglu(x, w1, w3, w2), ref.numpy(), rtol=1e-12, atol=1e-12)
+    # with the hidden activation rounded to bf16 (torch's conversion goes
+    # through fp32; a double-rounding tie is not expected in 100 values)
+    hid = (torch.nn.functional.silu(torch.nn.functional.linear(X, torch.from_numpy(w1)))
+           * torch.nn.functional.linear(X, torch.from_numpy(w3)))
+    ref_r = torch.nn.functional.linear(hid.float().to(torch.bfloat16).double(), torch.from_numpy(w2))
+    got_r = O.swiglu(x, w1, w3, w2, round_h=True)
+    np.testing.assert_allclose(got_r, ref_r.numpy(), rtol=1e-12, atol=1e-12)
+    assert np.abs(got_r - ref.numpy()).max() > 1e-4            # the rounding is really applied
 
 
 def test_widen_bf16_matches_torch():
