@@ -14,6 +14,9 @@ Prints one JSON line: EAT tokens/s (``value``), the Top-K (K=2) and Top-P
 the experts touched per step, the up/gate kernel's achieved HBM bandwidth
 against the MI355X peak (timed per launch with HIP events on the launch
 stream), a batch sweep, and the CPU oracle timed on a bounded sample.
+A ``stack`` object times the 16-layer workload (16 fine-grained layers,
+RMSNorm and a residual mixing matrix between them, decode batch 64) per
+routing mode, with every layer's mean activated experts.
 A ``prefill`` object adds the MFMA-bound side: one prefill call of the
 fine-grained layer (4096 tokens, 64 experts of width 1024, K=8) and of the
 shared-expert layer (8192 tokens, 60 experts of width 1408 + an always-on
@@ -200,6 +203,68 @@ def run_prefill(shape_name: str, reps: int, ev: HipEvents, modes=("eat", "topk")
     return out
 
 
+def run_stack(steps: int, warmup: int, ev: HipEvents, modes=("eat", "topk", "topp")):
+    """The 16-layer workload: decode batch 64 through 16 stacked fine-grained
+    layers (own accounts each, RMSNorm + residual mixing between layers),
+    `steps` timed steps per mode after `warmup` untimed ones on scratch
+    accounts (then reset).  Returns per-mode tokens/s, per-layer mean
+    activated experts and experts touched, and the step's algorithmic HBM
+    bandwidth (every layer's router, the experts its tokens touch, its mixing
+    matrix)."""
+    import torch
+
+    from paper_2609_33614_amd import _lib as L
+    from paper_2609_33614_amd.layer import EatStack, to_device
+    from workload import SHAPES, HiddenStream, make_layer_weights, make_mixing
+
+    shape = SHAPES["stack16"]
+    nl, B, d, E, F = shape.layers, shape.decode_batches[0], shape.d, shape.E, shape.F
+    t = time.time()
+    wdev, mdev = [], []
+    for l in range(nl):
+        wdev.append(to_device(make_layer_weights(shape, layer=l)))
+        mdev.append(torch.from_numpy(make_mixing(shape, l)).view(torch.bfloat16).cuda())
+    log(f"stack weights ready in {time.time() - t:.1f} s ({nl} layers)")
+    xs = torch.from_numpy(HiddenStream(shape, B).steps(warmup + steps)).view(torch.bfloat16).cuda()
+    out = {"workload": f"{nl}-layer stack decode (RMSNorm + residual mixing between layers)", "layers": nl,
+           "batch": B, "d_model": d, "experts": E, "d_ffn": F, "top_k": shape.K, "steps": steps}
+    for mode in modes:
+        params = [L.eat_params_default(mode=L.MODES[mode], E=E, d_model=d, d_ffn=F, top_k=shape.K,
+                                       top_p=shape.top_p, inv_temperature=shape.inv_temp) for _ in range(nl)]
+        st = EatStack(params, B, wdev, mdev)
+        h = torch.empty(B, d, dtype=torch.bfloat16, device="cuda")
+        masks = torch.empty(steps, nl, B, dtype=torch.int64, device="cuda")
+        scratch = torch.empty(nl, B, dtype=torch.int64, device="cuda")
+        for s_ in range(warmup):
+            st.forward(xs[s_], h_out=h, masks_out=scratch)
+        st.reset_accounts()
+        t0, t1 = ev.create(2)
+        stream = torch.cuda.current_stream().cuda_stream
+        torch.cuda.synchronize()
+        ev.hip.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
+        ev.hip.hipEventRecord(t0, stream)
+        for s_ in range(steps):
+            st.forward(xs[warmup + s_], h_out=h, masks_out=masks[s_])
+        ev.hip.hipEventRecord(t1, stream)
+        torch.cuda.synchronize()
+        ms = ev.elapsed_ms(t0, t1)
+        m = masks.cpu().numpy().astype(np.int64).view(np.uint64)                # [steps, layers, B]
+        k = np.stack([popcounts(m[:, l, :]) for l in range(nl)])                # [layers, steps, B]
+        U = np.stack([union_sizes(m[:, l, :]) for l in range(nl)])              # [layers, steps]
+        st.close()
+        bytes_step = (U.sum(axis=0) * 3.0 * d * F * 2 + nl * (E * d * 4 + d * d * 2 + B * d * 2 * 4)).mean()
+        out[mode] = {"tokens_per_s": round(B * steps / (ms / 1e3), 1), "ms_per_step": round(ms / steps, 4),
+                     "mean_activated_experts": round(float(k.mean()), 4),
+                     "per_layer_mean_activated_experts": [round(float(v), 3) for v in k.mean(axis=(1, 2))],
+                     "per_layer_experts_touched": [round(float(v), 2) for v in U.mean(axis=1)],
+                     "hbm_gbs": round(bytes_step / (ms / steps / 1e3) / 1e9, 1),
+                     "hbm_frac": round(bytes_step / (ms / steps / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+        log(f"stack {mode}: {out[mode]['tokens_per_s']} tok/s, {out[mode]['ms_per_step']} ms/step")
+    del wdev, mdev
+    torch.cuda.empty_cache()
+    return out
+
+
 def traffic_up(shape, B, k_row, U):
     """Algorithmic HBM bytes of one up/gate launch: W1 and W3 rows of every
     expert in the step's union, the B token rows read, the H rows written."""
@@ -266,6 +331,9 @@ def main(argv=None) -> int:
     ap.add_argument("--modes", default="eat,topk,topp", help="routing modes to time (eat first)")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill (MFMA-bound) measurement")
     ap.add_argument("--prefill-reps", type=int, default=10)
+    ap.add_argument("--no-stack", action="store_true", help="skip the 16-layer stack measurement")
+    ap.add_argument("--stack-steps", type=int, default=1024)
+    ap.add_argument("--only-stack", action="store_true", help="time only the 16-layer stack and print its JSON")
     ap.add_argument("--only-prefill", default="", metavar="LAYER",
                     help="time only the prefill of LAYER (finegrained or shared) in --modes and print "
                          "its JSON object (for kernel traces of the MFMA-bound path)")
@@ -287,6 +355,12 @@ def main(argv=None) -> int:
 
     L.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.only_stack:
+        ev = HipEvents()
+        res = run_stack(args.stack_steps, 16, ev, modes=[m for m in args.modes.split(",") if m])
+        ev.close()
+        print(json.dumps({"stack": res}), flush=True)
+        return 0
     if args.only_prefill:
         ev = HipEvents()
         res = run_prefill(args.only_prefill, args.prefill_reps, ev, modes=[m for m in args.modes.split(",") if m])
@@ -359,6 +433,12 @@ def main(argv=None) -> int:
         for name in ("finegrained", "shared"):
             log(f"prefill {name}: {args.prefill_reps} timed calls per mode")
             prefill.append(run_prefill(name, args.prefill_reps, ev))
+    stack = None
+    if not args.no_stack:
+        if "wdev" in locals():
+            del wdev
+            torch.cuda.empty_cache()
+        stack = run_stack(args.stack_steps, 16, ev)
     ev.close()
 
     cpu = None
@@ -394,6 +474,7 @@ def main(argv=None) -> int:
         "modes": {name: summary(res) for name, res in results.items()},
         "sweep": sweep,
         "prefill": prefill,
+        "stack": stack,
     }
     print(json.dumps(out), flush=True)
     return 0

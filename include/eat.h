@@ -209,6 +209,60 @@ eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, 
                                       void* ws, size_t ws_bytes, hipStream_t stream,
                                       const hipEvent_t* events, int32_t n_events);
 
+/* ---- stacked layers -------------------------------------------------------
+ *
+ * The paper applies EAT in every MoE layer of a model, each layer keeping
+ * its own account statistics (Sec. 3.2: the accounts are per expert of a
+ * layer; Sec. 4 evaluates whole models).  eat_stack_forward runs one decode
+ * step through n stacked MoE layers the way a decoder interleaves them with
+ * its other blocks, here a normalisation and a residual mixing matrix:
+ *
+ *   u_l     = bf16( h_l / sqrt(mean_j h_l[j]^2 + rms_eps) )     (RMSNorm, unit gain)
+ *   r_l     = bf16( h_l + MoE_l(u_l) )                          (layer l's forward)
+ *   h_{l+1} = bf16( r_l . M_l^T )                               (fp32 accumulation)
+ *
+ * with h_0 = x and h_n written to h_out.  MoE_l is exactly eat_moe_forward
+ * with layer l's handle, weights and accounts (which it reads and updates).
+ * All layers need bf16 activations and experts and the same d_model. */
+typedef struct {
+    eat_handle_t layer;        /* the layer's handle (its mode, E, d_ffn, K, ...)        */
+    const float* w_router;     /* [E][d] fp32                                            */
+    const void* w1;            /* [E][F][d] bf16                                         */
+    const void* w3;            /* [E][F][d] bf16                                         */
+    const void* w2;            /* [E][d][F] bf16                                         */
+    const void* ws1;           /* always-on expert [F_sh][d], [F_sh][d], [d][F_sh] bf16, */
+    const void* ws3;           /*   or NULL when the layer declares none                 */
+    const void* ws2;
+    const void* mix;           /* [d][d] bf16 mixing matrix M_l (row-major, M_l[out][in]) */
+    eat_accounts_t acc;        /* layer l's account state (EAT mode)                     */
+} eat_stack_layer_t;
+
+/* Workspace bytes eat_stack_forward needs for T tokens through `layers`
+ * (host array of n_layers entries).  Errors: EAT_ERR_INVALID_ARG (null
+ * pointers, n_layers outside [1, 1024], T < 0 or above a layer's max_tokens,
+ * different d_model, a null or misaligned mix), EAT_ERR_UNSUPPORTED (a layer
+ * that is not bf16, or d_model not a multiple of 8 or above 8192). */
+eat_status_t eat_stack_workspace_size(const eat_stack_layer_t* layers, int32_t n_layers, int32_t T,
+                                      size_t* bytes);
+
+/* One step of T tokens through the stacked layers (formulas above).
+ *   layers     host array [n_layers]; device pointers inside, 16-byte aligned
+ *   x          [T][d] bf16 input h_0 (device, read only)
+ *   ppl_trend  [T] int8 or NULL, passed to every layer (Sec. 3.3)
+ *   rms_eps    RMSNorm epsilon (finite, >= 0)
+ *   h_out      [T][d] bf16 output h_n (device; must not alias x)
+ *   masks_out  [n_layers][T] uint64 selection masks, or NULL
+ *   probs_out  every layer's router probabilities p (Sec. 3.1), layer after
+ *              layer, [T][E_l] fp32 each (T * sum of E_l floats), or NULL
+ *   ws         device workspace of eat_stack_workspace_size bytes, 256-byte aligned
+ * Enqueues on `stream` only; no host synchronisation, no allocation.  Every
+ * layer's accounts are updated as its eat_moe_forward would (EAT mode).
+ * Errors: as eat_stack_workspace_size and eat_moe_forward, checked on the
+ * host before anything is enqueued; EAT_ERR_HIP if a launch fails. */
+eat_status_t eat_stack_forward(const eat_stack_layer_t* layers, int32_t n_layers, const void* x, int32_t T,
+                               const int8_t* ppl_trend, float rms_eps, void* h_out, uint64_t* masks_out,
+                               float* probs_out, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Static description of a status code (never NULL). */
 const char* eat_status_string(eat_status_t s);
 

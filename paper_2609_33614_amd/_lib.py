@@ -45,6 +45,12 @@ class eat_accounts_t(C.Structure):
     _fields_ = [("n", C.c_void_p), ("p_total", C.c_void_p), ("c_s", C.c_void_p)]
 
 
+class eat_stack_layer_t(C.Structure):
+    _fields_ = [("layer", C.c_void_p), ("w_router", C.c_void_p), ("w1", C.c_void_p), ("w3", C.c_void_p),
+                ("w2", C.c_void_p), ("ws1", C.c_void_p), ("ws3", C.c_void_p), ("ws2", C.c_void_p),
+                ("mix", C.c_void_p), ("acc", eat_accounts_t)]
+
+
 _lib = None
 
 
@@ -70,10 +76,14 @@ def load() -> C.CDLL:
     lib.eat_moe_forward.argtypes = [P, P, C.c_int32, P, P, P, P, P, P, P, eat_accounts_t, P, P, P, P, P,
                                     C.c_size_t, P]
     lib.eat_moe_forward_profiled.argtypes = lib.eat_moe_forward.argtypes + [P, C.c_int32]
+    if hasattr(lib, "eat_stack_forward"):
+        lib.eat_stack_workspace_size.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(C.c_size_t)]
+        lib.eat_stack_forward.argtypes = [P, C.c_int32, P, C.c_int32, P, C.c_float, P, P, P, P, C.c_size_t, P]
     lib.eat_status_string.argtypes = [C.c_int]
     lib.eat_status_string.restype = C.c_char_p
     for name in ("eat_params_default", "eat_create", "eat_destroy", "eat_workspace_size", "eat_route_workspace_size",
-                 "eat_reset_accounts", "eat_route", "eat_moe_forward", "eat_moe_forward_profiled"):
+                 "eat_reset_accounts", "eat_route", "eat_moe_forward", "eat_moe_forward_profiled",
+                 "eat_stack_workspace_size", "eat_stack_forward"):
         if hasattr(lib, name):
             getattr(lib, name).restype = st
     _lib = lib
@@ -178,3 +188,24 @@ def eat_moe_forward_profiled(handle: int, x, T: int, w_router, w1, w3, w2, ws1, 
                                            _ptr(y), _ptr(mask_out), _ptr(expert_load_out), _ptr(ws),
                                            int(ws_bytes), _stream(stream), arr, len(events)),
            "eat_moe_forward_profiled")
+
+
+def stack_layers(entries) -> "C.Array":
+    """Host array of eat_stack_layer_t from a sequence of eat_stack_layer_t."""
+    entries = list(entries)
+    return (eat_stack_layer_t * len(entries))(*entries)
+
+
+def eat_stack_workspace_size(layers, n_layers: int, T: int) -> int:
+    b = C.c_size_t()
+    _check(load().eat_stack_workspace_size(C.cast(layers, C.c_void_p) if layers is not None else None,
+                                           int(n_layers), int(T), C.byref(b)), "eat_stack_workspace_size")
+    return b.value
+
+
+def eat_stack_forward(layers, n_layers: int, x, T: int, ppl_trend, rms_eps: float, h_out, masks_out, probs_out,
+                      ws, ws_bytes: int, stream=None) -> None:
+    _check(load().eat_stack_forward(C.cast(layers, C.c_void_p) if layers is not None else None, int(n_layers),
+                                    _ptr(x), int(T), _ptr(ppl_trend), float(rms_eps), _ptr(h_out),
+                                    _ptr(masks_out), _ptr(probs_out), _ptr(ws), int(ws_bytes), _stream(stream)),
+           "eat_stack_forward")

@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <functional>
 #include <new>
 
@@ -180,14 +181,16 @@ eat_status_t eat_route(eat_handle_t h, const void* x, int32_t T, const float* w_
     return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;
 }
 
-eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, const float* w_router,
-                                      const void* w1, const void* w3, const void* w2, const void* ws1,
-                                      const void* ws3, const void* ws2, eat_accounts_t acc,
-                                      const int8_t* ppl_trend, void* y, uint64_t* mask_out,
-                                      int32_t* expert_load_out, void* ws, size_t ws_bytes, hipStream_t stream,
-                                      const hipEvent_t* events, int32_t n_events) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks shared by the forward entry points (host only).
+eat_status_t check_forward(const eat_ctx* h, const void* x, int32_t T, const float* w_router, const void* w1,
+                           const void* w3, const void* w2, const void* ws1, const void* ws3, const void* ws2,
+                           const eat_accounts_t& acc, const void* y, const uint64_t* mask_out,
+                           const int32_t* expert_load_out) {
     if (!h || T < 0 || T > h->max_tokens) return EAT_ERR_INVALID_ARG;
-    if (n_events < 0 || n_events > EAT_NUM_STAGE_EVENTS || (n_events > 0 && !events)) return EAT_ERR_INVALID_ARG;
     const eat_params_t& p = h->p;
     if (!x || !w_router || !w1 || !w3 || !w2 || !y) return EAT_ERR_INVALID_ARG;
     const void* a16[] = {x, w_router, w1, w3, w2, y};
@@ -201,17 +204,22 @@ eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, 
     }
     if ((mask_out && !aligned(mask_out, 8)) || (expert_load_out && !aligned(expert_load_out, 4)))
         return EAT_ERR_INVALID_ARG;
-    const eat_status_t st = check_accounts(*h, acc);
-    if (st != EAT_OK) return st;
-    const eat::Workspace w = eat::plan_workspace(*h, T);
-    if (T > 0 && (!ws || ws_bytes < w.total)) return EAT_ERR_WORKSPACE;
-    if (ws && !aligned(ws, 256)) return EAT_ERR_INVALID_ARG;
-    if (T == 0) return EAT_OK;
+    return check_accounts(*h, acc);
+}
 
+// Enqueue one layer forward (arguments already checked, T > 0, workspace
+// large enough).  `residual` (bf16 [T][d] or null) is added to y.
+hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float* w_router, const void* w1,
+                        const void* w3, const void* w2, const void* ws1, const void* ws3, const void* ws2,
+                        eat_accounts_t acc, const int8_t* ppl_trend, const uint16_t* residual, void* y,
+                        uint64_t* mask_out, int32_t* expert_load_out, float* prob_out, void* ws,
+                        hipStream_t stream, const hipEvent_t* events, int32_t n_events) {
+    const eat_params_t& p = h.p;
+    const eat::Workspace w = eat::plan_workspace(h, T);
     char* base = static_cast<char*>(ws);
     eat::Buffers b;
     b.lpart = reinterpret_cast<float*>(base + w.lpart);
-    b.prob = reinterpret_cast<float*>(base + w.prob);
+    b.prob = prob_out ? prob_out : reinterpret_cast<float*>(base + w.prob);
     b.gate = reinterpret_cast<float*>(base + w.gate);
     b.mask = mask_out ? mask_out : reinterpret_cast<uint64_t*>(base + w.mask);
     b.k = reinterpret_cast<int32_t*>(base + w.k);
@@ -226,7 +234,6 @@ eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, 
     b.hs = base + w.hs;
     b.ys = reinterpret_cast<float*>(base + w.ys);
 
-    (void)hipGetLastError();
     hipError_t e = hipSuccess;
     auto mark = [&](int stage) {
         if (e == hipSuccess && stage < n_events && events[stage]) e = hipEventRecord(events[stage], stream);
@@ -266,12 +273,137 @@ eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, 
     }
     mark(EAT_STAGE_SHARED);
     if (e == hipSuccess)
-        e = eat::launch_combine(p, T, b.mask, b.gate, b.inv, b.yp, shared ? b.ys : nullptr, y, b.nrm2, w.splits,
-                                w.rows * p.d_model, stream);
+        e = eat::launch_combine(p, T, b.mask, b.gate, b.inv, b.yp, shared ? b.ys : nullptr, residual, y, b.nrm2,
+                                w.splits, w.rows * p.d_model, stream);
     mark(EAT_STAGE_COMBINED);
     if (e == hipSuccess && p.mode == EAT_MODE_EAT)
         e = eat::launch_update_accounts(p, b.offsets, b.tok_idx, b.prob, b.nrm2, acc, stream);
     mark(EAT_STAGE_END);
+    return e;
+}
+
+// Stacked-layer workspace: the largest layer workspace, then u, r and two
+// h rows (bf16 [T][d] each), then the mixing GEMM's fp32 slices.
+struct StackPlan {
+    size_t layer, u, r, h0, h1, mix, total;
+    int splits;
+};
+
+StackPlan plan_stack(const eat_stack_layer_t* layers, int32_t n, int32_t T) {
+    StackPlan s{};
+    auto up = [](size_t v) { return (v + 255) & ~static_cast<size_t>(255); };
+    size_t lw = 0;
+    for (int32_t l = 0; l < n; ++l) lw = std::max(lw, eat::plan_workspace(*layers[l].layer, T).total);
+    const int d = layers[0].layer->p.d_model;
+    const size_t row = up(static_cast<size_t>(T) * d * 2);
+    s.splits = eat::dense_splits(d, d, T);
+    s.layer = 0;
+    s.u = up(lw);
+    s.r = s.u + row;
+    s.h0 = s.r + row;
+    s.h1 = s.h0 + row;
+    s.mix = s.h1 + row;
+    s.total = s.mix + up(static_cast<size_t>(s.splits) * T * d * 4);
+    return s;
+}
+
+eat_status_t check_stack(const eat_stack_layer_t* layers, int32_t n, int32_t T) {
+    if (!layers || n < 1 || n > 1024 || T < 0) return EAT_ERR_INVALID_ARG;
+    for (int32_t l = 0; l < n; ++l) {
+        const eat_ctx* c = layers[l].layer;
+        if (!c || T > c->max_tokens) return EAT_ERR_INVALID_ARG;
+        if (c->p.act_dtype != EAT_BF16 || c->p.expert_dtype != EAT_BF16) return EAT_ERR_UNSUPPORTED;
+        if (c->p.d_model != layers[0].layer->p.d_model) return EAT_ERR_INVALID_ARG;
+        if (!layers[l].mix || !aligned(layers[l].mix, 16)) return EAT_ERR_INVALID_ARG;
+    }
+    if (!eat::mix_norm_fits(layers[0].layer->p.d_model)) return EAT_ERR_UNSUPPORTED;
+    return EAT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+eat_status_t eat_moe_forward_profiled(eat_handle_t h, const void* x, int32_t T, const float* w_router,
+                                      const void* w1, const void* w3, const void* w2, const void* ws1,
+                                      const void* ws3, const void* ws2, eat_accounts_t acc,
+                                      const int8_t* ppl_trend, void* y, uint64_t* mask_out,
+                                      int32_t* expert_load_out, void* ws, size_t ws_bytes, hipStream_t stream,
+                                      const hipEvent_t* events, int32_t n_events) {
+    if (n_events < 0 || n_events > EAT_NUM_STAGE_EVENTS || (n_events > 0 && !events)) return EAT_ERR_INVALID_ARG;
+    const eat_status_t st = check_forward(h, x, T, w_router, w1, w3, w2, ws1, ws3, ws2, acc, y, mask_out,
+                                          expert_load_out);
+    if (st != EAT_OK) return st;
+    const eat::Workspace w = eat::plan_workspace(*h, T);
+    if (T > 0 && (!ws || ws_bytes < w.total)) return EAT_ERR_WORKSPACE;
+    if (ws && !aligned(ws, 256)) return EAT_ERR_INVALID_ARG;
+    if (T == 0) return EAT_OK;
+    (void)hipGetLastError();
+    const hipError_t e = forward_impl(*h, x, T, w_router, w1, w3, w2, ws1, ws3, ws2, acc, ppl_trend, nullptr, y,
+                                      mask_out, expert_load_out, nullptr, ws, stream, events, n_events);
+    return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;
+}
+
+eat_status_t eat_stack_workspace_size(const eat_stack_layer_t* layers, int32_t n_layers, int32_t T,
+                                      size_t* bytes) {
+    if (!bytes) return EAT_ERR_INVALID_ARG;
+    const eat_status_t st = check_stack(layers, n_layers, T);
+    if (st != EAT_OK) return st;
+    *bytes = plan_stack(layers, n_layers, T).total;
+    return EAT_OK;
+}
+
+eat_status_t eat_stack_forward(const eat_stack_layer_t* layers, int32_t n_layers, const void* x, int32_t T,
+                               const int8_t* ppl_trend, float rms_eps, void* h_out, uint64_t* masks_out,
+                               float* probs_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+    eat_status_t st = check_stack(layers, n_layers, T);
+    if (st != EAT_OK) return st;
+    if (!x || !h_out || !aligned(x, 16) || !aligned(h_out, 16)) return EAT_ERR_INVALID_ARG;
+    if ((masks_out && !aligned(masks_out, 8)) || (probs_out && !aligned(probs_out, 4))) return EAT_ERR_INVALID_ARG;
+    if (!(rms_eps >= 0.0f) || !std::isfinite(rms_eps)) return EAT_ERR_INVALID_ARG;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        const eat_stack_layer_t& L = layers[l];
+        st = check_forward(L.layer, x, T, L.w_router, L.w1, L.w3, L.w2, L.ws1, L.ws3, L.ws2, L.acc, h_out,
+                           masks_out, nullptr);
+        if (st != EAT_OK) return st;
+    }
+    const StackPlan sp = plan_stack(layers, n_layers, T);
+    if (T > 0 && (!ws || ws_bytes < sp.total)) return EAT_ERR_WORKSPACE;
+    if (ws && !aligned(ws, 256)) return EAT_ERR_INVALID_ARG;
+    if (T == 0) return EAT_OK;
+
+    char* base = static_cast<char*>(ws);
+    uint16_t* u = reinterpret_cast<uint16_t*>(base + sp.u);
+    uint16_t* r = reinterpret_cast<uint16_t*>(base + sp.r);
+    uint16_t* hb[2] = {reinterpret_cast<uint16_t*>(base + sp.h0), reinterpret_cast<uint16_t*>(base + sp.h1)};
+    float* mix = reinterpret_cast<float*>(base + sp.mix);
+    const int d = layers[0].layer->p.d_model;
+    const int64_t stride = static_cast<int64_t>(T) * d;
+
+    (void)hipGetLastError();
+    size_t prob_off = 0;                      // layer l's probabilities start after T * E_j of the layers before
+    // u_0 = bf16(RMSNorm(x))
+    hipError_t e = eat::launch_mix_norm(nullptr, 0, 0, static_cast<const uint16_t*>(x), T, d, rms_eps, nullptr, u,
+                                        stream);
+    const uint16_t* h = static_cast<const uint16_t*>(x);
+    for (int32_t l = 0; l < n_layers && e == hipSuccess; ++l) {
+        const eat_stack_layer_t& L = layers[l];
+        // r = bf16(h + MoE_l(u))
+        e = forward_impl(*L.layer, u, T, L.w_router, L.w1, L.w3, L.w2, L.ws1, L.ws3, L.ws2, L.acc, ppl_trend, h, r,
+                         masks_out ? masks_out + static_cast<size_t>(l) * T : nullptr, nullptr,
+                         probs_out ? probs_out + prob_off : nullptr, base + sp.layer, stream, nullptr, 0);
+        prob_off += static_cast<size_t>(T) * L.layer->p.E;
+        // h' = bf16(r M_l^T); u = bf16(RMSNorm(h')) for the next layer
+        if (e == hipSuccess)
+            e = eat::launch_dense_bf16(r, T, static_cast<const uint16_t*>(L.mix), d, d, mix, sp.splits, stride,
+                                       stream);
+        const bool last = l + 1 == n_layers;
+        uint16_t* hn = last ? static_cast<uint16_t*>(h_out) : hb[l & 1];
+        if (e == hipSuccess)
+            e = eat::launch_mix_norm(mix, sp.splits, stride, nullptr, T, d, rms_eps, hn, last ? nullptr : u,
+                                     stream);
+        h = hn;
+    }
     return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;
 }
 

@@ -1,11 +1,15 @@
-// Combine and account kernels (gfx950).
+// Combine, account and stacked-layer kernels (gfx950).
 //
 // combine: per token and 1024-element slice of d, gathers the token's expert
 // rows in increasing expert order, adds the split-K partials of each row (in
 // split order), writes each row slice's sum of squares, and accumulates
-// y_t = sum_e g_norm,t,e o_t,e (+ shared expert) in fp32 (Eq. 7-8 and the
-// weighted fusion of Sec. 3.4).  No atomics: every output element has one
-// writer and a fixed summation order.
+// y_t = sum_e g_norm,t,e o_t,e (+ shared expert) (+ a residual row) in fp32
+// (Eq. 7-8 and the weighted fusion of Sec. 3.4).  No atomics: every output
+// element has one writer and a fixed summation order.
+//
+// mix_norm: between stacked layers, h' = bf16(sum of the mixing GEMM's
+// split partials) and the next layer's input u = bf16(h' / rms(h')), one
+// workgroup per token.
 //
 // accounts: one workgroup per expert reduces its contiguous row segment in fp64
 // and applies the Sec. 3.2 bookkeeping once per call:
@@ -29,6 +33,7 @@ struct CombineArgs {
     const int32_t* inv;
     const float* yp;           // [splits][rows_cap][d]
     const float* ys;           // [T][d] shared output or null
+    const uint16_t* res;       // [T][d] bf16 residual rows added to y, or null
     void* y;
     float* nrm2;               // [rows_cap][nchunk] partial sums of squares
     int64_t split_stride;
@@ -82,6 +87,13 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
         const float4 q = *reinterpret_cast<const float4*>(a.ys + static_cast<size_t>(t) * a.d + 4 * j);
         acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
     }
+    if (a.res) {
+        const uint2 q = *reinterpret_cast<const uint2*>(a.res + static_cast<size_t>(t) * a.d + 4 * j);
+        acc.x += bf16_to_f32(static_cast<uint16_t>(q.x & 0xffffu));
+        acc.y += bf16_to_f32(static_cast<uint16_t>(q.x >> 16));
+        acc.z += bf16_to_f32(static_cast<uint16_t>(q.y & 0xffffu));
+        acc.w += bf16_to_f32(static_cast<uint16_t>(q.y >> 16));
+    }
     if constexpr (sizeof(YT) == 4) {
         *reinterpret_cast<float4*>(static_cast<float*>(a.y) + static_cast<size_t>(t) * a.d + 4 * j) = acc;
     } else {
@@ -124,6 +136,72 @@ __global__ __launch_bounds__(kThreads) void update_accounts_kernel(
     }
 }
 
+// One workgroup per token row of d <= kMixMax elements: v = the row's
+// split partials added in split order (or the bf16 source row), h = bf16(v)
+// (written when h_out is set), then u = bf16(h * (1 / sqrt(mean(h^2) + eps)))
+// with the sum of squares taken over the bf16 values, per thread then per
+// wave (butterfly) then over the waves in order.
+constexpr int kMixVec = 4;                                  // floats per thread and group
+constexpr int kMixGroups = 8;                               // d <= 256 * 4 * 8 = 8192
+__global__ __launch_bounds__(kThreads) void mix_norm_kernel(const float* __restrict__ part, int splits,
+                                                            int64_t split_stride, const uint16_t* __restrict__ src,
+                                                            int d, float eps, uint16_t* __restrict__ h_out,
+                                                            uint16_t* __restrict__ u_out) {
+    __shared__ float red[kWaves];
+    const int t = blockIdx.x;
+    const int lane = lane_id(), wave = threadIdx.x / kWave;
+    float v[kMixGroups][kMixVec];
+    float ss = 0.f;
+#pragma unroll
+    for (int g = 0; g < kMixGroups; ++g) {
+        const int j = (g * kThreads + threadIdx.x) * kMixVec;
+        if (j >= d) continue;
+        const size_t o = static_cast<size_t>(t) * d + j;
+        if (splits > 0) {
+            float4 q = *reinterpret_cast<const float4*>(part + o);
+            for (int sp = 1; sp < splits; ++sp) {
+                const float4 r = *reinterpret_cast<const float4*>(part + sp * split_stride + o);
+                q.x += r.x; q.y += r.y; q.z += r.z; q.w += r.w;
+            }
+            v[g][0] = bf16_to_f32(f32_to_bf16(q.x)); v[g][1] = bf16_to_f32(f32_to_bf16(q.y));
+            v[g][2] = bf16_to_f32(f32_to_bf16(q.z)); v[g][3] = bf16_to_f32(f32_to_bf16(q.w));
+        } else {
+            const uint2 q = *reinterpret_cast<const uint2*>(src + o);
+            v[g][0] = bf16_to_f32(static_cast<uint16_t>(q.x & 0xffffu));
+            v[g][1] = bf16_to_f32(static_cast<uint16_t>(q.x >> 16));
+            v[g][2] = bf16_to_f32(static_cast<uint16_t>(q.y & 0xffffu));
+            v[g][3] = bf16_to_f32(static_cast<uint16_t>(q.y >> 16));
+        }
+#pragma unroll
+        for (int i = 0; i < kMixVec; ++i) ss = fmaf(v[g][i], v[g][i], ss);
+        if (h_out) {
+            uint2 pk;
+            pk.x = static_cast<uint32_t>(f32_to_bf16(v[g][0])) | (static_cast<uint32_t>(f32_to_bf16(v[g][1])) << 16);
+            pk.y = static_cast<uint32_t>(f32_to_bf16(v[g][2])) | (static_cast<uint32_t>(f32_to_bf16(v[g][3])) << 16);
+            *reinterpret_cast<uint2*>(h_out + o) = pk;
+        }
+    }
+    if (!u_out) return;
+    ss = wave_sum(ss);
+    if (lane == 0) red[wave] = ss;
+    __syncthreads();
+    float tot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) tot += red[w];
+    const float scale = 1.0f / sqrtf(tot / static_cast<float>(d) + eps);
+#pragma unroll
+    for (int g = 0; g < kMixGroups; ++g) {
+        const int j = (g * kThreads + threadIdx.x) * kMixVec;
+        if (j >= d) continue;
+        uint2 pk;
+        pk.x = static_cast<uint32_t>(f32_to_bf16(v[g][0] * scale)) |
+               (static_cast<uint32_t>(f32_to_bf16(v[g][1] * scale)) << 16);
+        pk.y = static_cast<uint32_t>(f32_to_bf16(v[g][2] * scale)) |
+               (static_cast<uint32_t>(f32_to_bf16(v[g][3] * scale)) << 16);
+        *reinterpret_cast<uint2*>(u_out + static_cast<size_t>(t) * d + j) = pk;
+    }
+}
+
 __global__ __launch_bounds__(kWave) void reset_accounts_kernel(int E, int64_t* n, float* p, float* c) {
     const int e = lane_id();
     if (e < E) { n[e] = 0; p[e] = 0.f; c[e] = 0.f; }
@@ -134,10 +212,10 @@ __global__ __launch_bounds__(kWave) void reset_accounts_kernel(int E, int64_t* n
 int combine_chunks(const eat_params_t& p) { return (p.d_model / 4 + kThreads - 1) / kThreads; }
 
 hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask, const float* gate,
-                          const int32_t* inv, const float* yp, const float* ys, void* y, float* nrm2,
-                          int splits, int64_t split_stride, hipStream_t s) {
+                          const int32_t* inv, const float* yp, const float* ys, const uint16_t* residual,
+                          void* y, float* nrm2, int splits, int64_t split_stride, hipStream_t s) {
     const int nchunk = combine_chunks(p);
-    CombineArgs a{mask, gate, inv, yp, ys, y, nrm2, split_stride, splits, T, p.E, p.d_model, nchunk};
+    CombineArgs a{mask, gate, inv, yp, ys, residual, y, nrm2, split_stride, splits, T, p.E, p.d_model, nchunk};
     const dim3 grid(T, nchunk);
     if (p.act_dtype == EAT_BF16) combine_kernel<uint16_t><<<grid, kThreads, 0, s>>>(a);
     else combine_kernel<float><<<grid, kThreads, 0, s>>>(a);
@@ -148,6 +226,14 @@ hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets,
                                   const float* prob, const float* nrm2, eat_accounts_t acc, hipStream_t s) {
     update_accounts_kernel<<<p.E, kThreads, 0, s>>>(offsets, tok_idx, prob, nrm2, combine_chunks(p), p.E, p.alpha,
                                                  acc.n, acc.p_total, acc.c_s);
+    return hipGetLastError();
+}
+
+bool mix_norm_fits(int d) { return d % (kMixVec * 2) == 0 && d <= kThreads * kMixVec * kMixGroups; }
+
+hipError_t launch_mix_norm(const float* part, int splits, int64_t split_stride, const uint16_t* src, int32_t T,
+                           int d, float eps, uint16_t* h_out, uint16_t* u_out, hipStream_t s) {
+    mix_norm_kernel<<<T, kThreads, 0, s>>>(part, splits, split_stride, src, d, eps, h_out, u_out);
     return hipGetLastError();
 }
 

@@ -92,11 +92,26 @@ hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* 
                               uint16_t* hs, float* ys, hipStream_t s);
 
 // yp holds `splits` partial slices of the down projection, `split_stride`
-// floats apart; they are added in slice order.
+// floats apart; they are added in slice order.  `residual` (bf16 [T][d], or
+// null) is added to y before the cast.
 hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask,
                           const float* gate, const int32_t* inv, const float* yp,
-                          const float* ys, void* y, float* nrm2, int splits,
-                          int64_t split_stride, hipStream_t s);
+                          const float* ys, const uint16_t* residual, void* y, float* nrm2,
+                          int splits, int64_t split_stride, hipStream_t s);
+
+// Between stacked layers (combine.hip): h = bf16(sum of `splits` fp32
+// partial rows, or the bf16 rows of src when splits == 0), written to h_out
+// if set; u = bf16(h / sqrt(mean(h^2) + eps)) written to u_out if set.
+bool mix_norm_fits(int d);
+hipError_t launch_mix_norm(const float* part, int splits, int64_t split_stride, const uint16_t* src,
+                           int32_t T, int d, float eps, uint16_t* h_out, uint16_t* u_out, hipStream_t s);
+
+// Dense bf16 projection out[split][T][M] = src[T][K] . W^T (fp32 slices of
+// the reduction dimension, split_stride floats apart), W [M][K]: the
+// residual mixing of stacked layers (expert.hip).
+int dense_splits(int M, int K, int32_t T);
+hipError_t launch_dense_bf16(const uint16_t* src, int32_t T, const uint16_t* w, int M, int K, float* out,
+                             int splits, int64_t split_stride, hipStream_t s);
 // 1024-element slices of d the combine works in (and nrm2 holds per row).
 int combine_chunks(const eat_params_t& p);
 

@@ -455,6 +455,33 @@ int up_splits(const eat_params_t& p, int32_t T) {
     return stream_splits(p.d_ffn, p.d_model, p, T, EAT_UP_SPLIT_MAX, EAT_UP_SPLIT_WAVES);
 }
 
+// Dense projection (one group of T identity rows): the wide tiles from 384
+// rows, else the plain stream kernel with its reduction dimension split
+// until ~4096 wave tiles exist.
+static bool dense_wide(int M, int K, int32_t T) { return T >= 384 && wide_fits(false, M, K); }
+
+int dense_splits(int M, int K, int32_t T) {
+    if (dense_wide(M, K, T)) return 1;
+    const int64_t bn = 16 * pick_nsub(T);
+    const int64_t waves = static_cast<int64_t>(M / 16) * ((T + bn - 1) / bn);
+    int s = 1;
+    while (s < 8 && K % (64 * 2 * s) == 0 && waves * s < EAT_SPLIT_WAVES) s *= 2;
+    return s;
+}
+
+hipError_t launch_dense_bf16(const uint16_t* src, int32_t T, const uint16_t* w, int M, int K, float* out,
+                             int splits, int64_t split_stride, hipStream_t s) {
+    if (dense_wide(M, K, T)) return launch_wide(false, w, nullptr, src, nullptr, nullptr, 1, T, M, K, out, T, s);
+    const int nsub = pick_nsub(T);
+    const int bn = 16 * nsub;
+    const int tiles = (T + bn - 1) / bn;
+    StreamArgs a{};
+    a.wa = w; a.src = src; a.nrows = T; a.groups = 1; a.M = M; a.K = K; a.ksplit = K / splits;
+    a.split_stride = split_stride; a.out = out;
+    const int cap = std::max(1, 2048 / std::max(1, (M / 64) * splits));
+    return launch_stream<false>(a, nsub, std::min(tiles, cap), splits, s);
+}
+
 hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap, const float* x,
                               const float* w1, const float* w3, const float* w2,
                               const int32_t* offsets, const int32_t* tok_idx,

@@ -91,6 +91,51 @@ class EatLayer:
             pass
 
 
+class EatStack:
+    """Stacked layers (one EatLayer each, own accounts) with their d x d
+    mixing matrices, run one decode step at a time by eat_stack_forward."""
+
+    def __init__(self, params, max_tokens: int, weights, mixes, device: str = "cuda"):
+        self.layers = [EatLayer(p, max_tokens, w, device) for p, w in zip(params, weights)]
+        self.mixes = list(mixes)
+        self.device = torch.device(device)
+        self._ws: Optional[torch.Tensor] = None
+        self._arr = None
+
+    def _entries(self):
+        out = []
+        for lay, m in zip(self.layers, self.mixes):
+            w = lay.w
+            out.append(L.eat_stack_layer_t(lay.handle, L._ptr(w["w_router"]), L._ptr(w["w1"]), L._ptr(w["w3"]),
+                                           L._ptr(w["w2"]), L._ptr(w.get("ws1")), L._ptr(w.get("ws3")),
+                                           L._ptr(w.get("ws2")), L._ptr(m), lay.acc))
+        return L.stack_layers(out)
+
+    def reset_accounts(self, stream=None) -> None:
+        for lay in self.layers:
+            lay.reset_accounts(stream)
+
+    def forward(self, x: torch.Tensor, trend: Optional[torch.Tensor] = None, h_out: Optional[torch.Tensor] = None,
+                masks_out: Optional[torch.Tensor] = None, probs_out: Optional[torch.Tensor] = None,
+                rms_eps: float = 1e-6, stream=None) -> torch.Tensor:
+        T = x.shape[0]
+        if h_out is None:
+            h_out = torch.empty_like(x)
+        if self._arr is None:
+            self._arr = self._entries()
+        n = len(self.layers)
+        need = L.eat_stack_workspace_size(self._arr, n, T)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        L.eat_stack_forward(self._arr, n, x, T, trend, rms_eps, h_out, masks_out, probs_out, self._ws,
+                            self._ws.numel(), stream)
+        return h_out
+
+    def close(self) -> None:
+        for lay in self.layers:
+            lay.close()
+
+
 def to_device(weights: Dict, device: str = "cuda") -> Dict[str, torch.Tensor]:
     """Upload generator output (fp32 arrays or bf16 bit patterns as uint16)
     to device tensors (torch.bfloat16 for bf16)."""

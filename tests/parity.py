@@ -22,10 +22,14 @@ TOL_C_BF16 = 1e-2
 TOL_P_TOTAL = 1e-5
 
 
-def borderline(r: O.Routing, prm: O.Params, eps_b: float = EPS_B) -> np.ndarray:
+def borderline(r: O.Routing, prm: O.Params, eps_b=EPS_B) -> np.ndarray:
+    """Tokens whose selection the oracle's values decide within the band
+    ``eps_b`` (a scalar, or one band per token)."""
     T, E = r.p.shape
     out = np.zeros(T, dtype=bool)
+    bands = np.broadcast_to(np.asarray(eps_b, dtype=np.float64), (T,))
     for t in range(T):
+        eps_b = float(bands[t])
         p = r.p[t]
         if prm.mode == O.MODE_EAT:
             I = r.I[t]

@@ -46,6 +46,10 @@ def test_struct_layout_matches_header(tmp_path):
              'printf("%zu\\n", sizeof(eat_accounts_t));']
     for f in fields:
         lines.append(f'printf("%zu\\n", offsetof(eat_params_t, {f}));')
+    sfields = [f for f, _ in L.eat_stack_layer_t._fields_]
+    lines.append('printf("%zu\\n", sizeof(eat_stack_layer_t));')
+    for f in sfields:
+        lines.append(f'printf("%zu\\n", offsetof(eat_stack_layer_t, {f}));')
     lines.append("return 0;}")
     c = tmp_path / "probe.c"
     c.write_text("\n".join(lines))
@@ -58,6 +62,10 @@ def test_struct_layout_matches_header(tmp_path):
     assert out[1] == C.sizeof(L.eat_accounts_t)
     for f, off in zip(fields, out[2:]):
         assert getattr(L.eat_params_t, f).offset == off, f
+    rest = out[2 + len(fields):]
+    assert rest[0] == C.sizeof(L.eat_stack_layer_t)
+    for f, off in zip(sfields, rest[1:]):
+        assert getattr(L.eat_stack_layer_t, f).offset == off, f
 
 
 def test_defaults_are_the_papers_table():
@@ -219,3 +227,62 @@ def test_status_strings():
     for s in range(6):
         assert isinstance(eat.eat_status_string(s), str) and eat.eat_status_string(s)
     assert eat.eat_status_string(99) == "unknown status"
+
+
+def _stack_entry(h, **kw):
+    e = dict(layer=h, w_router=FAKE, w1=FAKE, w3=FAKE, w2=FAKE, ws1=None, ws3=None, ws2=None, mix=FAKE,
+             acc=L.accounts(FAKE, FAKE, FAKE))
+    e.update(kw)
+    return L.eat_stack_layer_t(e["layer"], e["w_router"], e["w1"], e["w3"], e["w2"], e["ws1"], e["ws3"], e["ws2"],
+                               e["mix"], e["acc"])
+
+
+def test_stack_validation_happens_on_the_host():
+    bf = dict(act_dtype=eat.EAT_BF16, expert_dtype=eat.EAT_BF16)
+    hs = [eat.eat_create(_params(**bf), 16) for _ in range(3)]
+    h_f32 = eat.eat_create(_params(), 16)
+    h_d256 = eat.eat_create(_params(d_model=256, **bf), 16)
+    try:
+        arr = L.stack_layers([_stack_entry(h) for h in hs])
+        need = eat.eat_stack_workspace_size(arr, 3, 4)
+        assert need > eat.eat_workspace_size(hs[0], 4)
+        assert eat.eat_stack_workspace_size(arr, 3, 8) > need
+        base = dict(x=FAKE, T=4, ppl_trend=None, rms_eps=1e-6, h_out=FAKE, masks_out=None, probs_out=None, ws=FAKE,
+                    ws_bytes=need, stream=0)
+        cases = [
+            (dict(n_layers=0), L.EAT_ERR_INVALID_ARG),
+            (dict(T=17), L.EAT_ERR_INVALID_ARG),                      # above the layers' max_tokens
+            (dict(x=None), L.EAT_ERR_INVALID_ARG),
+            (dict(h_out=FAKE + 8), L.EAT_ERR_INVALID_ARG),
+            (dict(rms_eps=-1.0), L.EAT_ERR_INVALID_ARG),
+            (dict(rms_eps=float("nan")), L.EAT_ERR_INVALID_ARG),
+            (dict(ws_bytes=need - 1), L.EAT_ERR_WORKSPACE),
+            (dict(ws=FAKE + 128), L.EAT_ERR_INVALID_ARG),
+            (dict(masks_out=FAKE + 4), L.EAT_ERR_INVALID_ARG),
+            (dict(probs_out=FAKE + 2), L.EAT_ERR_INVALID_ARG),
+        ]
+        for kw, status in cases:
+            args = dict(base, n_layers=3); args.update(kw)
+            with pytest.raises(eat.EatError) as ei:
+                eat.eat_stack_forward(arr, **args)
+            assert ei.value.status == status, kw
+        bad_layers = [
+            ([_stack_entry(hs[0]), _stack_entry(h_f32)], L.EAT_ERR_UNSUPPORTED),      # fp32 layer
+            ([_stack_entry(hs[0]), _stack_entry(h_d256)], L.EAT_ERR_INVALID_ARG),     # different d_model
+            ([_stack_entry(hs[0], mix=None)], L.EAT_ERR_INVALID_ARG),
+            ([_stack_entry(hs[0], mix=FAKE + 2)], L.EAT_ERR_INVALID_ARG),
+            ([_stack_entry(hs[0], w2=None)], L.EAT_ERR_INVALID_ARG),
+            ([_stack_entry(hs[0], acc=L.accounts(FAKE, None, FAKE))], L.EAT_ERR_INVALID_ARG),
+            ([_stack_entry(hs[0], ws1=FAKE)], L.EAT_ERR_INVALID_ARG),                 # no shared expert declared
+            ([_stack_entry(None)], L.EAT_ERR_INVALID_ARG),
+        ]
+        for entries, status in bad_layers:
+            a2 = L.stack_layers(entries)
+            with pytest.raises(eat.EatError) as ei:
+                eat.eat_stack_forward(a2, len(entries), FAKE, 4, None, 1e-6, FAKE, None, None, FAKE, 1 << 40, stream=0)
+            assert ei.value.status == status
+        # an empty step is valid and launches nothing
+        eat.eat_stack_forward(arr, 3, FAKE, 0, None, 1e-6, FAKE, None, None, None, 0, stream=0)
+    finally:
+        for h in hs + [h_f32, h_d256]:
+            eat.eat_destroy(h)
