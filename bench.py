@@ -7,7 +7,11 @@ of width 14336, bf16 experts, fp32 router and accounts, logits scaled by
 from a seeded 16-cluster Gaussian mixture (cluster-sticky per sequence,
 10% re-draw per step), accounts starting at zero.  A step is one whole
 layer forward (route, permute, experts, combine, account update) over one
-batch; all inputs are resident in HBM before timing starts.
+batch; all inputs are resident in HBM before timing starts.  Steps are
+launched eagerly (the host enqueues ahead of the GPU), with HIP events
+around the expert kernels of every step.  ``--graph`` also replays one
+captured step per step (input copied in, masks copied out inside the timed
+region) and reports that as the headline.
 
 Prints one JSON line: EAT tokens/s (``value``), the Top-K (K=2) and Top-P
 (p=0.6) baselines on the same inputs, mean activated experts per token,
@@ -96,11 +100,16 @@ def union_sizes(masks: np.ndarray) -> np.ndarray:
     return np.array(out)
 
 
-def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bool):
+def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bool, graph: bool = False):
+    """`steps` timed decode steps after `warmup` untimed ones on scratch
+    accounts.  profile: eager launches with HIP events around the expert
+    kernels of every step.  graph: one step captured in a HIP graph and
+    replayed per step (the step's input copied into the captured buffer and
+    its masks copied out, both inside the timed region)."""
     import torch
 
     from paper_2609_33614_amd import _lib as L
-    from paper_2609_33614_amd.layer import EatLayer
+    from paper_2609_33614_amd.layer import EatLayer, capture
 
     p = L.eat_params_default(mode=mode, E=shape.E, d_model=shape.d, d_ffn=shape.F, top_k=shape.K,
                              top_p=0.6, inv_temperature=shape.inv_temp)
@@ -112,6 +121,8 @@ def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bo
     # warm-up on a scratch account state, then start from zero accounts
     for s in range(warmup):
         lay.forward(xs[s % xs.shape[0]], y=y, mask_out=scratch)
+    x_in = xs[0].clone()
+    g = capture(lambda: lay.forward(x_in, y=y, mask_out=scratch)) if graph else None
     lay.reset_accounts()
     torch.cuda.synchronize()
 
@@ -124,7 +135,11 @@ def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bo
     ev.hip.hipEventRecord(t0, stream.cuda_stream)
     for s in range(steps):
         x = xs[warmup + s]
-        if profile:
+        if g is not None:
+            x_in.copy_(x)
+            g.replay()
+            masks[s].copy_(scratch)
+        elif profile:
             stage[L.EAT_STAGE_PERMUTED] = evs[3 * s]
             stage[L.EAT_STAGE_UP] = evs[3 * s + 1]
             stage[L.EAT_STAGE_DOWN] = evs[3 * s + 2]
@@ -142,6 +157,7 @@ def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bo
     k = popcounts(m)
     U = union_sizes(m)
     acc = lay.accounts_host()
+    del g
     lay.close()
     return dict(total_ms=total_ms, up_ms=up_ms, dn_ms=dn_ms, k=k, U=U, E=E, accounts=acc)
 
@@ -331,6 +347,8 @@ def main(argv=None) -> int:
     ap.add_argument("--modes", default="eat,topk,topp", help="routing modes to time (eat first)")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill (MFMA-bound) measurement")
     ap.add_argument("--prefill-reps", type=int, default=10)
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the decode steps as HIP graph replays and report those as the headline")
     ap.add_argument("--no-stack", action="store_true", help="skip the 16-layer stack measurement")
     ap.add_argument("--stack-steps", type=int, default=1024)
     ap.add_argument("--only-stack", action="store_true", help="time only the 16-layer stack and print its JSON")
@@ -389,24 +407,30 @@ def main(argv=None) -> int:
         del src, dst
         log(f"copy calibration: 4 x {args.calibrate_copy} MiB read + written")
 
-    results = {}
+    results, graphed = {}, {}
     modes = [m for m in args.modes.split(",") if m]
     assert modes and modes[0] == "eat", "the headline mode (eat) is timed first"
     for name in modes:
-        log(f"timing {name}: {K} steps (+{W} warm-up)")
+        log(f"timing {name}: {K} steps (+{W} warm-up), eager with kernel events")
         results[name] = run_mode(L.MODES[name], shape, wdev, xs, B, K, W, ev, profile=True)
+        if args.graph:
+            log(f"timing {name}: {K} steps (+{W} warm-up), HIP graph replay")
+            graphed[name] = run_mode(L.MODES[name], shape, wdev, xs, B, K, W, ev, profile=False, graph=True)
     r = results["eat"]
-    ms_step = r["total_ms"] / K
-    value = B * K / (r["total_ms"] / 1e3)
+    head = graphed.get("eat", r)
+    ms_step = head["total_ms"] / K
+    value = B * K / (head["total_ms"] / 1e3)
 
     up_bytes = np.array([traffic_up(shape, B, r["k"][s], r["U"][s]) for s in range(K)], dtype=np.float64)
     dn_bytes = np.array([traffic_down(shape, r["k"][s], r["U"][s]) for s in range(K)], dtype=np.float64)
     up_gbs = up_bytes.sum() / (r["up_ms"].sum() / 1e3) / 1e9
     dn_gbs = dn_bytes.sum() / (r["dn_ms"].sum() / 1e3) / 1e9
 
-    def summary(res):
-        return {"tokens_per_s": round(B * K / (res["total_ms"] / 1e3), 1),
-                "ms_per_step": round(res["total_ms"] / K, 4),
+    def summary(res, gres):
+        best = gres if gres is not None else res
+        return {"tokens_per_s": round(B * K / (best["total_ms"] / 1e3), 1),
+                "ms_per_step": round(best["total_ms"] / K, 4),
+                "eager_tokens_per_s": round(B * K / (res["total_ms"] / 1e3), 1),
                 "mean_activated_experts": round(float(res["k"].mean()), 4),
                 "mean_experts_touched_per_step": round(float(res["U"].mean()), 3),
                 "up_gate_us_per_launch": round(float(res["up_ms"].mean() * 1e3), 2),
@@ -419,7 +443,7 @@ def main(argv=None) -> int:
             row = {"batch": b}
             for name in ("eat", "topk"):
                 log(f"sweep B={b} {name}")
-                rr = run_mode(L.MODES[name], shape, wdev, xb, b, K, W, ev, profile=False)
+                rr = run_mode(L.MODES[name], shape, wdev, xb, b, K, W, ev, profile=False, graph=args.graph)
                 row[name] = {"tokens_per_s": round(b * K / (rr["total_ms"] / 1e3), 1),
                              "ms_per_step": round(rr["total_ms"] / K, 4),
                              "mean_activated_experts": round(float(rr["k"].mean()), 4),
@@ -461,7 +485,8 @@ def main(argv=None) -> int:
         "data": "synthetic (seeded Gaussian-mixture hidden states, random-init weights)",
         "config": {"workload": "Mixtral-shaped MoE layer decode, EAT routing",
                    "d_model": shape.d, "experts": shape.E, "d_ffn": shape.F, "top_k": shape.K,
-                   "batch": B, "logit_scale": shape.inv_temp, "router": "fp32", "experts_dtype": "bf16"},
+                   "batch": B, "logit_scale": shape.inv_temp, "router": "fp32", "experts_dtype": "bf16",
+                   "launch": "HIP graph replay per step" if args.graph else "eager"},
         "roofline": {"bound": "hbm", "kernel": "expert up/gate (stream_kernel<gated>)",
                      "achieved": round(up_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(up_gbs / HBM_PEAK_GBS, 4),
@@ -471,7 +496,7 @@ def main(argv=None) -> int:
                      "bytes_per_launch": round(float(up_bytes.mean()), 0),
                      "us_per_launch": round(float(r["up_ms"].mean() * 1e3), 2)},
         "cpu_baseline": cpu,
-        "modes": {name: summary(res) for name, res in results.items()},
+        "modes": {name: summary(res, graphed.get(name)) for name, res in results.items()},
         "sweep": sweep,
         "prefill": prefill,
         "stack": stack,

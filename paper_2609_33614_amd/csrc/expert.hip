@@ -408,7 +408,10 @@ static int pick_nsub(int64_t T) {
 // number of 16-row wave tiles over the experts a call may be left with is
 // below EAT_SPLIT_WAVES.  Only K experts are counted (the union of a call
 // can be that small: EAT concentrates its picks), so short launches still
-// spread over the whole chip and end without a long tail.
+// spread over the whole chip and end without a long tail.  Each slice costs
+// the combine one more fp32 row per assignment to read: calls whose union
+// really is K experts (EAT) gain from 4096, calls that touch every expert
+// (Top-K at B=64) would prefer 2048; the union is only known on the device.
 #ifndef EAT_SPLIT_WAVES
 #define EAT_SPLIT_WAVES 4096
 #endif

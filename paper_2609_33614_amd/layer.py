@@ -136,6 +136,27 @@ class EatStack:
             lay.close()
 
 
+def capture(fn, warmup: int = 2) -> "torch.cuda.CUDAGraph":
+    """Capture ``fn()`` -- calls into the library, which only enqueue on the
+    current stream and never allocate or synchronise -- into a HIP graph.
+    ``warmup`` eager calls first size every workspace (they run the layers,
+    so reset accounts afterwards where that matters).  Replay with
+    ``graph.replay()`` after copying new inputs into the tensors ``fn``
+    reads; account updates inside the graph act on the live account
+    tensors, so replays carry the history forward."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(warmup):
+            fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    return g
+
+
 def to_device(weights: Dict, device: str = "cuda") -> Dict[str, torch.Tensor]:
     """Upload generator output (fp32 arrays or bf16 bit patterns as uint16)
     to device tensors (torch.bfloat16 for bf16)."""
