@@ -63,6 +63,7 @@ class Params:
     cs_mode: int = 0           # 0: C_s used as is in Eq. 1; 1: C_s / sum(C_s)
     shared: bool = False       # always-on shared expert added with weight 1
     round_h: bool = False      # round the experts' hidden activation to bf16 (R27)
+    expert_scale: Optional[np.ndarray] = None   # OPD per-expert reweighting (Sec. 3.5), or None
 
 
 # ---------------------------------------------------------------- inputs --
@@ -246,11 +247,21 @@ class Routing:
         return [i for i in range(self.p.shape[1]) if (m >> i) & 1]
 
 
+def reweight(p: np.ndarray, scale: np.ndarray) -> np.ndarray:
+    """Sec. 3.5 (OPD at inference): scale each expert's raw routing
+    probability and renormalise the row, p'_i = s_i p_i / sum_j s_j p_j."""
+    q = np.asarray(p, dtype=np.float64) * widen(scale)[None, :]
+    return q / q.sum(axis=1, keepdims=True)
+
+
 def route_probs(p: np.ndarray, acc, trend: Optional[np.ndarray], prm: Params) -> Routing:
     """Selection and renormalisation for a block of tokens whose router
     probabilities are already known.  Every token is judged against the
-    same account snapshot ``acc`` = (N, P_total, C_s)."""
+    same account snapshot ``acc`` = (N, P_total, C_s).  With an OPD scale
+    the reweighted probabilities take the place of p everywhere below."""
     p = np.asarray(p, dtype=np.float64)
+    if prm.expert_scale is not None:
+        p = reweight(p, prm.expert_scale)
     T, E = p.shape
     masks, ks = [], np.zeros(T, dtype=np.int64)
     g = np.zeros((T, E))

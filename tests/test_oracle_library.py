@@ -89,3 +89,28 @@ def test_router_softmax_rows_far_apart():
     ref = scipy.special.softmax(x.astype(np.float64) @ w.astype(np.float64).T, axis=1)
     np.testing.assert_allclose(p, ref, rtol=1e-12, atol=1e-300)
     assert np.isfinite(p).all()
+
+
+def test_opd_reweighting():
+    """Sec. 3.5: p' = s p / sum(s p) before selection."""
+    rng = np.random.default_rng(11)
+    E, T = 8, 200
+    p = torch.softmax(torch.from_numpy(rng.standard_normal((T, E))), dim=1).numpy()
+    s = rng.uniform(0.25, 4.0, E)
+    # unit scales leave every routing decision unchanged
+    for mode in (O.MODE_EAT, O.MODE_TOPK, O.MODE_TOPP):
+        a = O.route_probs(p, O.zero_accounts(E), None, O.Params(mode=mode, K=2))
+        b = O.route_probs(p, O.zero_accounts(E), None, O.Params(mode=mode, K=2, expert_scale=np.ones(E)))
+        assert a.masks == b.masks
+        np.testing.assert_allclose(a.g_norm, b.g_norm, rtol=1e-15, atol=0)
+    # Top-K on the reweighted row is torch.topk of s * p (the renormaliser is a positive factor)
+    r = O.route_probs(p, None, None, O.Params(mode=O.MODE_TOPK, K=3, expert_scale=s))
+    ref = torch.topk(torch.from_numpy(p * s), 3, dim=1).indices.numpy()
+    for t in range(T):
+        assert r.masks[t] == sum(1 << int(e) for e in ref[t])
+    np.testing.assert_allclose(r.p.sum(axis=1), 1.0, rtol=1e-14)
+    np.testing.assert_allclose(r.p, (p * s) / (p * s).sum(axis=1, keepdims=True), rtol=1e-15)
+    # a dominant scale forces its expert into every Top-K selection
+    big = np.ones(E); big[5] = 1e6
+    r2 = O.route_probs(p, None, None, O.Params(mode=O.MODE_TOPK, K=2, expert_scale=big))
+    assert all((m >> 5) & 1 for m in r2.masks)
