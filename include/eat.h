@@ -97,6 +97,13 @@ typedef struct {
     int32_t act_dtype;       /* eat_dtype_t of x and y                              */
     int32_t expert_dtype;    /* eat_dtype_t of w1/w3/w2 (and ws1/ws3/ws2)           */
     int32_t d_shared;        /* width of an always-on shared SwiGLU expert, 0 = none */
+    const float* expert_scale; /* OPD reweighting (Sec. 3.5): device [E] fp32 scales s,
+                                  p_i -> s_i p_i / sum_j s_j p_j before everything that
+                                  uses p (importance, threshold, selection, gates,
+                                  P_total), in every mode; NULL (default) = none.  The
+                                  pointer is kept by eat_create and must stay valid,
+                                  with s_i >= 0 and sum_j s_j p_j > 0, while the handle
+                                  is used; 4-byte aligned.                          */
 } eat_params_t;
 
 /* Per-layer account state (Sec. 3.2), device memory, length E each, owned by

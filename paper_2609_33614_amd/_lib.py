@@ -37,7 +37,7 @@ class eat_params_t(C.Structure):
         ("kappa1", C.c_float), ("kappa2", C.c_float), ("ppl_up", C.c_float), ("ppl_down", C.c_float),
         ("q_lo", C.c_float), ("q_hi", C.c_float), ("eps", C.c_float), ("inv_temperature", C.c_float),
         ("cs_mode", C.c_int32), ("act_dtype", C.c_int32), ("expert_dtype", C.c_int32),
-        ("d_shared", C.c_int32),
+        ("d_shared", C.c_int32), ("expert_scale", C.c_void_p),
     ]
 
 

@@ -34,6 +34,7 @@ eat_status_t check_params(const eat_params_t& p) {
     if (!in01(p.q_lo) || !in01(p.q_hi) || p.q_lo > p.q_hi) return EAT_ERR_INVALID_ARG;
     if (p.eps < 0.f || p.inv_temperature <= 0.f) return EAT_ERR_INVALID_ARG;
     if (p.cs_mode != 0 && p.cs_mode != 1) return EAT_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(p.expert_scale) % 4) return EAT_ERR_INVALID_ARG;
     if ((p.act_dtype != EAT_F32 && p.act_dtype != EAT_BF16) ||
         (p.expert_dtype != EAT_F32 && p.expert_dtype != EAT_BF16))
         return EAT_ERR_INVALID_ARG;
@@ -108,6 +109,7 @@ eat_status_t eat_params_default(eat_params_t* out) {
     out->act_dtype = EAT_BF16;
     out->expert_dtype = EAT_BF16;
     out->d_shared = 0;
+    out->expert_scale = nullptr;
     return EAT_OK;
 }
 

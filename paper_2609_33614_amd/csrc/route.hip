@@ -9,7 +9,8 @@
 // bytes per token tile) off a single CU.
 //
 // select_kernel: one wave per token, one lane per expert.  Adds the slice
-// partials in slice order, then softmax (Sec. 3.1) and the mode's selection
+// partials in slice order, then softmax (Sec. 3.1), the optional OPD
+// reweighting (Sec. 3.5) and the mode's selection
 // (EAT: history score S_h from the account snapshot in fp64 (Eq. 1),
 // importance (Eq. 2), threshold (Eq. 3-5, Sec. 3.3), activation set (Eq. 6);
 // Top-K; Top-P) and the renormalisation of Eq. 7-8.
@@ -39,6 +40,7 @@ struct RouteArgs {
     int32_t* k;
     float* gate;
     float* prob;
+    const float* scale;        // OPD per-expert reweighting [E], or null
     int T, d, E, K, mode, cs_mode, top_p_cap, slices;
     float top_p, w1, w2, w3, beta, alpha1, alpha2, kappa1, kappa2, ppl_up, ppl_down, q_lo, q_hi,
         eps, inv_temp;
@@ -209,7 +211,13 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
         }
         const float zmax = wave_max(z);
         const float ez = valid ? expf(z - zmax) : 0.f;
-        const float p = ez / wave_sum(ez);
+        float p = ez / wave_sum(ez);
+        if (a.scale) {
+            // Sec. 3.5: OPD reweighting, p'_i = s_i p_i / sum_j s_j p_j, used for
+            // everything below (importance, threshold, selection, gates, P_total)
+            const float q = valid ? a.scale[lane] * p : 0.f;
+            p = q / wave_sum(q);
+        }
 
         uint64_t msk = 0;
         if (a.mode == EAT_MODE_EAT) {
@@ -353,6 +361,7 @@ hipError_t launch_route(const eat_params_t& p, const void* x, int32_t T, const f
     a.w1 = p.w1; a.w2 = p.w2; a.w3 = p.w3; a.beta = p.beta; a.alpha1 = p.alpha1; a.alpha2 = p.alpha2;
     a.kappa1 = p.kappa1; a.kappa2 = p.kappa2; a.ppl_up = p.ppl_up; a.ppl_down = p.ppl_down;
     a.q_lo = p.q_lo; a.q_hi = p.q_hi; a.eps = p.eps; a.inv_temp = p.inv_temperature;
+    a.scale = p.expert_scale;
     if (p.act_dtype == EAT_BF16) return launch_route_t<uint16_t>(a, s);
     return launch_route_t<float>(a, s);
 }

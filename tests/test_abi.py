@@ -76,7 +76,7 @@ def test_defaults_are_the_papers_table():
                   inv_temperature=1.0)
     for k, v in expect.items():
         assert getattr(p, k) == pytest.approx(v, rel=1e-6), k
-    assert p.cs_mode == 0 and p.d_shared == 0
+    assert p.cs_mode == 0 and p.d_shared == 0 and not p.expert_scale
 
 
 def _params(**kw):
@@ -103,6 +103,7 @@ def _params(**kw):
     ("act_dtype", 7, L.EAT_ERR_INVALID_ARG),
     ("expert_dtype", 1, L.EAT_ERR_UNSUPPORTED),
     ("top_p_cap", 9, L.EAT_ERR_INVALID_ARG),
+    ("expert_scale", (1 << 20) + 2, L.EAT_ERR_INVALID_ARG),     # misaligned scale vector
 ])
 def test_create_rejects_bad_params(field, value, status):
     p = _params(**{field: value})

@@ -14,7 +14,8 @@ import oracle as O
 from paper_2609_33614_amd import _lib as L
 from paper_2609_33614_amd.layer import EatLayer, to_device
 from tests import parity as PT
-from workload import SHAPES, HiddenStream, make_accounts, make_layer_weights, make_prefill, make_trend
+from workload import (SHAPES, HiddenStream, make_accounts, make_expert_scale, make_layer_weights, make_prefill,
+                      make_trend)
 
 pytestmark = pytest.mark.gpu
 
@@ -44,7 +45,7 @@ def _y_host(y):
     return y.float().cpu().numpy().astype(np.float64)
 
 
-def _layer(case, mode, K=None, top_p=None, cs_mode=0, max_tokens=512, seed=None):
+def _layer(case, mode, K=None, top_p=None, cs_mode=0, max_tokens=512, seed=None, scale=None):
     shape = SHAPES[case["shape"]]
     w = make_layer_weights(shape, seed=seed, E=case["E"], d=case["d"], F=case["F"], F_shared=case["Fs"])
     dt = L.EAT_BF16 if shape.bf16 else L.EAT_F32
@@ -53,8 +54,14 @@ def _layer(case, mode, K=None, top_p=None, cs_mode=0, max_tokens=512, seed=None)
                              top_p=(shape.top_p or 0.6) if top_p is None else top_p,
                              inv_temperature=shape.inv_temp, cs_mode=cs_mode, act_dtype=dt,
                              expert_dtype=dt, d_shared=case["Fs"])
+    scale_dev = None
+    if scale is not None:
+        scale_dev = torch.from_numpy(scale).cuda()
+        p.expert_scale = scale_dev.data_ptr()
     lay = EatLayer(p, max_tokens, to_device(w))
+    lay.scale_dev = scale_dev            # the handle keeps the pointer: keep the tensor alive
     prm = PT.oracle_params(shape, MODES[mode], K=K, top_p=top_p, cs_mode=cs_mode, shared=case["Fs"] > 0)
+    prm.expert_scale = scale
     return shape, w, lay, prm
 
 
@@ -95,6 +102,39 @@ def test_route_parity(case, mode, T):
     torch.cuda.synchronize()
     r = O.route(x, w["w_router"], acc, trend, prm)
     _check_routing(f"route {case} {mode} T={T}", r, prm, mask, gate, prob, k)
+
+
+@pytest.mark.parametrize("case", ["tiny", "mixtral", "finegrained"])
+@pytest.mark.parametrize("mode", ["eat", "topk", "topp"])
+def test_opd_reweighting_parity(case, mode):
+    """Sec. 3.5: per-expert scales applied to p before selection (routing,
+    gates, probabilities, and the forward's accounts)."""
+    c = SMALL[case]
+    T = 200
+    scale = make_expert_scale(c["E"], seed=17)
+    shape, w, lay, prm = _layer(c, mode, scale=scale)
+    x = _x_host(shape, T, c["d"], seed=55)
+    acc = make_accounts(c["E"], seed=3, c_scale=0.05)
+    if mode == "eat":
+        lay.load_accounts(*acc)
+    mask, k, gate, prob = lay.route(_x_dev(x))
+    torch.cuda.synchronize()
+    r = O.route(x, w["w_router"], acc, None, prm)
+    _check_routing(f"opd route {case} {mode} T={T}", r, prm, mask, gate, prob, k)
+    # the scales change the selection of some tokens (the hook is live)
+    plain = O.route(x, w["w_router"], acc, None, PT.oracle_params(shape, MODES[mode]))
+    assert sum(a != b for a, b in zip(plain.masks, r.masks)) > 0
+    # forward: y and the account update use the reweighted probabilities
+    y = lay.forward(_x_dev(x), mask_out=mask)
+    torch.cuda.synchronize()
+    ref = O.moe_step(x, w, acc if mode == "eat" else None, None, prm)
+    border = PT.borderline(ref.routing, prm)
+    err = PT.row_rel_err(_y_host(y), ref.y)[~border]
+    assert (err <= (PT.TOL_Y_BF16 if shape.bf16 else PT.TOL_Y_F32)).all()
+    if mode == "eat" and not border.any():
+        n, pt, cs = lay.accounts_host()
+        np.testing.assert_array_equal(n, ref.acc[0])
+        np.testing.assert_allclose(pt, ref.acc[1], rtol=PT.TOL_P_TOTAL, atol=1e-6)
 
 
 def test_route_zero_input_takes_lowest_indices():

@@ -11,6 +11,7 @@ from .gmm import (  # noqa: F401
     bf16_bits,
     make_layer_weights,
     make_mixing,
+    make_expert_scale,
     HiddenStream,
     make_prefill,
     make_trend,

@@ -157,6 +157,13 @@ def make_layer_weights(shape: LayerShape, seed: Optional[int] = None, layer: int
     return out
 
 
+def make_expert_scale(E: int, seed: int, spread: float = 2.0) -> np.ndarray:
+    """Per-expert routing scales of the kind a recovery fine-tune leaves
+    behind: log-uniform in [1/spread, spread], fp32 [E]."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([int(seed), 0x6f7064])))
+    return np.exp(g.uniform(-np.log(spread), np.log(spread), E)).astype(np.float32)
+
+
 def make_mixing(shape: LayerShape, layer: int, seed: Optional[int] = None, d: Optional[int] = None) -> np.ndarray:
     """The d x d residual mixing matrix applied after stacked layer ``layer``:
     N(0, 1/d) entries from the layer's own stream, bf16 bits."""
