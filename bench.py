@@ -20,7 +20,8 @@ against the MI355X peak (timed per launch with HIP events on the launch
 stream), a batch sweep, and the CPU oracle timed on a bounded sample.
 A ``stack`` object times the 16-layer workload (16 fine-grained layers,
 RMSNorm and a residual mixing matrix between them, decode batch 64) per
-routing mode, with every layer's mean activated experts.
+routing mode, with every layer's mean activated experts, and EAT with
+layer-wise caps (2 in the lower 12 layers, K in the upper 4).
 A ``prefill`` object adds the MFMA-bound side: one prefill call of the
 fine-grained layer (4096 tokens, 64 experts of width 1024, K=8) and of the
 shared-expert layer (8192 tokens, 60 experts of width 1408 + an always-on
@@ -219,7 +220,7 @@ def run_prefill(shape_name: str, reps: int, ev: HipEvents, modes=("eat", "topk")
     return out
 
 
-def run_stack(steps: int, warmup: int, ev: HipEvents, modes=("eat", "topk", "topp")):
+def run_stack(steps: int, warmup: int, ev: HipEvents, modes=("eat", "topk", "topp", "eat_layerwise")):
     """The 16-layer workload: decode batch 64 through 16 stacked fine-grained
     layers (own accounts each, RMSNorm + residual mixing between layers),
     `steps` timed steps per mode after `warmup` untimed ones on scratch
@@ -230,7 +231,7 @@ def run_stack(steps: int, warmup: int, ev: HipEvents, modes=("eat", "topk", "top
     import torch
 
     from paper_2609_33614_amd import _lib as L
-    from paper_2609_33614_amd.layer import EatStack, to_device
+    from paper_2609_33614_amd.layer import EatStack, layerwise_caps, to_device
     from workload import SHAPES, HiddenStream, make_layer_weights, make_mixing
 
     shape = SHAPES["stack16"]
@@ -245,8 +246,12 @@ def run_stack(steps: int, warmup: int, ev: HipEvents, modes=("eat", "topk", "top
     out = {"workload": f"{nl}-layer stack decode (RMSNorm + residual mixing between layers)", "layers": nl,
            "batch": B, "d_model": d, "experts": E, "d_ffn": F, "top_k": shape.K, "steps": steps}
     for mode in modes:
-        params = [L.eat_params_default(mode=L.MODES[mode], E=E, d_model=d, d_ffn=F, top_k=shape.K,
-                                       top_p=shape.top_p, inv_temperature=shape.inv_temp) for _ in range(nl)]
+        # eat_layerwise: layer-wise sparsity, EAT capped at 2 in the lower 12
+        # layers and at the model's K in the upper 4
+        caps = layerwise_caps(nl, 12, 2, shape.K) if mode == "eat_layerwise" else [shape.K] * nl
+        rmode = "eat" if mode == "eat_layerwise" else mode
+        params = [L.eat_params_default(mode=L.MODES[rmode], E=E, d_model=d, d_ffn=F, top_k=caps[l],
+                                       top_p=shape.top_p, inv_temperature=shape.inv_temp) for l in range(nl)]
         st = EatStack(params, B, wdev, mdev)
         h = torch.empty(B, d, dtype=torch.bfloat16, device="cuda")
         masks = torch.empty(steps, nl, B, dtype=torch.int64, device="cuda")

@@ -91,6 +91,13 @@ class EatLayer:
             pass
 
 
+def layerwise_caps(n_layers: int, lower: int, k_lower: int, k_upper: int):
+    """Per-layer caps K for layer-wise sparsity: the paper's layer analysis
+    (Sec. 4) finds lower layers' experts less critical than higher layers',
+    so the lower ``lower`` layers get ``k_lower`` and the rest ``k_upper``."""
+    return [k_lower if l < lower else k_upper for l in range(n_layers)]
+
+
 class EatStack:
     """Stacked layers (one EatLayer each, own accounts) with their d x d
     mixing matrices, run one decode step at a time by eat_stack_forward."""
