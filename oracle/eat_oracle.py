@@ -455,3 +455,38 @@ def stack_step(x, layers: Sequence[dict], mixes: Sequence[np.ndarray], accs: Seq
         h = round_bf16(r @ widen(m).T)
         outs.append(o)
     return StackOut(h=h, layers=outs)
+
+
+# ------------------------------------------- perplexity signal (Sec 3.3) --
+#
+# The threshold's performance-based adjustment compares the current model
+# perplexity with the previous one.  Per sequence: the token's negative
+# log-likelihood under the LM head, NLL = logsumexp(h W_V^T) - (h W_V^T)[y],
+# a running perplexity exp(sum NLL / n) over the sequence so far, and the
+# trend +1 when it rose since the sequence's previous token, -1 when it did
+# not, 0 for a sequence's first token (reading R30).
+
+@dataclass
+class PplState:
+    nll_sum: np.ndarray        # [S] float64
+    count: np.ndarray          # [S] int64
+    ppl_prev: np.ndarray       # [S] float64
+
+
+def ppl_zero_state(S: int) -> PplState:
+    return PplState(np.zeros(S), np.zeros(S, np.int64), np.zeros(S))
+
+
+def ppl_update(h, w_vocab, target, state: PplState):
+    """One token per sequence: returns (nll [S], ppl [S], trend [S] int8,
+    new state)."""
+    z = widen(h) @ widen(w_vocab).T
+    zmax = z.max(axis=1, keepdims=True)
+    lse = zmax[:, 0] + np.log(np.exp(z - zmax).sum(axis=1))
+    tgt = np.asarray(target, dtype=np.int64)
+    nll = lse - z[np.arange(z.shape[0]), tgt]
+    nll_sum = state.nll_sum + nll
+    count = state.count + 1
+    ppl = np.exp(nll_sum / count)
+    trend = np.where(count > 1, np.where(ppl > state.ppl_prev, 1, -1), 0).astype(np.int8)
+    return nll, ppl, trend, PplState(nll_sum, count, ppl)

@@ -12,6 +12,8 @@ from .gmm import (  # noqa: F401
     make_layer_weights,
     make_mixing,
     make_expert_scale,
+    make_vocab_head,
+    make_targets,
     HiddenStream,
     make_prefill,
     make_trend,

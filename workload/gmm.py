@@ -157,6 +157,18 @@ def make_layer_weights(shape: LayerShape, seed: Optional[int] = None, layer: int
     return out
 
 
+def make_vocab_head(d: int, V: int, seed: int) -> np.ndarray:
+    """A synthetic LM head W_V [V, d] ~ N(0, 1/d), bf16 bits."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([int(seed), 0x766f63])))
+    return bf16_bits(_normal(g, (V, d), 1.0 / np.sqrt(d)))
+
+
+def make_targets(S: int, V: int, seed: int) -> np.ndarray:
+    """Next-token ids, uniform over the vocabulary, int32 [S]."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([int(seed), 0x746774])))
+    return g.integers(0, V, S).astype(np.int32)
+
+
 def make_expert_scale(E: int, seed: int, spread: float = 2.0) -> np.ndarray:
     """Per-expert routing scales of the kind a recovery fine-tune leaves
     behind: log-uniform in [1/spread, spread], fp32 [E]."""
