@@ -21,7 +21,9 @@ stream), a batch sweep, and the CPU oracle timed on a bounded sample.
 A ``stack`` object times the 16-layer workload (16 fine-grained layers,
 RMSNorm and a residual mixing matrix between them, decode batch 64) per
 routing mode, with every layer's mean activated experts, and EAT with
-layer-wise caps (2 in the lower 12 layers, K in the upper 4).
+layer-wise caps (2 in the lower 12 layers, K in the upper 4); a
+``ppl_signal`` object times the LM-head perplexity signal (Sec. 3.3) for 64
+sequences at the Mixtral head shape.
 A ``prefill`` object adds the MFMA-bound side: one prefill call of the
 fine-grained layer (4096 tokens, 64 experts of width 1024, K=8) and of the
 shared-expert layer (8192 tokens, 60 experts of width 1408 + an always-on
@@ -286,6 +288,39 @@ def run_stack(steps: int, warmup: int, ev: HipEvents, modes=("eat", "topk", "top
     return out
 
 
+def run_ppl(ev: HipEvents, S: int = 64, d: int = 4096, V: int = 32000, reps: int = 50):
+    """The perplexity signal (LM-head NLL, running perplexity, trend) for S
+    sequences at the Mixtral head shape: microseconds per call and the
+    achieved bandwidth on its algorithmic bytes (W_V, the hidden rows, the
+    fp32 logits written and read once, the state)."""
+    import torch
+
+    from paper_2609_33614_amd.layer import PplSignal
+    from workload import SHAPES, HiddenStream, make_targets, make_vocab_head
+
+    w = torch.from_numpy(make_vocab_head(d, V, seed=1)).view(torch.bfloat16).cuda()
+    h = torch.from_numpy(HiddenStream(SHAPES["mixtral"], S).next()).view(torch.bfloat16).cuda()
+    y = torch.from_numpy(make_targets(S, V, seed=2)).cuda()
+    sig = PplSignal(S, w)
+    sig.reset()
+    for _ in range(5):
+        sig.step(h, y)
+    t0, t1 = ev.create(2)
+    stream = torch.cuda.current_stream().cuda_stream
+    torch.cuda.synchronize()
+    ev.hip.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
+    ev.hip.hipEventRecord(t0, stream)
+    for _ in range(reps):
+        sig.step(h, y)
+    ev.hip.hipEventRecord(t1, stream)
+    torch.cuda.synchronize()
+    us = ev.elapsed_ms(t0, t1) / reps * 1e3
+    nbytes = V * d * 2 + S * d * 2 + 2 * S * V * 4 + S * 21
+    return {"workload": "LM-head perplexity signal", "sequences": S, "d_model": d, "vocab": V,
+            "us_per_call": round(us, 2), "hbm_gbs": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "hbm_frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+
 def traffic_up(shape, B, k_row, U):
     """Algorithmic HBM bytes of one up/gate launch: W1 and W3 rows of every
     expert in the step's union, the B token rows read, the H rows written."""
@@ -462,6 +497,8 @@ def main(argv=None) -> int:
         for name in ("finegrained", "shared"):
             log(f"prefill {name}: {args.prefill_reps} timed calls per mode")
             prefill.append(run_prefill(name, args.prefill_reps, ev))
+    log("perplexity signal")
+    ppl = run_ppl(ev)
     stack = None
     if not args.no_stack:
         if "wdev" in locals():
@@ -505,6 +542,7 @@ def main(argv=None) -> int:
         "sweep": sweep,
         "prefill": prefill,
         "stack": stack,
+        "ppl_signal": ppl,
     }
     print(json.dumps(out), flush=True)
     return 0

@@ -270,6 +270,44 @@ eat_status_t eat_stack_forward(const eat_stack_layer_t* layers, int32_t n_layers
                                const int8_t* ppl_trend, float rms_eps, void* h_out, uint64_t* masks_out,
                                float* probs_out, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- perplexity signal ----------------------------------------------------
+ *
+ * Sec. 3.3 raises the threshold by 20% when the model's perplexity rose
+ * (PPL_curr - PPL_prev > 0) and lowers it by 10% otherwise.  eat_ppl_trend
+ * produces that signal for S sequences, one token each, from the LM head:
+ *
+ *   z_s   = h_s . W_V^T                      (bf16 in, fp32 accumulation)
+ *   NLL_s = logsumexp(z_s) - z_s[target_s]
+ *   sum_s += NLL_s;  n_s += 1;  PPL_s = exp(sum_s / n_s)        (fp64 state)
+ *   trend_s = +1 if n_s > 1 and PPL_s > PPL_prev_s, -1 if n_s > 1 otherwise,
+ *             0 for a sequence's first token;  PPL_prev_s = PPL_s
+ *
+ * trend_out is the int8 ppl_trend the next step's eat_route /
+ * eat_moe_forward / eat_stack_forward take for those sequences' tokens. */
+
+/* Workspace bytes for S sequences, width d (multiple of 64) and vocabulary
+ * V (multiple of 64).  EAT_ERR_INVALID_ARG otherwise. */
+eat_status_t eat_ppl_workspace_size(int32_t S, int32_t d, int32_t V, size_t* bytes);
+
+/* Zero the running state of S sequences (device arrays, caller-owned):
+ * nll_sum [S] fp64, count [S] int32, ppl_prev [S] fp64. */
+eat_status_t eat_ppl_reset(int32_t S, double* nll_sum, int32_t* count, double* ppl_prev, hipStream_t stream);
+
+/* One token per sequence through the LM head (formulas above).
+ *   h          [S][d] bf16 final hidden rows (device)
+ *   w_vocab    [V][d] bf16 LM head (device)
+ *   target     [S] int32 next-token ids; an id outside [0, V) gives a NaN
+ *              NLL (and a NaN running sum) for that sequence
+ *   nll_sum, count, ppl_prev   the running state, updated in place
+ *   trend_out  [S] int8;  nll_out [S] fp32 or NULL
+ *   ws         workspace of eat_ppl_workspace_size bytes, 256-byte aligned
+ * Enqueues on `stream` only; no synchronisation, no allocation.  Errors:
+ * EAT_ERR_INVALID_ARG (shapes, null or misaligned pointers),
+ * EAT_ERR_WORKSPACE, EAT_ERR_HIP. */
+eat_status_t eat_ppl_trend(const void* h, int32_t S, int32_t d, const void* w_vocab, int32_t V,
+                           const int32_t* target, double* nll_sum, int32_t* count, double* ppl_prev,
+                           int8_t* trend_out, float* nll_out, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Static description of a status code (never NULL). */
 const char* eat_status_string(eat_status_t s);
 

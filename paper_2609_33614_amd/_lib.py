@@ -79,11 +79,16 @@ def load() -> C.CDLL:
     if hasattr(lib, "eat_stack_forward"):
         lib.eat_stack_workspace_size.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(C.c_size_t)]
         lib.eat_stack_forward.argtypes = [P, C.c_int32, P, C.c_int32, P, C.c_float, P, P, P, P, C.c_size_t, P]
+    if hasattr(lib, "eat_ppl_trend"):
+        lib.eat_ppl_workspace_size.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_size_t)]
+        lib.eat_ppl_reset.argtypes = [C.c_int32, P, P, P, P]
+        lib.eat_ppl_trend.argtypes = [P, C.c_int32, C.c_int32, P, C.c_int32, P, P, P, P, P, P, P, C.c_size_t, P]
     lib.eat_status_string.argtypes = [C.c_int]
     lib.eat_status_string.restype = C.c_char_p
     for name in ("eat_params_default", "eat_create", "eat_destroy", "eat_workspace_size", "eat_route_workspace_size",
                  "eat_reset_accounts", "eat_route", "eat_moe_forward", "eat_moe_forward_profiled",
-                 "eat_stack_workspace_size", "eat_stack_forward"):
+                 "eat_stack_workspace_size", "eat_stack_forward", "eat_ppl_workspace_size", "eat_ppl_reset",
+                 "eat_ppl_trend"):
         if hasattr(lib, name):
             getattr(lib, name).restype = st
     _lib = lib
@@ -209,3 +214,20 @@ def eat_stack_forward(layers, n_layers: int, x, T: int, ppl_trend, rms_eps: floa
                                     _ptr(x), int(T), _ptr(ppl_trend), float(rms_eps), _ptr(h_out),
                                     _ptr(masks_out), _ptr(probs_out), _ptr(ws), int(ws_bytes), _stream(stream)),
            "eat_stack_forward")
+
+
+def eat_ppl_workspace_size(S: int, d: int, V: int) -> int:
+    b = C.c_size_t()
+    _check(load().eat_ppl_workspace_size(int(S), int(d), int(V), C.byref(b)), "eat_ppl_workspace_size")
+    return b.value
+
+
+def eat_ppl_reset(S: int, nll_sum, count, ppl_prev, stream=None) -> None:
+    _check(load().eat_ppl_reset(int(S), _ptr(nll_sum), _ptr(count), _ptr(ppl_prev), _stream(stream)), "eat_ppl_reset")
+
+
+def eat_ppl_trend(h, S: int, d: int, w_vocab, V: int, target, nll_sum, count, ppl_prev, trend_out, nll_out, ws,
+                  ws_bytes: int, stream=None) -> None:
+    _check(load().eat_ppl_trend(_ptr(h), int(S), int(d), _ptr(w_vocab), int(V), _ptr(target), _ptr(nll_sum),
+                                _ptr(count), _ptr(ppl_prev), _ptr(trend_out), _ptr(nll_out), _ptr(ws), int(ws_bytes),
+                                _stream(stream)), "eat_ppl_trend")

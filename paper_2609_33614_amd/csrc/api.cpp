@@ -418,6 +418,48 @@ eat_status_t eat_moe_forward(eat_handle_t h, const void* x, int32_t T, const flo
                                     expert_load_out, ws, ws_bytes, stream, nullptr, 0);
 }
 
+eat_status_t eat_ppl_workspace_size(int32_t S, int32_t d, int32_t V, size_t* bytes) {
+    if (!bytes || S < 0 || S > kMaxTokens || d < 64 || d % 64 || V < 64 || V % 64) return EAT_ERR_INVALID_ARG;
+    *bytes = align256(static_cast<size_t>(eat::ppl_splits(S, d, V)) * S * V * 4) +
+             align256(static_cast<size_t>(S) * eat::ppl_chunks(V) * 8);
+    return EAT_OK;
+}
+
+eat_status_t eat_ppl_reset(int32_t S, double* nll_sum, int32_t* count, double* ppl_prev, hipStream_t stream) {
+    if (S < 0 || (S > 0 && (!nll_sum || !count || !ppl_prev))) return EAT_ERR_INVALID_ARG;
+    if (!aligned(nll_sum, 8) || !aligned(count, 4) || !aligned(ppl_prev, 8)) return EAT_ERR_INVALID_ARG;
+    if (S == 0) return EAT_OK;
+    (void)hipGetLastError();
+    return eat::launch_ppl_reset(S, nll_sum, count, ppl_prev, stream) == hipSuccess ? EAT_OK : EAT_ERR_HIP;
+}
+
+eat_status_t eat_ppl_trend(const void* h, int32_t S, int32_t d, const void* w_vocab, int32_t V,
+                           const int32_t* target, double* nll_sum, int32_t* count, double* ppl_prev,
+                           int8_t* trend_out, float* nll_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+    size_t need = 0;
+    const eat_status_t st = eat_ppl_workspace_size(S, d, V, &need);
+    if (st != EAT_OK) return st;
+    if (S == 0) return EAT_OK;
+    if (!h || !w_vocab || !target || !nll_sum || !count || !ppl_prev || !trend_out) return EAT_ERR_INVALID_ARG;
+    if (!aligned(h, 16) || !aligned(w_vocab, 16) || !aligned(target, 4) || !aligned(nll_sum, 8) ||
+        !aligned(count, 4) || !aligned(ppl_prev, 8) || (nll_out && !aligned(nll_out, 4)))
+        return EAT_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < need) return EAT_ERR_WORKSPACE;
+    if (!aligned(ws, 256)) return EAT_ERR_INVALID_ARG;
+    float* z = static_cast<float*>(ws);
+    const int splits = eat::ppl_splits(S, d, V);
+    const int64_t stride = static_cast<int64_t>(S) * V;
+    (void)hipGetLastError();
+    hipError_t e = eat::launch_dense_bf16(static_cast<const uint16_t*>(h), S, static_cast<const uint16_t*>(w_vocab),
+                                          V, d, z, splits, stride, stream);
+    if (e == hipSuccess)
+        e = eat::launch_ppl(z, splits, stride, S, V, target, nll_sum, count, ppl_prev, trend_out, nll_out,
+                            reinterpret_cast<float2*>(static_cast<char*>(ws) +
+                                                      align256(static_cast<size_t>(splits) * S * V * 4)),
+                            stream);
+    return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;
+}
+
 const char* eat_status_string(eat_status_t s) {
     switch (s) {
         case EAT_OK: return "ok";

@@ -132,6 +132,17 @@ hipError_t launch_wide(bool gated, const uint16_t* wa, const uint16_t* wb, const
                        const int32_t* gather, const int32_t* offsets, int groups, int nrows, int M,
                        int K, void* out, int64_t rows_cap, hipStream_t s);
 
+// Perplexity signal (ppl.hip): z [S][V] fp32 LM-head rows -> NLL of target,
+// running per-sequence state (fp64 NLL sum, count, previous perplexity) and
+// the int8 trend; z holds `splits` slices `stride` floats apart.
+// launch_ppl_reset zeroes the state.
+hipError_t launch_ppl(const float* z, int splits, int64_t stride, int32_t S, int V, const int32_t* target,
+                      double* nll_sum, int32_t* count, double* ppl_prev, int8_t* trend, float* nll_out,
+                      float2* part, hipStream_t s);
+int ppl_splits(int32_t S, int d, int V);
+int ppl_chunks(int V);                 // (max, sum) pairs per row in `part`
+hipError_t launch_ppl_reset(int32_t S, double* nll_sum, int32_t* count, double* ppl_prev, hipStream_t s);
+
 hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets,
                                   const int32_t* tok_idx, const float* prob, const float* nrm2,
                                   eat_accounts_t acc, hipStream_t s);

@@ -91,6 +91,31 @@ class EatLayer:
             pass
 
 
+class PplSignal:
+    """Running perplexity of S sequences through an LM head (Sec. 3.3's
+    signal): ``step(h, target)`` returns the int8 trend for the sequences'
+    next tokens (eat_ppl_trend)."""
+
+    def __init__(self, S: int, w_vocab: torch.Tensor, device: str = "cuda"):
+        self.S, self.w = int(S), w_vocab
+        self.V, self.d = w_vocab.shape
+        dev = torch.device(device)
+        self.nll_sum = torch.zeros(S, dtype=torch.float64, device=dev)
+        self.count = torch.zeros(S, dtype=torch.int32, device=dev)
+        self.ppl_prev = torch.zeros(S, dtype=torch.float64, device=dev)
+        self.trend = torch.zeros(S, dtype=torch.int8, device=dev)
+        self.nll = torch.zeros(S, dtype=torch.float32, device=dev)
+        self.ws = torch.empty(max(256, L.eat_ppl_workspace_size(S, self.d, self.V)), dtype=torch.uint8, device=dev)
+
+    def reset(self, stream=None) -> None:
+        L.eat_ppl_reset(self.S, self.nll_sum, self.count, self.ppl_prev, stream)
+
+    def step(self, h: torch.Tensor, target: torch.Tensor, stream=None) -> torch.Tensor:
+        L.eat_ppl_trend(h, self.S, self.d, self.w, self.V, target, self.nll_sum, self.count, self.ppl_prev,
+                        self.trend, self.nll, self.ws, self.ws.numel(), stream)
+        return self.trend
+
+
 def layerwise_caps(n_layers: int, lower: int, k_lower: int, k_upper: int):
     """Per-layer caps K for layer-wise sparsity: the paper's layer analysis
     (Sec. 4) finds lower layers' experts less critical than higher layers',

@@ -287,3 +287,26 @@ def test_stack_validation_happens_on_the_host():
     finally:
         for h in hs + [h_f32, h_d256]:
             eat.eat_destroy(h)
+
+
+def test_ppl_validation_happens_on_the_host():
+    need = eat.eat_ppl_workspace_size(4, 128, 256)
+    assert need >= 4 * 256 * 4
+    for args in ((-1, 128, 256), (4, 100, 256), (4, 128, 100), (4, 0, 256), (4, 128, 0)):
+        with pytest.raises(eat.EatError):
+            eat.eat_ppl_workspace_size(*args)
+    base = dict(h=FAKE, S=4, d=128, w_vocab=FAKE, V=256, target=FAKE, nll_sum=FAKE, count=FAKE, ppl_prev=FAKE,
+                trend_out=FAKE, nll_out=None, ws=FAKE, ws_bytes=need, stream=0)
+    cases = [(dict(h=None), L.EAT_ERR_INVALID_ARG), (dict(target=None), L.EAT_ERR_INVALID_ARG),
+             (dict(h=FAKE + 8), L.EAT_ERR_INVALID_ARG), (dict(nll_sum=FAKE + 4), L.EAT_ERR_INVALID_ARG),
+             (dict(V=100), L.EAT_ERR_INVALID_ARG), (dict(ws_bytes=need - 1), L.EAT_ERR_WORKSPACE),
+             (dict(ws=None), L.EAT_ERR_WORKSPACE), (dict(ws=FAKE + 64), L.EAT_ERR_INVALID_ARG)]
+    for kw, status in cases:
+        args = dict(base); args.update(kw)
+        with pytest.raises(eat.EatError) as ei:
+            eat.eat_ppl_trend(**args)
+        assert ei.value.status == status, kw
+    args = dict(base); args.update(S=0, h=None, ws=None, ws_bytes=0)
+    eat.eat_ppl_trend(**args)
+    with pytest.raises(eat.EatError):
+        eat.eat_ppl_reset(4, None, FAKE, FAKE, stream=0)
