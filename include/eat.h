@@ -297,7 +297,8 @@ eat_status_t eat_ppl_reset(int32_t S, double* nll_sum, int32_t* count, double* p
  *   h          [S][d] bf16 final hidden rows (device)
  *   w_vocab    [V][d] bf16 LM head (device)
  *   target     [S] int32 next-token ids; an id outside [0, V) gives a NaN
- *              NLL (and a NaN running sum) for that sequence
+ *              NLL and a NaN running sum for that sequence, whose trend
+ *              is then -1 until eat_ppl_reset (NaN compares false)
  *   nll_sum, count, ppl_prev   the running state, updated in place
  *   trend_out  [S] int8;  nll_out [S] fp32 or NULL
  *   ws         workspace of eat_ppl_workspace_size bytes, 256-byte aligned
