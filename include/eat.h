@@ -28,7 +28,7 @@
  *  - Errors: no C++ exception crosses this interface.  A HIP launch failure
  *    is reported as EAT_ERR_HIP (the enqueued work up to the failure may
  *    have run).
- *  - Limits: 1 <= E <= 64 (one bit per expert in a 64-bit mask);
+ *  - Limits: 1 <= E <= 256 (a token's mask is up to four 64-bit words);
  *    1 <= top_k <= E; d_model, d_ffn and d_shared are multiples of 64;
  *    activations and expert weights are both fp32 or both bf16.
  *  - Layouts (all row-major, densely packed, 16-byte aligned):
@@ -38,7 +38,9 @@
  *      w2       [E][d_model][d_ffn]     expert_dtype  (down rows)
  *      ws1, ws3 [d_shared][d_model], ws2 [d_model][d_shared]
  *      y        [T][d_model]            act_dtype
- *      masks    [T] uint64, bit i set <=> expert i selected
+ *      masks    [T][W] uint64 with W = ceil(E / 64) words per token
+ *               (one word for E <= 64): bit i % 64 of word i / 64 set
+ *               <=> expert i selected
  *      gates    [T][E] fp32, renormalised gate (0 for unselected experts)
  *  - Thread safety: a handle is immutable after eat_create; calls that use
  *    different workspaces and account buffers may run concurrently.
@@ -157,7 +159,8 @@ eat_status_t eat_route_workspace_size(eat_handle_t h, int32_t T, size_t* bytes);
  *              ignored by Top-K / Top-P, may then hold null pointers)
  *   ppl_trend  [T] int8 or NULL: > 0 means the perplexity rose for that
  *              token's sequence (tau x ppl_up), anything else tau x ppl_down
- *   mask_out   [T] uint64, k_out [T] int32, gate_out [T][E] fp32: required
+ *   mask_out   [T][W] uint64 (W = ceil(E / 64)), k_out [T] int32,
+ *              gate_out [T][E] fp32: required
  *   prob_out   [T][E] fp32 router probabilities, or NULL
  *   ws         device workspace of at least eat_route_workspace_size(h, T)
  *              bytes, 256-byte aligned (EAT_ERR_WORKSPACE otherwise)
@@ -179,7 +182,7 @@ eat_status_t eat_route(eat_handle_t h, const void* x, int32_t T, const float* w_
  *   w1, w3, w2     routed experts (layouts in the file header)
  *   ws1, ws3, ws2  shared expert when d_shared > 0, else all NULL
  *   y              [T][d_model] act_dtype output
- *   mask_out       [T] uint64 or NULL
+ *   mask_out       [T][W] uint64 (W = ceil(E / 64)) or NULL
  *   expert_load_out [E] int32 tokens per expert, or NULL
  */
 eat_status_t eat_moe_forward(eat_handle_t h, const void* x, int32_t T, const float* w_router,
@@ -258,7 +261,8 @@ eat_status_t eat_stack_workspace_size(const eat_stack_layer_t* layers, int32_t n
  *   ppl_trend  [T] int8 or NULL, passed to every layer (Sec. 3.3)
  *   rms_eps    RMSNorm epsilon (finite, >= 0)
  *   h_out      [T][d] bf16 output h_n (device; must not alias x)
- *   masks_out  [n_layers][T] uint64 selection masks, or NULL
+ *   masks_out  every layer's selection masks, layer after layer,
+ *              [T][ceil(E_l / 64)] uint64 each, or NULL
  *   probs_out  every layer's router probabilities p (Sec. 3.1), layer after
  *              layer, [T][E_l] fp32 each (T * sum of E_l floats), or NULL
  *   ws         device workspace of eat_stack_workspace_size bytes, 256-byte aligned

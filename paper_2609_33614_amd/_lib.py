@@ -124,6 +124,11 @@ def accounts(n=None, p_total=None, c_s=None) -> eat_accounts_t:
     return eat_accounts_t(_ptr(n), _ptr(p_total), _ptr(c_s))
 
 
+def mask_words(E: int) -> int:
+    """64-bit words of one token's selection mask (the ABI's [T][W] layout)."""
+    return (int(E) + 63) // 64
+
+
 # -------------------------------------------------------------- entry points --
 
 def eat_status_string(status: int) -> str:

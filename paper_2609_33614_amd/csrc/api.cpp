@@ -66,7 +66,7 @@ Workspace plan_workspace(const eat_ctx& c, int32_t T) {
     w.route_total = off;
     w.prob = take(t * E * 4);
     w.gate = take(t * E * 4);
-    w.mask = take(t * 8);
+    w.mask = take(t * eat::mask_words(p.E) * 8);
     w.k = take(t * 4);
     w.offsets = take((E + 1) * 4);
     w.tok_idx = take(rows * 4);
@@ -384,6 +384,7 @@ eat_status_t eat_stack_forward(const eat_stack_layer_t* layers, int32_t n_layers
 
     (void)hipGetLastError();
     size_t prob_off = 0;                      // layer l's probabilities start after T * E_j of the layers before
+    size_t mask_off = 0;                      // and its masks after T * mask_words(E_j)
     // u_0 = bf16(RMSNorm(x))
     hipError_t e = eat::launch_mix_norm(nullptr, 0, 0, static_cast<const uint16_t*>(x), T, d, rms_eps, nullptr, u,
                                         stream);
@@ -392,9 +393,10 @@ eat_status_t eat_stack_forward(const eat_stack_layer_t* layers, int32_t n_layers
         const eat_stack_layer_t& L = layers[l];
         // r = bf16(h + MoE_l(u))
         e = forward_impl(*L.layer, u, T, L.w_router, L.w1, L.w3, L.w2, L.ws1, L.ws3, L.ws2, L.acc, ppl_trend, h, r,
-                         masks_out ? masks_out + static_cast<size_t>(l) * T : nullptr, nullptr,
+                         masks_out ? masks_out + mask_off : nullptr, nullptr,
                          probs_out ? probs_out + prob_off : nullptr, base + sp.layer, stream, nullptr, 0);
         prob_off += static_cast<size_t>(T) * L.layer->p.E;
+        mask_off += static_cast<size_t>(T) * eat::mask_words(L.layer->p.E);
         // h' = bf16(r M_l^T); u = bf16(RMSNorm(h')) for the next layer
         if (e == hipSuccess)
             e = eat::launch_dense_bf16(r, T, static_cast<const uint16_t*>(L.mix), d, d, mix, sp.splits, stride,

@@ -28,7 +28,7 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 
 struct CombineArgs {
-    const uint64_t* mask;
+    const uint64_t* mask;      // [T][words]
     const float* gate;
     const int32_t* inv;
     const float* yp;           // [splits][rows_cap][d]
@@ -37,7 +37,7 @@ struct CombineArgs {
     void* y;
     float* nrm2;               // [rows_cap][nchunk] partial sums of squares
     int64_t split_stride;
-    int splits, T, E, d, nchunk;
+    int splits, T, E, d, nchunk, words;
 };
 
 // One workgroup per (token, 1024-element slice of d): 4 elements per
@@ -53,9 +53,9 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     const bool on = 4 * j < a.d;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 
-    const uint64_t m = a.mask[t];
-    for (uint64_t rest = m; rest; rest &= rest - 1) {
-        const int e = __builtin_ctzll(rest);
+    for (int w = 0; w < a.words; ++w)
+    for (uint64_t rest = a.mask[static_cast<size_t>(t) * a.words + w]; rest; rest &= rest - 1) {
+        const int e = 64 * w + __builtin_ctzll(rest);
         const int64_t row = a.inv[static_cast<size_t>(t) * a.E + e];
         const float g = a.gate[static_cast<size_t>(t) * a.E + e];
         float ss = 0.f;
@@ -215,7 +215,8 @@ hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask
                           const int32_t* inv, const float* yp, const float* ys, const uint16_t* residual,
                           void* y, float* nrm2, int splits, int64_t split_stride, hipStream_t s) {
     const int nchunk = combine_chunks(p);
-    CombineArgs a{mask, gate, inv, yp, ys, residual, y, nrm2, split_stride, splits, T, p.E, p.d_model, nchunk};
+    CombineArgs a{mask,   gate,   inv, yp,  ys,        residual, y,     nrm2, split_stride,
+                  splits, T,      p.E, p.d_model, nchunk, mask_words(p.E)};
     const dim3 grid(T, nchunk);
     if (p.act_dtype == EAT_BF16) combine_kernel<uint16_t><<<grid, kThreads, 0, s>>>(a);
     else combine_kernel<float><<<grid, kThreads, 0, s>>>(a);

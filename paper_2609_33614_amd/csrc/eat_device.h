@@ -37,6 +37,42 @@ __device__ __forceinline__ float wave_max(float v) {
     return v;
 }
 
+// Tile table of expert-major row segments: tstart[g] = sum over h < g of
+// ceil((offsets[h+1] - offsets[h]) / bm), for g = 0..groups.  Wave 0 reads
+// one segment per lane and scans 64 at a time (integer sums, so the order
+// does not matter); every thread of the workgroup must call it.
+__device__ __forceinline__ void tile_starts(const int32_t* offsets, int groups, int bm, int* tstart) {
+    if (threadIdx.x < kWave) {
+        const int lane = __lane_id();
+        int carry = 0;
+        for (int g0 = 0; g0 < groups; g0 += kWave) {
+            const int g = g0 + lane;
+            int c = g < groups ? (offsets[g + 1] - offsets[g] + bm - 1) / bm : 0;
+#pragma unroll
+            for (int o = 1; o < kWave; o <<= 1) {
+                const int u = __shfl_up(c, o, kWave);
+                if (lane >= o) c += u;
+            }
+            if (g < groups) tstart[g + 1] = carry + c;
+            carry += __shfl(c, kWave - 1, kWave);
+        }
+        if (lane == 0) tstart[0] = 0;
+    }
+    __syncthreads();
+}
+
+// Segment holding tile `tile` (0 <= tile < tstart[groups]): the first g with
+// tstart[g + 1] > tile, by binary search (empty segments are skipped).
+__device__ __forceinline__ int tile_group(const int* tstart, int groups, int tile) {
+    int lo = 0, hi = groups - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (tstart[mid + 1] > tile) hi = mid;
+        else lo = mid + 1;
+    }
+    return lo;
+}
+
 // Broadcast lane j's value (j uniform across the wave) through an SGPR.
 __device__ __forceinline__ float read_lane(float v, int j) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), j));

@@ -18,7 +18,10 @@ struct eat_ctx {
 
 namespace eat {
 
-constexpr int kMaxExperts = 64;    // one 64-bit selection mask per token
+constexpr int kMaxExperts = 256;   // selection masks of up to four 64-bit words per token
+
+// 64-bit words of one token's selection mask: bit e % 64 of word e / 64 is expert e.
+inline int mask_words(int E) { return (E + 63) / 64; }
 
 // Offsets (bytes) of the workspace regions for T tokens.  Every region
 // starts on a 256-byte boundary.
@@ -37,7 +40,7 @@ struct Buffers {
     float* lpart;            // [route_slices][T][E] partial router scores
     float* prob;             // [T][E] router probabilities
     float* gate;             // [T][E] renormalised gates
-    uint64_t* mask;          // [T]
+    uint64_t* mask;          // [T][mask_words(E)]
     int32_t* k;              // [T]
     int32_t* offsets;        // [E+1] expert-major row offsets
     int32_t* tok_idx;        // [rows] token of each expert-major row

@@ -131,21 +131,13 @@ __global__ __launch_bounds__(WPB * 64) void stream_kernel(StreamArgs a) {
     constexpr int VPR = KC / 8;                       // 16-byte vectors per token row per chunk
     constexpr int RMAX = (BN * VPR + NT - 1) / NT;    // vectors per thread per chunk
     __shared__ __attribute__((aligned(16))) uint16_t xs[2][BN * LDS_ROW];
-    __shared__ int tstart[65];
+    __shared__ int tstart[kMaxExperts + 1];
     const int tid = threadIdx.x;
     const int lane = lane_id(), wave = tid / kWave;
 
     int ntiles;
     if (a.offsets) {
-        if (tid == 0) {
-            int acc = 0;
-            for (int e = 0; e < a.groups; ++e) {
-                tstart[e] = acc;
-                acc += (a.offsets[e + 1] - a.offsets[e] + BN - 1) / BN;
-            }
-            tstart[a.groups] = acc;
-        }
-        __syncthreads();
+        tile_starts(a.offsets, a.groups, BN, tstart);
         ntiles = tstart[a.groups];
     } else {
         ntiles = (a.nrows + BN - 1) / BN;
@@ -159,7 +151,7 @@ __global__ __launch_bounds__(WPB * 64) void stream_kernel(StreamArgs a) {
     for (int tile = blockIdx.y; tile < ntiles; tile += gridDim.y) {
         int e = 0, r0, n;
         if (a.offsets) {
-            while (tstart[e + 1] <= tile) ++e;
+            e = tile_group(tstart, a.groups, tile);
             r0 = a.offsets[e] + (tile - tstart[e]) * BN;
             n = min(BN, a.offsets[e + 1] - r0);
         } else {

@@ -3,7 +3,9 @@
 // The selected (token, expert) pairs are laid out expert-major: expert e
 // owns rows [offsets[e], offsets[e+1]), and inside that range its tokens
 // appear in increasing token order.  One workgroup per expert:
-//   offsets[e] = sum_t popcount(mask_t & lower bits below e)
+//   offsets[e] = sum_t popcount(mask_t & bits below e)
+// (a token's mask is W = ceil(E / 64) words; expert e is bit e % 64 of word
+// e / 64, so the words before e's word count whole)
 // needs no global histogram, so no inter-workgroup synchronisation or
 // atomics.  Positions inside the segment come from wave ballots and an
 // LDS-staged prefix over the 4 waves, chunk by chunk in token order.
@@ -17,20 +19,23 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 
 __global__ __launch_bounds__(kThreads) void permute_kernel(
-    const uint64_t* __restrict__ mask, int T, int E, int32_t* __restrict__ offsets,
+    const uint64_t* __restrict__ mask, int T, int E, int W, int32_t* __restrict__ offsets,
     int32_t* __restrict__ tok_idx, int32_t* __restrict__ inv, int32_t* __restrict__ row_expert,
     int32_t* __restrict__ expert_load) {
     __shared__ int red[2][kWaves];
     __shared__ int wtot[kWaves];
     const int e = blockIdx.x;
     const int lane = lane_id(), wave = threadIdx.x / kWave;
-    const uint64_t below = (e == 0) ? 0ull : ((~0ull) >> (64 - e));
-    const uint64_t bit = 1ull << e;
+    const int we = e >> 6, be = e & 63;
+    const uint64_t below = (be == 0) ? 0ull : ((~0ull) >> (64 - be));
+    const uint64_t bit = 1ull << be;
 
     // segment start and size
     int before = 0, mine = 0;
     for (int t = threadIdx.x; t < T; t += kThreads) {
-        const uint64_t m = mask[t];
+        const uint64_t* mt = mask + static_cast<size_t>(t) * W;
+        for (int w = 0; w < we; ++w) before += __popcll(mt[w]);
+        const uint64_t m = mt[we];
         before += __popcll(m & below);
         mine += (m & bit) ? 1 : 0;
     }
@@ -52,7 +57,7 @@ __global__ __launch_bounds__(kThreads) void permute_kernel(
     const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
     for (int base = 0; base < T; base += kThreads) {
         const int t = base + threadIdx.x;
-        const bool on = t < T && (mask[t] & bit);
+        const bool on = t < T && (mask[static_cast<size_t>(t) * W + we] & bit);
         const uint64_t b = ballot(on);
         if (lane == 0) wtot[wave] = __popcll(b);
         __syncthreads();
@@ -78,8 +83,8 @@ __global__ __launch_bounds__(kThreads) void permute_kernel(
 hipError_t launch_permute(const eat_params_t& p, int32_t T, const uint64_t* mask, int32_t* offsets,
                           int32_t* tok_idx, int32_t* inv, int32_t* row_expert, int32_t* expert_load,
                           hipStream_t s) {
-    permute_kernel<<<dim3(p.E), dim3(kThreads), 0, s>>>(mask, T, p.E, offsets, tok_idx, inv, row_expert,
-                                                        expert_load);
+    permute_kernel<<<dim3(p.E), dim3(kThreads), 0, s>>>(mask, T, p.E, mask_words(p.E), offsets, tok_idx, inv,
+                                                        row_expert, expert_load);
     return hipGetLastError();
 }
 

@@ -1,14 +1,17 @@
 // Router + EAT selection kernels (gfx950).
 //
 // logits_kernel: one workgroup of 4 waves per (tile of 16*TT tokens,
-// slice of d).  Router scores x W_r^T for the tile's tokens and all E
-// experts over its slice, fp32 MFMA (v_mfma_f32_16x16x4_f32, fp32 router
-// weights); the waves take interleaved 16-wide k-steps of the slice and add
-// their tiles in wave order; the slice's partial scores go to the workspace.
-// Spreading d over many workgroups keeps the router-weight reads (E*d*4
-// bytes per token tile) off a single CU.
+// slice of d, group of 64 experts).  Router scores x W_r^T for the tile's
+// tokens and the group's experts over its slice, fp32 MFMA
+// (v_mfma_f32_16x16x4_f32, fp32 router weights); the waves take interleaved
+// 16-wide k-steps of the slice and add their tiles in wave order; the
+// slice's partial scores go to the workspace.  Spreading d over many
+// workgroups keeps the router-weight reads (E*d*4 bytes per token tile) off
+// a single CU.
 //
-// select_kernel: one wave per token, one lane per expert.  Adds the slice
+// select_kernel<J>: one wave per token; lane l holds experts l, 64 + l, ...
+// (J = ceil(E / 64) of them), and the token's mask is J 64-bit words, word
+// j being the wave ballot over experts 64 j .. 64 j + 63.  Adds the slice
 // partials in slice order, then softmax (Sec. 3.1), the optional OPD
 // reweighting (Sec. 3.5) and the mode's selection
 // (EAT: history score S_h from the account snapshot in fp64 (Eq. 1),
@@ -36,7 +39,7 @@ struct RouteArgs {
     const float* acc_c;
     const int8_t* trend;
     float* part;               // [slices][T][E] partial router scores
-    uint64_t* mask;
+    uint64_t* mask;            // [T][J] words
     int32_t* k;
     float* gate;
     float* prob;
@@ -63,10 +66,22 @@ __device__ __forceinline__ void load_x4<uint16_t>(const uint16_t* row, int k, fl
     v[3] = __uint_as_float(q.y & 0xffff0000u);
 }
 
-// Value held by the lane whose rank (a permutation of 0..E-1) equals r.
-__device__ __forceinline__ float value_at_rank(float v, int rank, int r, bool valid) {
-    const uint64_t b = ballot(valid && rank == r);
-    return read_lane(v, __builtin_ctzll(b));
+// Value of the expert whose rank (a permutation of 0..E-1 for ordered
+// values) equals r; NaN when no expert holds it (NaN scores).
+template <int J>
+__device__ __forceinline__ float value_at_rank(const float (&v)[J], const int (&rank)[J], int r,
+                                               const bool (&valid)[J]) {
+    float out = NAN;
+    bool found = false;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        const uint64_t b = ballot(valid[j] && rank[j] == r);
+        if (!found && b) {
+            out = read_lane(v[j], __builtin_ctzll(b));
+            found = true;
+        }
+    }
+    return out;
 }
 
 template <typename XT, int NT, int TT>
@@ -76,6 +91,8 @@ __global__ __launch_bounds__(256) void logits_kernel(RouteArgs a) {
     const int wave = threadIdx.x / kWave;
     const int t0 = blockIdx.x * 16 * TT;
     const int E = a.E;
+    const int e0 = blockIdx.z * 64;              // this workgroup's expert group
+    const int EG = min(64, E - e0);
     const XT* x = static_cast<const XT*>(a.x);
     const int kq = 4 * (lane >> 4);          // this lane's 4 k values in a 16-wide k-step
     const int nsteps = a.d / 16;
@@ -94,7 +111,7 @@ __global__ __launch_bounds__(256) void logits_kernel(RouteArgs a) {
     bool e_ok[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-        const int e = nt * 16 + (lane & 15);
+        const int e = e0 + nt * 16 + (lane & 15);
         e_ok[nt] = e < E;
         wrow[nt] = a.w_router + static_cast<size_t>(e_ok[nt] ? e : 0) * a.d;
     }
@@ -150,52 +167,75 @@ __global__ __launch_bounds__(256) void logits_kernel(RouteArgs a) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) red[wave][tt * 16 + 4 * (lane >> 4) + i][nt * 16 + (lane & 15)] = acc[tt][nt][i];
     __syncthreads();
-    for (int v = threadIdx.x; v < TT * 16 * E; v += 256) {
-        const int tl = v / E, e = v % E;
+    for (int v = threadIdx.x; v < TT * 16 * EG; v += 256) {
+        const int tl = v / EG, e = v % EG;
         const int t = t0 + tl;
         if (t >= a.T) continue;
         float sum = 0.f;
 #pragma unroll
         for (int w = 0; w < kLogitWaves; ++w) sum += red[w][tl][e];
-        a.part[(static_cast<size_t>(blockIdx.y) * a.T + t) * E + e] = sum;
+        a.part[(static_cast<size_t>(blockIdx.y) * a.T + t) * E + e0 + e] = sum;
     }
 }
 
 constexpr int kSelWaves = 4;
 
+// Sum over the wave of each lane's J values (lane-local first, in expert
+// order, then the butterfly); for J = 1 this is the plain butterfly.
+template <int J>
+__device__ __forceinline__ float wave_sum_j(const float (&v)[J]) {
+    float s = v[0];
+#pragma unroll
+    for (int j = 1; j < J; ++j) s += v[j];
+    return wave_sum(s);
+}
+
+template <int J>
 __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
-    __shared__ float sh[64];
+    __shared__ float sh[64 * J];
     const int lane = lane_id();
     const int wave = threadIdx.x / kWave;
     const int E = a.E;
+    bool valid[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) valid[j] = 64 * j + lane < E;
 
     // ---- history score from the account snapshot (Eq. 1) --------------
     if (a.mode == EAT_MODE_EAT && wave == 0) {
-        const bool valid = lane < E;
-        const double n = valid ? static_cast<double>(a.acc_n[lane]) : 0.0;
-        const double pt = valid ? static_cast<double>(a.acc_p[lane]) : 0.0;
-        const double c = valid ? static_cast<double>(a.acc_c[lane]) : 0.0;
-        const double sum_n = wave_sum(n);
-        const double t1 = sum_n > 0.0 ? n / sum_n : 0.0;
-        const double t2 = n > 0.0 ? pt / n : 0.0;
-        double t3 = c;
-        if (a.cs_mode == 1) {
-            const double sum_c = wave_sum(c);
-            t3 = sum_c > 0.0 ? c / sum_c : 0.0;
+        double n[J], pt[J], c[J];
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int e = 64 * j + lane;
+            n[j] = valid[j] ? static_cast<double>(a.acc_n[e]) : 0.0;
+            pt[j] = valid[j] ? static_cast<double>(a.acc_p[e]) : 0.0;
+            c[j] = valid[j] ? static_cast<double>(a.acc_c[e]) : 0.0;
         }
-        sh[lane] = static_cast<float>(a.w1 * t1 + a.w2 * t2 + a.w3 * t3);
+        double ln = n[0], lc = c[0];
+#pragma unroll
+        for (int j = 1; j < J; ++j) { ln += n[j]; lc += c[j]; }
+        const double sum_n = wave_sum(ln);
+        const double sum_c = a.cs_mode == 1 ? wave_sum(lc) : 0.0;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const double t1 = sum_n > 0.0 ? n[j] / sum_n : 0.0;
+            const double t2 = n[j] > 0.0 ? pt[j] / n[j] : 0.0;
+            double t3 = c[j];
+            if (a.cs_mode == 1) t3 = sum_c > 0.0 ? c[j] / sum_c : 0.0;
+            sh[64 * j + lane] = static_cast<float>(a.w1 * t1 + a.w2 * t2 + a.w3 * t3);
+        }
     }
     __syncthreads();
 
     // ---- per-token softmax, selection, renormalisation ----------------
-    const bool valid = lane < E;
-    {
-        const int t = blockIdx.x * kSelWaves + wave;
-        if (t >= a.T) return;
-        float z = -INFINITY;
-        if (valid) {
+    const int t = blockIdx.x * kSelWaves + wave;
+    if (t >= a.T) return;
+    float z[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        z[j] = -INFINITY;
+        if (valid[j]) {
             // slices added in slice order; loads issued 8 at a time
-            const float* src = a.part + static_cast<size_t>(t) * E + lane;
+            const float* src = a.part + static_cast<size_t>(t) * E + 64 * j + lane;
             const size_t stride = static_cast<size_t>(a.T) * E;
             float sum = 0.f;
             int sl = 0;
@@ -207,106 +247,184 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
                 for (int u = 0; u < 8; ++u) sum += v[u];
             }
             for (; sl < a.slices; ++sl) sum += src[sl * stride];
-            z = sum * a.inv_temp;
+            z[j] = sum * a.inv_temp;
         }
-        const float zmax = wave_max(z);
-        const float ez = valid ? expf(z - zmax) : 0.f;
-        float p = ez / wave_sum(ez);
-        if (a.scale) {
-            // Sec. 3.5: OPD reweighting, p'_i = s_i p_i / sum_j s_j p_j, used for
-            // everything below (importance, threshold, selection, gates, P_total)
-            const float q = valid ? a.scale[lane] * p : 0.f;
-            p = q / wave_sum(q);
-        }
-
-        uint64_t msk = 0;
-        if (a.mode == EAT_MODE_EAT) {
-            // Eq. 3-5 grounding on the token's routing weights
-            const float mu = wave_sum(valid ? p : 0.f) / static_cast<float>(E);
-            const float dv = valid ? p - mu : 0.f;
-            const float sigma = sqrtf(wave_sum(dv * dv) / static_cast<float>(E));
-            const float tau = fmaxf(a.alpha1 * mu, mu - a.alpha2 * sigma);
-            // perplexity adjustment and smoothing (Sec. 3.3)
-            const float f = (a.trend != nullptr && a.trend[t] > 0) ? a.ppl_up : a.ppl_down;
-            const float tau_s = a.kappa1 * (f * tau) + a.kappa2 * tau;
-            // bounds: q_lo / q_hi points of the sorted routing weights
-            int rank = 0;
-            for (int j = 0; j < E; ++j) {
-                const float pj = read_lane(p, j);
-                rank += (pj < p) || (pj == p && j < lane);
-            }
-            float qv[2];
-            const float qs[2] = {a.q_lo, a.q_hi};
+    }
+    float zl = z[0];
 #pragma unroll
-            for (int qi = 0; qi < 2; ++qi) {
-                const float h = qs[qi] * static_cast<float>(E - 1);
-                const int lo = static_cast<int>(floorf(h));
-                const int hi = lo + 1 < E ? lo + 1 : E - 1;
-                const float vlo = value_at_rank(p, rank, lo, valid);
-                const float vhi = value_at_rank(p, rank, hi, valid);
-                qv[qi] = vlo + (h - static_cast<float>(lo)) * (vhi - vlo);
+    for (int j = 1; j < J; ++j) zl = fmaxf(zl, z[j]);
+    const float zmax = wave_max(zl);
+    float p[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) p[j] = valid[j] ? expf(z[j] - zmax) : 0.f;
+    {
+        const float den = wave_sum_j<J>(p);
+#pragma unroll
+        for (int j = 0; j < J; ++j) p[j] = p[j] / den;
+    }
+    if (a.scale) {
+        // Sec. 3.5: OPD reweighting, p'_i = s_i p_i / sum_j s_j p_j, used for
+        // everything below (importance, threshold, selection, gates, P_total)
+#pragma unroll
+        for (int j = 0; j < J; ++j) p[j] = valid[j] ? a.scale[64 * j + lane] * p[j] : 0.f;
+        const float den = wave_sum_j<J>(p);
+#pragma unroll
+        for (int j = 0; j < J; ++j) p[j] = p[j] / den;
+    }
+
+    uint64_t msk[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) msk[j] = 0;
+    if (a.mode == EAT_MODE_EAT) {
+        // Eq. 3-5 grounding on the token's routing weights
+        float tmp[J];
+#pragma unroll
+        for (int j = 0; j < J; ++j) tmp[j] = valid[j] ? p[j] : 0.f;
+        const float mu = wave_sum_j<J>(tmp) / static_cast<float>(E);
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const float dv = valid[j] ? p[j] - mu : 0.f;
+            tmp[j] = dv * dv;
+        }
+        const float sigma = sqrtf(wave_sum_j<J>(tmp) / static_cast<float>(E));
+        const float tau = fmaxf(a.alpha1 * mu, mu - a.alpha2 * sigma);
+        // perplexity adjustment and smoothing (Sec. 3.3)
+        const float f = (a.trend != nullptr && a.trend[t] > 0) ? a.ppl_up : a.ppl_down;
+        const float tau_s = a.kappa1 * (f * tau) + a.kappa2 * tau;
+        // bounds: q_lo / q_hi points of the sorted routing weights
+        int rank[J];
+#pragma unroll
+        for (int j = 0; j < J; ++j) rank[j] = 0;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            const int nl = min(64, E - 64 * jj);
+            for (int l = 0; l < nl; ++l) {
+                const float pv = read_lane(p[jj], l);
+                const int ev = 64 * jj + l;
+#pragma unroll
+                for (int j = 0; j < J; ++j) rank[j] += (pv < p[j]) || (pv == p[j] && ev < 64 * j + lane);
             }
-            const float tau_final = fminf(fmaxf(tau_s, qv[0]), qv[1]);
-            // Eq. 2 importance and Eq. 6 activation set
-            const float I = (1.f - a.beta) * p + a.beta * (valid ? sh[lane] : 0.f);
-            const uint64_t cand = ballot(valid && I > tau_final);
-            const int c = __popcll(cand);
-            if (c == 0) {
-                const float imax = wave_max(valid ? I : -INFINITY);
-                const uint64_t b = ballot(valid && I == imax);
-                msk = b & (~b + 1);                  // lowest index among maximisers
-            } else if (c <= a.K) {
-                msk = cand;
-            } else {
-                int beaten = 0;
-                for (uint64_t rest = cand; rest; rest &= rest - 1) {
-                    const int j = __builtin_ctzll(rest);
-                    beaten += read_lane(I, j) > I;
-                }
-                msk = ballot(valid && ((cand >> lane) & 1ull) && beaten < a.K);
+        }
+        float qv[2];
+        const float qs[2] = {a.q_lo, a.q_hi};
+#pragma unroll
+        for (int qi = 0; qi < 2; ++qi) {
+            const float h = qs[qi] * static_cast<float>(E - 1);
+            const int lo = static_cast<int>(floorf(h));
+            const int hi = lo + 1 < E ? lo + 1 : E - 1;
+            const float vlo = value_at_rank<J>(p, rank, lo, valid);
+            const float vhi = value_at_rank<J>(p, rank, hi, valid);
+            qv[qi] = vlo + (h - static_cast<float>(lo)) * (vhi - vlo);
+        }
+        const float tau_final = fminf(fmaxf(tau_s, qv[0]), qv[1]);
+        // Eq. 2 importance and Eq. 6 activation set
+        float I[J];
+        uint64_t cand[J];
+        int c = 0;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            I[j] = (1.f - a.beta) * p[j] + a.beta * (valid[j] ? sh[64 * j + lane] : 0.f);
+            cand[j] = ballot(valid[j] && I[j] > tau_final);
+            c += __popcll(cand[j]);
+        }
+        if (c == 0) {
+            // argmax of I, lowest index among maximisers
+            float il = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < J; ++j) il = fmaxf(il, valid[j] ? I[j] : -INFINITY);
+            const float imax = wave_max(il);
+            bool done = false;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const uint64_t b = ballot(valid[j] && I[j] == imax);
+                if (!done && b) { msk[j] = b & (~b + 1); done = true; }
             }
+        } else if (c <= a.K) {
+#pragma unroll
+            for (int j = 0; j < J; ++j) msk[j] = cand[j];
         } else {
-            // descending rank, ties to the lower expert index
-            int rank = 0;
-            for (int j = 0; j < E; ++j) {
-                const float pj = read_lane(p, j);
-                rank += (pj > p) || (pj == p && j < lane);
-            }
-            int kk;
-            if (a.mode == EAT_MODE_TOPK) {
-                kk = a.K;
-            } else {
-                // Top-P: shortest descending prefix whose running sum reaches top_p
-                float run = 0.f;
-                kk = E;
-                for (int r = 0; r < E; ++r) {
-                    run += value_at_rank(p, rank, r, valid);
-                    if (run >= a.top_p) { kk = r + 1; break; }
+            // keep the candidates beaten (strictly) by fewer than K others
+            int beaten[J];
+#pragma unroll
+            for (int j = 0; j < J; ++j) beaten[j] = 0;
+#pragma unroll
+            for (int jj = 0; jj < J; ++jj)
+                for (uint64_t rest = cand[jj]; rest; rest &= rest - 1) {
+                    const float iv = read_lane(I[jj], __builtin_ctzll(rest));
+#pragma unroll
+                    for (int j = 0; j < J; ++j) beaten[j] += iv > I[j];
                 }
-                if (a.top_p_cap > 0 && kk > a.top_p_cap) kk = a.top_p_cap;
+#pragma unroll
+            for (int j = 0; j < J; ++j) msk[j] = ballot(valid[j] && ((cand[j] >> lane) & 1ull) && beaten[j] < a.K);
+        }
+    } else {
+        // descending rank, ties to the lower expert index
+        int rank[J];
+#pragma unroll
+        for (int j = 0; j < J; ++j) rank[j] = 0;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            const int nl = min(64, E - 64 * jj);
+            for (int l = 0; l < nl; ++l) {
+                const float pv = read_lane(p[jj], l);
+                const int ev = 64 * jj + l;
+#pragma unroll
+                for (int j = 0; j < J; ++j) rank[j] += (pv > p[j]) || (pv == p[j] && ev < 64 * j + lane);
             }
-            msk = ballot(valid && rank < kk);
-            // Ranks are a permutation for ordered values; NaN scores would
-            // break that, so never keep more than kk experts (the workspace
-            // holds at most kk rows per token in these modes).
-            if (__popcll(msk) > kk) {
-                uint64_t keep = 0, rest = msk;
-                for (int i = 0; i < kk; ++i) { keep |= rest & (~rest + 1); rest &= rest - 1; }
-                msk = keep;
+        }
+        int kk;
+        if (a.mode == EAT_MODE_TOPK) {
+            kk = a.K;
+        } else {
+            // Top-P: shortest descending prefix whose running sum reaches top_p
+            float run = 0.f;
+            kk = E;
+            for (int r = 0; r < E; ++r) {
+                run += value_at_rank<J>(p, rank, r, valid);
+                if (run >= a.top_p) { kk = r + 1; break; }
+            }
+            if (a.top_p_cap > 0 && kk > a.top_p_cap) kk = a.top_p_cap;
+        }
+        int c = 0;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            msk[j] = ballot(valid[j] && rank[j] < kk);
+            c += __popcll(msk[j]);
+        }
+        // Ranks are a permutation for ordered values; NaN scores would
+        // break that, so never keep more than kk experts (the workspace
+        // holds at most kk rows per token in these modes): the lowest
+        // indices are kept.
+        if (c > kk) {
+            int left = kk;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                uint64_t keep = 0, rest = msk[j];
+                for (; left > 0 && rest; --left) { keep |= rest & (~rest + 1); rest &= rest - 1; }
+                msk[j] = keep;
             }
         }
-        // Eq. 7-8 renormalisation over the selected experts
-        const bool on = valid && ((msk >> lane) & 1ull);
-        const float g = on ? p : 0.f;
-        const float gsum = wave_sum(g);
-        if (valid) {
-            a.gate[static_cast<size_t>(t) * E + lane] = g / (gsum + a.eps);
-            if (a.prob) a.prob[static_cast<size_t>(t) * E + lane] = p;
-        }
-        if (lane == 0) {
-            a.mask[t] = msk;
-            a.k[t] = __popcll(msk);
-        }
+    }
+    // Eq. 7-8 renormalisation over the selected experts
+    float g[J];
+    int kt = 0;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        g[j] = (valid[j] && ((msk[j] >> lane) & 1ull)) ? p[j] : 0.f;
+        kt += __popcll(msk[j]);
+    }
+    const float gsum = wave_sum_j<J>(g);
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        if (!valid[j]) continue;
+        const size_t o = static_cast<size_t>(t) * E + 64 * j + lane;
+        a.gate[o] = g[j] / (gsum + a.eps);
+        if (a.prob) a.prob[o] = p[j];
+    }
+    if (lane == 0) {
+#pragma unroll
+        for (int j = 0; j < J; ++j) a.mask[static_cast<size_t>(t) * J + j] = msk[j];
+        a.k[t] = kt;
     }
 }
 
@@ -320,16 +438,23 @@ hipError_t launch_logits_n(const RouteArgs& a, int tt, dim3 grid, hipStream_t s)
 template <typename XT>
 hipError_t launch_route_t(const RouteArgs& a, hipStream_t s) {
     const int tt = route_token_tiles(a.T);
-    const dim3 grid((a.T + 16 * tt - 1) / (16 * tt), a.slices);
+    const int words = mask_words(a.E);
+    const dim3 grid((a.T + 16 * tt - 1) / (16 * tt), a.slices, words);
     hipError_t err;
-    switch ((a.E + 15) / 16) {
+    switch ((std::min(a.E, 64) + 15) / 16) {
         case 1: err = launch_logits_n<XT, 1>(a, tt, grid, s); break;
         case 2: err = launch_logits_n<XT, 2>(a, tt, grid, s); break;
         case 3: err = launch_logits_n<XT, 3>(a, tt, grid, s); break;
         default: err = launch_logits_n<XT, 4>(a, tt, grid, s); break;
     }
     if (err != hipSuccess) return err;
-    select_kernel<<<(a.T + kSelWaves - 1) / kSelWaves, kSelWaves * kWave, 0, s>>>(a);
+    const dim3 sg((a.T + kSelWaves - 1) / kSelWaves), sb(kSelWaves * kWave);
+    switch (words) {
+        case 1: select_kernel<1><<<sg, sb, 0, s>>>(a); break;
+        case 2: select_kernel<2><<<sg, sb, 0, s>>>(a); break;
+        case 3: select_kernel<3><<<sg, sb, 0, s>>>(a); break;
+        default: select_kernel<4><<<sg, sb, 0, s>>>(a); break;
+    }
     return hipGetLastError();
 }
 

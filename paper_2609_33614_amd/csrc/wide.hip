@@ -192,15 +192,7 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
 
     int ntiles;
     if (a.offsets) {
-        if (tid == 0) {
-            int acc = 0;
-            for (int g = 0; g < a.groups; ++g) {
-                tstart[g] = acc;
-                acc += (a.offsets[g + 1] - a.offsets[g] + kWM - 1) / kWM;
-            }
-            tstart[a.groups] = acc;
-        }
-        __syncthreads();
+        tile_starts(a.offsets, a.groups, kWM, tstart);
         ntiles = tstart[a.groups];
     } else {
         ntiles = (a.nrows + kWM - 1) / kWM;
@@ -213,9 +205,12 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
     const int part = (work + kXcd - 1) / kXcd;
     const int wbeg = xcd * part, wend = min(work, wbeg + part);
 
+    // a workgroup's tiles only increase, so its segment search resumes where
+    // the previous tile's ended
+    int e = 0;
     for (int wid = wbeg + slot; wid < wend; wid += per_xcd) {
         const int tile = wid / nx, xt = wid % nx;
-        int e = 0, r0, n;
+        int r0, n;
         if (a.offsets) {
             while (tstart[e + 1] <= tile) ++e;
             r0 = a.offsets[e] + (tile - tstart[e]) * kWM;

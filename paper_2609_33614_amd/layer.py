@@ -67,10 +67,15 @@ class EatLayer:
             L.eat_moe_forward_profiled(*args, events=events)
         return y
 
+    def mask_tensor(self, T: int) -> torch.Tensor:
+        """Mask output for T tokens: [T] for E <= 64, else [T, words]."""
+        W = L.mask_words(self.params.E)
+        return torch.empty((T,) if W == 1 else (T, W), dtype=torch.int64, device=self.device)
+
     def route(self, x: torch.Tensor, trend: Optional[torch.Tensor] = None, stream=None):
         T = x.shape[0]
         E = self.params.E
-        mask = torch.empty(T, dtype=torch.int64, device=self.device)
+        mask = self.mask_tensor(T)
         k = torch.empty(T, dtype=torch.int32, device=self.device)
         gate = torch.empty(T, E, dtype=torch.float32, device=self.device)
         prob = torch.empty(T, E, dtype=torch.float32, device=self.device)

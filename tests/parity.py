@@ -61,8 +61,12 @@ def borderline(r: O.Routing, prm: O.Params, eps_b=EPS_B) -> np.ndarray:
 
 
 def masks_to_list(mask_tensor) -> list:
+    """[T] or [T, W] uint64 words (word j holds experts 64 j .. 64 j + 63)
+    -> one Python int per token, bit e <=> expert e."""
     a = mask_tensor.detach().cpu().numpy().astype(np.int64).view(np.uint64)
-    return [int(v) for v in a]
+    if a.ndim == 1:
+        return [int(v) for v in a]
+    return [sum(int(w) << (64 * j) for j, w in enumerate(row)) for row in a]
 
 
 def row_rel_err(y_gpu: np.ndarray, y_ref: np.ndarray) -> np.ndarray:

@@ -87,7 +87,7 @@ def _params(**kw):
 
 @pytest.mark.parametrize("field,value,status", [
     ("E", 0, L.EAT_ERR_INVALID_ARG),
-    ("E", 65, L.EAT_ERR_UNSUPPORTED),
+    ("E", 257, L.EAT_ERR_UNSUPPORTED),
     ("top_k", 0, L.EAT_ERR_INVALID_ARG),
     ("top_k", 9, L.EAT_ERR_INVALID_ARG),
     ("d_model", 100, L.EAT_ERR_UNSUPPORTED),
@@ -110,6 +110,17 @@ def test_create_rejects_bad_params(field, value, status):
     with pytest.raises(eat.EatError) as ei:
         eat.eat_create(p, 32)
     assert ei.value.status == status
+
+
+@pytest.mark.parametrize("E", [64, 65, 128, 200, 256])
+def test_create_accepts_up_to_256_experts(E):
+    # masks are ceil(E / 64) words per token; 257 experts are rejected above
+    h = eat.eat_create(_params(E=E, top_k=8), 128)
+    try:
+        assert L.mask_words(E) == (1 if E <= 64 else 2 if E <= 128 else 4)
+        assert eat.eat_workspace_size(h, 128) > eat.eat_workspace_size(h, 1) > 0
+    finally:
+        eat.eat_destroy(h)
 
 
 def test_create_rejects_bad_top_p_and_token_limits():

@@ -27,7 +27,13 @@ SMALL = {
     "mixtral": dict(shape="mixtral", d=512, F=768, E=8, Fs=0),
     "finegrained": dict(shape="finegrained", d=256, F=256, E=64, Fs=0),
     "shared": dict(shape="shared", d=256, F=192, E=60, Fs=320),
+    # more than 64 experts: masks of 2-4 words, ragged last words
+    "tiny_e100": dict(shape="tiny", d=128, F=128, E=100, Fs=0),
+    "qwen3": dict(shape="qwen3", d=256, F=256, E=128, Fs=0),
+    "qwen3_e200": dict(shape="qwen3", d=128, F=128, E=200, Fs=0),
+    "qwen3_e256": dict(shape="qwen3", d=128, F=192, E=256, Fs=0),
 }
+WIDE_E = ["tiny_e100", "qwen3", "qwen3_e200", "qwen3_e256"]
 
 
 def _x_host(shape, T, d, seed):
@@ -87,7 +93,7 @@ def _check_routing(name, r, prm, mask, gate, prob, k):
 
 # ------------------------------------------------------------------ routing --
 
-@pytest.mark.parametrize("case", ["tiny", "mixtral", "finegrained", "shared"])
+@pytest.mark.parametrize("case", ["tiny", "mixtral", "finegrained", "shared"] + WIDE_E)
 @pytest.mark.parametrize("mode", ["eat", "topk", "topp"])
 @pytest.mark.parametrize("T", [1, 37, 300])
 def test_route_parity(case, mode, T):
@@ -137,10 +143,12 @@ def test_opd_reweighting_parity(case, mode):
         np.testing.assert_allclose(pt, ref.acc[1], rtol=PT.TOL_P_TOTAL, atol=1e-6)
 
 
-def test_route_zero_input_takes_lowest_indices():
+@pytest.mark.parametrize("case", ["finegrained", "qwen3", "qwen3_e256"])
+def test_route_zero_input_takes_lowest_indices(case):
     # x = 0: every logit is 0, p is uniform; EAT with empty accounts has no
-    # candidate and takes expert 0; Top-K takes experts 0..K-1.
-    c = SMALL["finegrained"]
+    # candidate and takes expert 0; Top-K takes experts 0..K-1 (word 0 only,
+    # the other words stay 0).
+    c = SMALL[case]
     for mode, expect in (("eat", 1), ("topk", (1 << 8) - 1)):
         shape, w, lay, prm = _layer(c, mode)
         x = torch.zeros(5, c["d"], dtype=torch.bfloat16, device="cuda")
@@ -152,7 +160,7 @@ def test_route_zero_input_takes_lowest_indices():
 
 # ------------------------------------------------------------------ forward --
 
-@pytest.mark.parametrize("case", ["tiny", "mixtral", "finegrained", "shared"])
+@pytest.mark.parametrize("case", ["tiny", "mixtral", "finegrained", "shared"] + WIDE_E)
 @pytest.mark.parametrize("mode", ["eat", "topk", "topp"])
 @pytest.mark.parametrize("T", [1, 33, 200])
 def test_forward_parity(case, mode, T):
@@ -162,7 +170,7 @@ def test_forward_parity(case, mode, T):
     acc = make_accounts(c["E"], seed=7 + T, c_scale=0.05)
     if mode == "eat":
         lay.load_accounts(*acc)
-    mask = torch.empty(T, dtype=torch.int64, device="cuda")
+    mask = lay.mask_tensor(T)
     load = torch.empty(c["E"], dtype=torch.int32, device="cuda")
     y = lay.forward(_x_dev(x), mask_out=mask, load_out=load)
     torch.cuda.synchronize()
@@ -370,6 +378,42 @@ def test_full_finegrained_sampled(mode, T, prefill):
             np.testing.assert_allclose(cs, ref_acc[2], rtol=PT.TOL_C_BF16, atol=1e-6)
 
 
+@pytest.mark.parametrize("mode", ["topk", "topp", "eat"])
+@pytest.mark.parametrize("T,prefill", [(64, False), (4096, True)])
+def test_full_qwen3_sampled(mode, T, prefill):
+    """Qwen3-30B-A3B-shaped layer at full size (d=2048, E=128, F=768, K=8):
+    two mask words per token; decode batch 64 and a 4096-token prefill."""
+    shape = SHAPES["qwen3"]
+    w = make_layer_weights(shape)
+    p = L.eat_params_default(mode=MODES[mode], E=128, d_model=2048, d_ffn=768, top_k=8, top_p=0.6)
+    lay = EatLayer(p, T, to_device(w))
+    prm = PT.oracle_params(shape, MODES[mode])
+    x = make_prefill(shape) if prefill else HiddenStream(shape, T).next()
+    acc = make_accounts(128, seed=T, c_scale=0.05)
+    if mode == "eat":
+        lay.load_accounts(*acc)
+    mask = lay.mask_tensor(T)
+    assert mask.shape == (T, 2)
+    y = lay.forward(_x_dev(x), mask_out=mask)
+    torch.cuda.synchronize()
+    r = O.route(x, w["w_router"], acc, None, prm)
+    border = PT.borderline(r, prm)
+    gm = PT.masks_to_list(mask)
+    bad = [t for t in range(T) if not border[t] and gm[t] != r.masks[t]]
+    rng = np.random.default_rng(T)
+    sample = [int(t) for t in rng.choice(T, 16, replace=False) if not border[t]]
+    lo = O.layer_outputs(x, w, r, prm, tokens=sample)
+    err = PT.row_rel_err(_y_host(y)[sample], lo.y[sample])
+    PT.report(f"full qwen3 {mode} T={T}", borderline=int(border.sum()), mask_mismatch=len(bad),
+              max_rel_y=f"{err.max():.2e}", mean_k=f"{np.mean(r.k):.3f}",
+              upper_word_tokens=sum(1 for m in gm if m >> 64))
+    assert not bad
+    assert (err <= PT.TOL_Y_BF16).all()
+    lay.close()
+    del lay
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("T", [128, 8192])
 def test_full_shared_sampled(T):
     shape = SHAPES["shared"]
@@ -405,12 +449,16 @@ TILE_CASES = {
     # 2048-3000 tokens over 8 experts, K=2: 512-750 rows per expert, full
     # 256-token tiles plus ragged last ones
     "mixtral_wide": dict(shape="mixtral", d=512, F=768, E=8, Fs=0),
+    # 4096-4500 tokens over 128 experts, K=8: ~256-280 rows per expert on
+    # average, two mask words, 128 expert segments in the tile table
+    "qwen3_wide": dict(shape="qwen3", d=256, F=256, E=128, Fs=0),
 }
 
 
 @pytest.mark.parametrize("mode", ["eat", "topk", "topp"])
 @pytest.mark.parametrize("case,T", [("mixtral_tiles", 1024), ("mixtral_tiles", 1500), ("shared_tiles", 600),
-                                    ("mixtral_wide", 2048), ("mixtral_wide", 3000)])
+                                    ("mixtral_wide", 2048), ("mixtral_wide", 3000),
+                                    ("qwen3_wide", 4096), ("qwen3_wide", 4500)])
 def test_forward_parity_prefill_tiles(case, T, mode):
     c = TILE_CASES[case]
     shape, w, lay, prm = _layer(c, mode, max_tokens=T)
@@ -418,7 +466,7 @@ def test_forward_parity_prefill_tiles(case, T, mode):
     acc = make_accounts(c["E"], seed=T, c_scale=0.05)
     if mode == "eat":
         lay.load_accounts(*acc)
-    mask = torch.empty(T, dtype=torch.int64, device="cuda")
+    mask = lay.mask_tensor(T)
     y = lay.forward(_x_dev(x), mask_out=mask)
     torch.cuda.synchronize()
     ref = O.moe_step(x, w, acc if mode == "eat" else None, None, prm)

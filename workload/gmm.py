@@ -73,6 +73,11 @@ SHAPES = {
                          F_shared=5632, clusters=32, redraw=0.1, zipf=1.1,
                          decode_batches=(128,), decode_steps=256,
                          prefill_tokens=8192, prefill_seqs=16),
+    # Qwen3-30B-A3B-shaped MoE block: 128 routed experts (two 64-bit mask
+    # words per token), d=2048, F=768, Top-K=8; Top-P p=0.6 baseline.
+    "qwen3": LayerShape("qwen3", 6, d=2048, E=128, F=768, K=8, top_p=0.6, bf16=True,
+                        clusters=32, redraw=0.1, decode_batches=(64,), decode_steps=256,
+                        prefill_tokens=4096, prefill_seqs=8),
     # 16 stacked finegrained layers with independent accounts.
     "stack16": LayerShape("stack16", 5, d=2048, E=64, F=1024, K=8, top_p=0.6, bf16=True,
                           clusters=64, redraw=0.1, decode_batches=(64,), decode_steps=1024,
