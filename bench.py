@@ -25,10 +25,13 @@ layer-wise caps (2 in the lower 12 layers, K in the upper 4); a
 ``ppl_signal`` object times the LM-head perplexity signal (Sec. 3.3) for 64
 sequences at the Mixtral head shape.
 A ``prefill`` object adds the MFMA-bound side: one prefill call of the
-fine-grained layer (4096 tokens, 64 experts of width 1024, K=8) and of the
+fine-grained layer (4096 tokens, 64 experts of width 1024, K=8), of the
 shared-expert layer (8192 tokens, 60 experts of width 1408 + an always-on
-expert of width 5632, K=4), each starting from zero accounts, with the
-expert stages' achieved bf16 TFLOP/s against the dense MFMA peak.
+expert of width 5632, K=4) and of the Qwen3-30B-A3B-shaped layer (4096
+tokens, 128 experts of width 768, K=8), each starting from zero accounts,
+with the expert stages' achieved bf16 TFLOP/s against the dense MFMA peak.
+A ``wide_experts`` object times decode (batch 64) of that 128-expert layer,
+whose selection masks take two 64-bit words per token.
 
     python bench.py [--steps K] [--warmup W] [--batch B] [--gpus 1]
 """
@@ -88,19 +91,19 @@ class HipEvents:
         self.owned = []
 
 
-def popcounts(masks: np.ndarray) -> np.ndarray:
+def popcounts(masks: np.ndarray, words: int = 1) -> np.ndarray:
+    """Experts selected per token: masks [..., B] (one word per token) or
+    [..., B, words]."""
+    c = np.bitwise_count(masks.astype(np.uint64)).astype(np.int64)
+    return c.sum(axis=-1) if words > 1 else c
+
+
+def union_sizes(masks: np.ndarray, words: int = 1) -> np.ndarray:
+    """Experts touched by any token of each step: masks [steps, B(, words)]."""
     m = masks.astype(np.uint64)
-    return np.array([[bin(int(v)).count("1") for v in row] for row in m])
-
-
-def union_sizes(masks: np.ndarray) -> np.ndarray:
-    out = []
-    for row in masks.astype(np.uint64):
-        u = 0
-        for v in row:
-            u |= int(v)
-        out.append(bin(u).count("1"))
-    return np.array(out)
+    u = np.bitwise_or.reduce(m, axis=1)
+    c = np.bitwise_count(u).astype(np.int64)
+    return c.sum(axis=-1) if words > 1 else c
 
 
 def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bool, graph: bool = False):
@@ -118,9 +121,10 @@ def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bo
                              top_p=0.6, inv_temperature=shape.inv_temp)
     lay = EatLayer(p, B, wdev)
     E = shape.E
+    W = L.mask_words(E)
     y = torch.empty(B, shape.d, dtype=torch.bfloat16, device="cuda")
-    masks = torch.empty(steps, B, dtype=torch.int64, device="cuda")
-    scratch = torch.empty(B, dtype=torch.int64, device="cuda")
+    masks = torch.empty((steps, B) if W == 1 else (steps, B, W), dtype=torch.int64, device="cuda")
+    scratch = lay.mask_tensor(B)
     # warm-up on a scratch account state, then start from zero accounts
     for s in range(warmup):
         lay.forward(xs[s % xs.shape[0]], y=y, mask_out=scratch)
@@ -157,8 +161,8 @@ def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bo
         up_ms = np.array([ev.elapsed_ms(evs[3 * s], evs[3 * s + 1]) for s in range(steps)])
         dn_ms = np.array([ev.elapsed_ms(evs[3 * s + 1], evs[3 * s + 2]) for s in range(steps)])
     m = masks.cpu().numpy().astype(np.int64).view(np.uint64)
-    k = popcounts(m)
-    U = union_sizes(m)
+    k = popcounts(m, W)
+    U = union_sizes(m, W)
     acc = lay.accounts_host()
     del g
     lay.close()
@@ -180,7 +184,8 @@ def run_prefill(shape_name: str, reps: int, ev: HipEvents, modes=("eat", "topk")
     wdev = to_device(make_layer_weights(shape))
     x = torch.from_numpy(make_prefill(shape)).view(torch.bfloat16).cuda()
     y = torch.empty(T, shape.d, dtype=torch.bfloat16, device="cuda")
-    mask = torch.empty(T, dtype=torch.int64, device="cuda")
+    W = L.mask_words(shape.E)
+    mask = torch.empty((T,) if W == 1 else (T, W), dtype=torch.int64, device="cuda")
     d, F, Fs, E = shape.d, shape.F, shape.F_shared, shape.E
     out = {"workload": f"{shape_name} layer prefill", "tokens": T, "d_model": d, "experts": E, "d_ffn": F,
            "d_shared": Fs, "top_k": shape.K}
@@ -200,7 +205,7 @@ def run_prefill(shape_name: str, reps: int, ev: HipEvents, modes=("eat", "topk")
                 dn.append(ev.elapsed_ms(stage[L.EAT_STAGE_UP], stage[L.EAT_STAGE_DOWN]))
                 sh.append(ev.elapsed_ms(stage[L.EAT_STAGE_DOWN], stage[L.EAT_STAGE_SHARED]))
         lay.close()
-        sk = float(popcounts(mask.cpu().numpy().astype(np.int64).view(np.uint64)[None]).sum())
+        sk = float(popcounts(mask.cpu().numpy().astype(np.int64).view(np.uint64)[None], W).sum())
         t_ms, up_ms, dn_ms, sh_ms = (float(np.median(v)) for v in (tot, up, dn, sh))
         fl_up, fl_dn = 4.0 * d * F * sk, 2.0 * d * F * sk
         fl_sh = 6.0 * d * Fs * T
@@ -218,6 +223,43 @@ def run_prefill(shape_name: str, reps: int, ev: HipEvents, modes=("eat", "topk")
                            "frac": round(tf(fl_sh, sh_ms) / BF16_PEAK_TFLOPS, 4)}
         out[mode] = r
     del wdev
+    torch.cuda.empty_cache()
+    return out
+
+
+def run_decode(shape_name: str, steps: int, warmup: int, ev: HipEvents, modes=("eat", "topk", "topp")):
+    """Decode steps of one more layer shape (its own decode batch, zero
+    accounts after warm-up) per routing mode: tokens/s, activated experts,
+    experts touched and the expert kernels' achieved HBM bandwidth on their
+    algorithmic bytes."""
+    import torch
+
+    from paper_2609_33614_amd import _lib as L
+    from paper_2609_33614_amd.layer import to_device
+    from workload import SHAPES, HiddenStream, make_layer_weights
+
+    shape = SHAPES[shape_name]
+    B = shape.decode_batches[0]
+    wdev = to_device(make_layer_weights(shape))
+    xs = torch.from_numpy(HiddenStream(shape, B).steps(warmup + steps)).view(torch.bfloat16).cuda()
+    out = {"workload": f"{shape_name} layer decode", "batch": B, "d_model": shape.d, "experts": shape.E,
+           "d_ffn": shape.F, "top_k": shape.K, "mask_words": L.mask_words(shape.E), "steps": steps}
+    for name in modes:
+        r = run_mode(L.MODES[name], shape, wdev, xs, B, steps, warmup, ev, profile=True)
+        up_b = sum(traffic_up(shape, B, r["k"][s], r["U"][s]) for s in range(steps))
+        dn_b = sum(traffic_down(shape, r["k"][s], r["U"][s]) for s in range(steps))
+        up_gbs = up_b / (r["up_ms"].sum() / 1e3) / 1e9
+        dn_gbs = dn_b / (r["dn_ms"].sum() / 1e3) / 1e9
+        out[name] = {"tokens_per_s": round(B * steps / (r["total_ms"] / 1e3), 1),
+                     "ms_per_step": round(r["total_ms"] / steps, 4),
+                     "mean_activated_experts": round(float(r["k"].mean()), 4),
+                     "mean_experts_touched_per_step": round(float(r["U"].mean()), 3),
+                     "up_gate_us_per_launch": round(float(r["up_ms"].mean() * 1e3), 2),
+                     "up_gate_hbm_frac": round(up_gbs / HBM_PEAK_GBS, 4),
+                     "down_us_per_launch": round(float(r["dn_ms"].mean() * 1e3), 2),
+                     "down_hbm_frac": round(dn_gbs / HBM_PEAK_GBS, 4)}
+        log(f"{shape_name} decode {name}: {out[name]['tokens_per_s']} tok/s")
+    del wdev, xs
     torch.cuda.empty_cache()
     return out
 
@@ -390,6 +432,8 @@ def main(argv=None) -> int:
     ap.add_argument("--graph", action="store_true",
                     help="also time the decode steps as HIP graph replays and report those as the headline")
     ap.add_argument("--no-stack", action="store_true", help="skip the 16-layer stack measurement")
+    ap.add_argument("--no-wide-experts", action="store_true",
+                    help="skip the decode of the 128-expert (Qwen3-30B-A3B-shaped) layer")
     ap.add_argument("--stack-steps", type=int, default=1024)
     ap.add_argument("--only-stack", action="store_true", help="time only the 16-layer stack and print its JSON")
     ap.add_argument("--only-prefill", default="", metavar="LAYER",
@@ -494,9 +538,16 @@ def main(argv=None) -> int:
     if not args.no_prefill:
         del wdev
         torch.cuda.empty_cache()
-        for name in ("finegrained", "shared"):
+        for name in ("finegrained", "shared", "qwen3"):
             log(f"prefill {name}: {args.prefill_reps} timed calls per mode")
             prefill.append(run_prefill(name, args.prefill_reps, ev))
+    wide_e = None
+    if not args.no_wide_experts:
+        if "wdev" in locals():
+            del wdev
+            torch.cuda.empty_cache()
+        log("qwen3-shaped layer decode (128 experts)")
+        wide_e = run_decode("qwen3", K, W, ev)
     log("perplexity signal")
     ppl = run_ppl(ev)
     stack = None
@@ -543,6 +594,7 @@ def main(argv=None) -> int:
         "prefill": prefill,
         "stack": stack,
         "ppl_signal": ppl,
+        "wide_experts": wide_e,
     }
     print(json.dumps(out), flush=True)
     return 0

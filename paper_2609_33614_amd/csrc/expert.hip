@@ -8,7 +8,7 @@
 // the whole reduction dimension once, applying them to up to 16*NSUB
 // tokens of the same expert (the B operand, zero-padded).  Weight bytes are
 // read from HBM exactly once per token tile, which is what bounds decode.
-// The down projection may split its reduction dimension over gridDim.z;
+// The down projection may split its reduction dimension into slices;
 // the partial tiles are added, in split order, by the combine kernel.
 // Prefill-sized calls (hundreds of rows per expert) go to the wide MFMA
 // tiles of wide.hip instead.
@@ -99,7 +99,8 @@ struct StreamArgs {
     const int32_t* offsets;    // [groups+1] expert-major row offsets, or null
     int nrows;                 // rows of the single group when offsets is null
     int groups, M, K;
-    int ksplit;                // reduction length per gridDim.z slice
+    int splits;                // slices of the reduction dimension
+    int ksplit;                // reduction length per slice
     int64_t split_stride;      // elements between split slices of out / out2
     void* out;                 // gated: bf16 H [rows][M], or fp32 G partials
                                // [split][rows][M] when `partial`; plain: fp32 [split][rows][M]
@@ -144,11 +145,23 @@ __global__ __launch_bounds__(WPB * 64) void stream_kernel(StreamArgs a) {
     }
 
     const int i = lane & 15, g = lane >> 4;
-    const int m0 = blockIdx.x * (16 * WPB) + wave * 16;
-    const int kbeg = blockIdx.z * a.ksplit;
     const int nch = a.ksplit / KC;
+    const int nrb = a.M / (16 * WPB);                 // weight-row blocks
 
-    for (int tile = blockIdx.y; tile < ntiles; tile += gridDim.y) {
+    // Work items (token tile, reduction slice, row block), row block
+    // fastest; the grid holds about as many workgroups as the chip keeps
+    // resident, each taking items grid-stride.  Only the tiles in use count,
+    // so a call whose tokens land on few experts leaves no idle workgroups
+    // behind the working ones.
+    // (the launcher keeps the item count below 2^31)
+    const unsigned items = static_cast<unsigned>(ntiles) * a.splits * nrb;
+    for (unsigned w = blockIdx.x; w < items; w += gridDim.x) {
+        const int rb = static_cast<int>(w % nrb);
+        const unsigned rest = w / nrb;
+        const int split = static_cast<int>(rest % a.splits);
+        const int tile = static_cast<int>(rest / a.splits);
+        const int m0 = rb * (16 * WPB) + wave * 16;
+        const int kbeg = split * a.ksplit;
         int e = 0, r0, n;
         if (a.offsets) {
             e = tile_group(tstart, a.groups, tile);
@@ -256,7 +269,7 @@ __global__ __launch_bounds__(WPB * 64) void stream_kernel(StreamArgs a) {
             if (c >= n) continue;
             const size_t o = static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g;
             if (GATED && a.partial) {
-                const size_t po = blockIdx.z * a.split_stride + o;
+                const size_t po = split * a.split_stride + o;
                 *reinterpret_cast<float4*>(static_cast<float*>(a.out) + po) =
                     make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
                 *reinterpret_cast<float4*>(a.out2 + po) =
@@ -270,7 +283,7 @@ __global__ __launch_bounds__(WPB * 64) void stream_kernel(StreamArgs a) {
                 pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
                 *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + o) = pk;
             } else {
-                float* op = static_cast<float*>(a.out) + blockIdx.z * a.split_stride + o;
+                float* op = static_cast<float*>(a.out) + split * a.split_stride + o;
                 *reinterpret_cast<float4*>(op) =
                     make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
             }
@@ -347,40 +360,65 @@ constexpr int max_ks() {
 template <bool GATED, int NSUB>
 constexpr int stream_wpb() { return (!GATED && NSUB >= 4) ? 8 : 4; }
 
+// Workgroups of one stream-kernel instance the whole chip keeps resident
+// (occupancy per CU x CUs), asked once per instance.
+template <bool GATED, int NSUB, int KS, int WPB>
+int64_t stream_resident() {
+    static const int64_t v = [] {
+        int dev = 0, cus = 0, per_cu = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+            cus = 256;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, stream_kernel<GATED, NSUB, KS, WPB>, WPB * 64, 0) !=
+                hipSuccess ||
+            per_cu < 1)
+            per_cu = 1;
+        return static_cast<int64_t>(cus) * per_cu;
+    }();
+    return v;
+}
+
+// Grid: as many workgroups as there can be work items (max_tiles token
+// tiles x slices x row blocks), at most what the chip keeps resident.
+template <bool GATED, int NSUB, int KS, int WPB>
+hipError_t launch_stream_w(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
+    const int64_t items = max_tiles * a.splits * (a.M / (16 * WPB));
+    if (items >= (int64_t{1} << 31)) return hipErrorInvalidValue;
+    const int64_t blocks = std::max<int64_t>(1, std::min(items, stream_resident<GATED, NSUB, KS, WPB>()));
+    stream_kernel<GATED, NSUB, KS, WPB><<<dim3(static_cast<unsigned>(blocks)), dim3(WPB * 64), 0, s>>>(a);
+    return hipGetLastError();
+}
+
 template <bool GATED, int NSUB, int KS>
-hipError_t launch_stream_k(const StreamArgs& a, dim3 grid, hipStream_t s) {
+hipError_t launch_stream_k(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
     if constexpr (KS <= max_ks<GATED, NSUB>()) {
-        if (stream_wpb<GATED, NSUB>() == 8 && a.M % 128 == 0) {
-            grid.x = a.M / 128;
-            stream_kernel<GATED, NSUB, KS, 8><<<grid, dim3(512), 0, s>>>(a);
-        } else {
-            stream_kernel<GATED, NSUB, KS, 4><<<grid, dim3(256), 0, s>>>(a);
-        }
-        return hipGetLastError();
+        if (stream_wpb<GATED, NSUB>() == 8 && a.M % 128 == 0) return launch_stream_w<GATED, NSUB, KS, 8>(a, max_tiles, s);
+        return launch_stream_w<GATED, NSUB, KS, 4>(a, max_tiles, s);
     } else {
         return hipErrorInvalidValue;
     }
 }
 
 template <bool GATED, int NSUB>
-hipError_t launch_stream_n(const StreamArgs& a, int tiles_y, int splits, hipStream_t s) {
-    const dim3 grid(a.M / 64, tiles_y, splits);
+hipError_t launch_stream_n(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
     const int ks = std::min(pick_ks(a.ksplit), max_ks<GATED, NSUB>());
     switch (ks) {
-        case 8: return launch_stream_k<GATED, NSUB, 8>(a, grid, s);
-        case 4: return launch_stream_k<GATED, NSUB, 4>(a, grid, s);
-        case 2: return launch_stream_k<GATED, NSUB, 2>(a, grid, s);
-        default: return launch_stream_k<GATED, NSUB, 1>(a, grid, s);
+        case 8: return launch_stream_k<GATED, NSUB, 8>(a, max_tiles, s);
+        case 4: return launch_stream_k<GATED, NSUB, 4>(a, max_tiles, s);
+        case 2: return launch_stream_k<GATED, NSUB, 2>(a, max_tiles, s);
+        default: return launch_stream_k<GATED, NSUB, 1>(a, max_tiles, s);
     }
 }
 
+// `a.splits` slices of `a.ksplit` each; max_tiles bounds the token tiles a
+// call can hold (their count is only known on the device).
 template <bool GATED>
-hipError_t launch_stream(const StreamArgs& a, int nsub, int tiles_y, int splits, hipStream_t s) {
+hipError_t launch_stream(const StreamArgs& a, int nsub, int64_t max_tiles, hipStream_t s) {
     switch (nsub) {
-        case 1: return launch_stream_n<GATED, 1>(a, tiles_y, splits, s);
-        case 2: return launch_stream_n<GATED, 2>(a, tiles_y, splits, s);
-        case 4: return launch_stream_n<GATED, 4>(a, tiles_y, splits, s);
-        default: return launch_stream_n<GATED, 8>(a, tiles_y, splits, s);
+        case 1: return launch_stream_n<GATED, 1>(a, max_tiles, s);
+        case 2: return launch_stream_n<GATED, 2>(a, max_tiles, s);
+        case 4: return launch_stream_n<GATED, 4>(a, max_tiles, s);
+        default: return launch_stream_n<GATED, 8>(a, max_tiles, s);
     }
 }
 
@@ -471,10 +509,9 @@ hipError_t launch_dense_bf16(const uint16_t* src, int32_t T, const uint16_t* w, 
     const int bn = 16 * nsub;
     const int tiles = (T + bn - 1) / bn;
     StreamArgs a{};
-    a.wa = w; a.src = src; a.nrows = T; a.groups = 1; a.M = M; a.K = K; a.ksplit = K / splits;
+    a.wa = w; a.src = src; a.nrows = T; a.groups = 1; a.M = M; a.K = K; a.splits = splits; a.ksplit = K / splits;
     a.split_stride = split_stride; a.out = out;
-    const int cap = std::max(1, 2048 / std::max(1, (M / 64) * splits));
-    return launch_stream<false>(a, nsub, std::min(tiles, cap), splits, s);
+    return launch_stream<false>(a, nsub, tiles, s);
 }
 
 hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap, const float* x,
@@ -503,9 +540,6 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     // no expert holds more than T rows, so it needs at most ceil(T / bn) tiles
     const int64_t per_expert = (T + bn - 1) / bn;
     const int64_t max_tiles = std::min<int64_t>({rows_cap, per_expert * p.E, (rows_cap + bn - 1) / bn + p.E});
-    // keep roughly 8 workgroups per CU in flight; extra tiles loop
-    const int cap_up = std::max(1, 2048 / std::max(1, p.d_ffn / 64));
-    const int tiles_up = static_cast<int>(std::min<int64_t>(max_tiles, cap_up));
 
     if (use_wide(p, T)) {
         hipError_t err = launch_wide(true, w1, w3, x, tok_idx, offsets, p.E, 0, p.d_ffn, p.d_model, h, rows_cap, s);
@@ -516,12 +550,12 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     const int usplits = up_splits(p, T);
     StreamArgs up{};
     up.wa = w1; up.wb = w3; up.src = x; up.gather = tok_idx; up.offsets = offsets;
-    up.groups = p.E; up.M = p.d_ffn; up.K = p.d_model; up.ksplit = p.d_model / usplits;
+    up.groups = p.E; up.M = p.d_ffn; up.K = p.d_model; up.splits = usplits; up.ksplit = p.d_model / usplits;
     up.split_stride = rows_cap * p.d_ffn;
     up.partial = usplits > 1;
     up.out = up.partial ? static_cast<void*>(gu) : static_cast<void*>(h);
     up.out2 = up.partial ? gu + usplits * up.split_stride : nullptr;
-    hipError_t err = launch_stream<true>(up, nsub, tiles_up, usplits, s);
+    hipError_t err = launch_stream<true>(up, nsub, max_tiles, s);
     if (err != hipSuccess) return err;
     if (up.partial) {
         const int64_t vec = rows_cap * (p.d_ffn / 4);
@@ -533,13 +567,11 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     if (between) between();
 
     const int splits = down_splits(p, T);
-    const int cap_dn = std::max(1, 2048 / std::max(1, (p.d_model / 64) * splits));
-    const int tiles_dn = static_cast<int>(std::min<int64_t>(max_tiles, cap_dn));
     StreamArgs dn{};
     dn.wa = w2; dn.wb = nullptr; dn.src = h; dn.gather = nullptr; dn.offsets = offsets;
-    dn.groups = p.E; dn.M = p.d_model; dn.K = p.d_ffn; dn.ksplit = p.d_ffn / splits;
+    dn.groups = p.E; dn.M = p.d_model; dn.K = p.d_ffn; dn.splits = splits; dn.ksplit = p.d_ffn / splits;
     dn.split_stride = rows_cap * p.d_model; dn.out = yp;
-    return launch_stream<false>(dn, nsub, tiles_dn, splits, s);
+    return launch_stream<false>(dn, nsub, max_tiles, s);
 }
 
 hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* x, const uint16_t* ws1,
@@ -555,16 +587,14 @@ hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* 
     const int tiles = (T + bn - 1) / bn;
     StreamArgs up{};
     up.wa = ws1; up.wb = ws3; up.src = x; up.gather = nullptr; up.offsets = nullptr; up.nrows = T;
-    up.groups = 1; up.M = p.d_shared; up.K = p.d_model; up.ksplit = p.d_model; up.out = hs;
-    const int cap_up = std::max(1, 2048 / std::max(1, p.d_shared / 64));
-    hipError_t err = launch_stream<true>(up, nsub, std::min(tiles, cap_up), 1, s);
+    up.groups = 1; up.M = p.d_shared; up.K = p.d_model; up.splits = 1; up.ksplit = p.d_model; up.out = hs;
+    hipError_t err = launch_stream<true>(up, nsub, tiles, s);
     if (err != hipSuccess) return err;
     StreamArgs dn{};
     dn.wa = ws2; dn.wb = nullptr; dn.src = hs; dn.gather = nullptr; dn.offsets = nullptr; dn.nrows = T;
-    dn.groups = 1; dn.M = p.d_model; dn.K = p.d_shared; dn.ksplit = p.d_shared; dn.split_stride = 0;
+    dn.groups = 1; dn.M = p.d_model; dn.K = p.d_shared; dn.splits = 1; dn.ksplit = p.d_shared; dn.split_stride = 0;
     dn.out = ys;
-    const int cap_dn = std::max(1, 2048 / std::max(1, p.d_model / 64));
-    return launch_stream<false>(dn, nsub, std::min(tiles, cap_dn), 1, s);
+    return launch_stream<false>(dn, nsub, tiles, s);
 }
 
 }  // namespace eat
