@@ -51,6 +51,25 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "MoE-layer tokens/s + activated experts/token (EAT vs Top-K); HBM GB/s % peak"
+# expert-weight layout every timed layer uses ("packed": eat_pack_weights, set up
+# before timing like any weight load; "rows": row-major)
+LAYOUT = "packed"
+
+
+def layout_code() -> int:
+    from paper_2609_33614_amd import _lib as L
+    return L.EAT_LAYOUT_PACKED if LAYOUT == "packed" else L.EAT_LAYOUT_ROWS
+
+
+def device_weights(w_host):
+    """Host weights -> device tensors in the benchmark's layout."""
+    from paper_2609_33614_amd.layer import pack_weights, to_device
+    w = to_device(w_host)
+    if LAYOUT == "packed":
+        packed = pack_weights(w)
+        del w
+        return packed
+    return w
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0          # MI355X dense bf16 MFMA
 
@@ -118,7 +137,7 @@ def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bo
     from paper_2609_33614_amd.layer import EatLayer, capture
 
     p = L.eat_params_default(mode=mode, E=shape.E, d_model=shape.d, d_ffn=shape.F, top_k=shape.K,
-                             top_p=0.6, inv_temperature=shape.inv_temp)
+                             top_p=0.6, inv_temperature=shape.inv_temp, weight_layout=layout_code())
     lay = EatLayer(p, B, wdev)
     E = shape.E
     W = L.mask_words(E)
@@ -181,7 +200,7 @@ def run_prefill(shape_name: str, reps: int, ev: HipEvents, modes=("eat", "topk")
 
     shape = SHAPES[shape_name]
     T = shape.prefill_tokens
-    wdev = to_device(make_layer_weights(shape))
+    wdev = device_weights(make_layer_weights(shape))
     x = torch.from_numpy(make_prefill(shape)).view(torch.bfloat16).cuda()
     y = torch.empty(T, shape.d, dtype=torch.bfloat16, device="cuda")
     W = L.mask_words(shape.E)
@@ -191,7 +210,8 @@ def run_prefill(shape_name: str, reps: int, ev: HipEvents, modes=("eat", "topk")
            "d_shared": Fs, "top_k": shape.K}
     for mode in modes:
         p = L.eat_params_default(mode=L.MODES[mode], E=E, d_model=d, d_ffn=F, top_k=shape.K,
-                                 top_p=shape.top_p or 0.6, inv_temperature=shape.inv_temp, d_shared=Fs)
+                                 top_p=shape.top_p or 0.6, inv_temperature=shape.inv_temp, d_shared=Fs,
+                                 weight_layout=layout_code())
         lay = EatLayer(p, T, wdev)
         stage = ev.create(L.EAT_NUM_STAGE_EVENTS)
         tot, up, dn, sh = [], [], [], []
@@ -240,7 +260,7 @@ def run_decode(shape_name: str, steps: int, warmup: int, ev: HipEvents, modes=("
 
     shape = SHAPES[shape_name]
     B = shape.decode_batches[0]
-    wdev = to_device(make_layer_weights(shape))
+    wdev = device_weights(make_layer_weights(shape))
     xs = torch.from_numpy(HiddenStream(shape, B).steps(warmup + steps)).view(torch.bfloat16).cuda()
     out = {"workload": f"{shape_name} layer decode", "batch": B, "d_model": shape.d, "experts": shape.E,
            "d_ffn": shape.F, "top_k": shape.K, "mask_words": L.mask_words(shape.E), "steps": steps}
@@ -283,7 +303,7 @@ def run_stack(steps: int, warmup: int, ev: HipEvents, modes=("eat", "topk", "top
     t = time.time()
     wdev, mdev = [], []
     for l in range(nl):
-        wdev.append(to_device(make_layer_weights(shape, layer=l)))
+        wdev.append(device_weights(make_layer_weights(shape, layer=l)))
         mdev.append(torch.from_numpy(make_mixing(shape, l)).view(torch.bfloat16).cuda())
     log(f"stack weights ready in {time.time() - t:.1f} s ({nl} layers)")
     xs = torch.from_numpy(HiddenStream(shape, B).steps(warmup + steps)).view(torch.bfloat16).cuda()
@@ -295,7 +315,8 @@ def run_stack(steps: int, warmup: int, ev: HipEvents, modes=("eat", "topk", "top
         caps = layerwise_caps(nl, 12, 2, shape.K) if mode == "eat_layerwise" else [shape.K] * nl
         rmode = "eat" if mode == "eat_layerwise" else mode
         params = [L.eat_params_default(mode=L.MODES[rmode], E=E, d_model=d, d_ffn=F, top_k=caps[l],
-                                       top_p=shape.top_p, inv_temperature=shape.inv_temp) for l in range(nl)]
+                                       top_p=shape.top_p, inv_temperature=shape.inv_temp,
+                                       weight_layout=layout_code()) for l in range(nl)]
         st = EatStack(params, B, wdev, mdev)
         h = torch.empty(B, d, dtype=torch.bfloat16, device="cuda")
         masks = torch.empty(steps, nl, B, dtype=torch.int64, device="cuda")
@@ -432,6 +453,8 @@ def main(argv=None) -> int:
     ap.add_argument("--graph", action="store_true",
                     help="also time the decode steps as HIP graph replays and report those as the headline")
     ap.add_argument("--no-stack", action="store_true", help="skip the 16-layer stack measurement")
+    ap.add_argument("--layout", choices=("packed", "rows"), default="packed",
+                    help="expert-weight layout of every timed layer (default: packed)")
     ap.add_argument("--no-wide-experts", action="store_true",
                     help="skip the decode of the 128-expert (Qwen3-30B-A3B-shaped) layer")
     ap.add_argument("--stack-steps", type=int, default=1024)
@@ -443,6 +466,8 @@ def main(argv=None) -> int:
                     help="also run 4 plain device copies of MIB MiB (a known-size kernel for "
                          "calibrating HBM byte counters)")
     args = ap.parse_args(argv)
+    global LAYOUT
+    LAYOUT = args.layout
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the EAT layer path here is a single-GPU build "
@@ -474,7 +499,7 @@ def main(argv=None) -> int:
     log(f"generating weights d={shape.d} E={shape.E} F={shape.F}")
     t = time.time()
     w_host = make_layer_weights(shape)
-    wdev = to_device(w_host)
+    wdev = device_weights(w_host)
     log(f"weights ready in {time.time() - t:.1f} s; generating {W + K} steps of B={B}")
     xs_host = HiddenStream(shape, B).steps(W + K)
     xs = torch.from_numpy(xs_host).view(torch.bfloat16).cuda()
@@ -579,7 +604,8 @@ def main(argv=None) -> int:
         "config": {"workload": "Mixtral-shaped MoE layer decode, EAT routing",
                    "d_model": shape.d, "experts": shape.E, "d_ffn": shape.F, "top_k": shape.K,
                    "batch": B, "logit_scale": shape.inv_temp, "router": "fp32", "experts_dtype": "bf16",
-                   "launch": "HIP graph replay per step" if args.graph else "eager"},
+                   "launch": "HIP graph replay per step" if args.graph else "eager",
+                   "weight_layout": LAYOUT},
         "roofline": {"bound": "hbm", "kernel": "expert up/gate (stream_kernel<gated>)",
                      "achieved": round(up_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(up_gbs / HBM_PEAK_GBS, 4),

@@ -29,9 +29,11 @@
  *    is reported as EAT_ERR_HIP (the enqueued work up to the failure may
  *    have run).
  *  - Limits: 1 <= E <= 256 (a token's mask is up to four 64-bit words);
- *    1 <= top_k <= E; d_model, d_ffn and d_shared are multiples of 64;
+ *    1 <= top_k <= E; d_model, d_ffn and d_shared are multiples of 64, with
+ *    d_model * max(d_ffn, d_shared) < 2^31 elements per expert matrix;
  *    activations and expert weights are both fp32 or both bf16.
- *  - Layouts (all row-major, densely packed, 16-byte aligned):
+ *  - Layouts (all row-major, densely packed, 16-byte aligned; the expert
+ *    weights may instead be packed, see eat_layout_t):
  *      x        [T][d_model]            act_dtype
  *      w_router [E][d_model]            fp32
  *      w1, w3   [E][d_ffn][d_model]     expert_dtype  (gate / up rows)
@@ -74,12 +76,20 @@ typedef enum {
 
 typedef enum { EAT_F32 = 0, EAT_BF16 = 1 } eat_dtype_t;
 
+/* Layout of the bf16 expert weights w1, w3, w2 (and ws1, ws3, ws2).
+ * ROWS: row-major as in the file header.  PACKED: the form eat_pack_weights
+ * writes -- each matrix [groups][M][K] as 1 KB blocks of 16 rows x 32
+ * reduction elements (block (g, r, s) at index (g M / 16 + r) K / 32 + s,
+ * lane order of the matrix-core operand inside a block), which the decode
+ * kernels read one contiguous kilobyte per load instruction. */
+typedef enum { EAT_LAYOUT_ROWS = 0, EAT_LAYOUT_PACKED = 1 } eat_layout_t;
+
 /* Layer shape and routing hyper-parameters.  eat_params_default() fills the
  * values of the paper's hyper-parameter table (Sec. 4.1) and the constants
  * of Sec. 3.3 / Eq. 7; the caller then sets the shape fields. */
 typedef struct {
     int32_t mode;            /* eat_mode_t                                          */
-    int32_t E;               /* routed experts, 1..64                               */
+    int32_t E;               /* routed experts, 1..256                              */
     int32_t d_model;         /* hidden width d                                      */
     int32_t d_ffn;           /* expert FFN width F                                  */
     int32_t top_k;           /* K: EAT's cap (Eq. 6) and Top-K's k; default 2       */
@@ -106,6 +116,8 @@ typedef struct {
                                   pointer is kept by eat_create and must stay valid,
                                   with s_i >= 0 and sum_j s_j p_j > 0, while the handle
                                   is used; 4-byte aligned.                          */
+    int32_t weight_layout;   /* eat_layout_t of the expert weights; ROWS (default).
+                                PACKED needs bf16 experts (UNSUPPORTED otherwise). */
 } eat_params_t;
 
 /* Per-layer account state (Sec. 3.2), device memory, length E each, owned by
@@ -290,7 +302,7 @@ eat_status_t eat_stack_forward(const eat_stack_layer_t* layers, int32_t n_layers
  * eat_moe_forward / eat_stack_forward take for those sequences' tokens. */
 
 /* Workspace bytes for S sequences, width d (multiple of 64) and vocabulary
- * V (multiple of 64).  EAT_ERR_INVALID_ARG otherwise. */
+ * V (multiple of 64), d * V < 2^31.  EAT_ERR_INVALID_ARG otherwise. */
 eat_status_t eat_ppl_workspace_size(int32_t S, int32_t d, int32_t V, size_t* bytes);
 
 /* Zero the running state of S sequences (device arrays, caller-owned):
@@ -312,6 +324,18 @@ eat_status_t eat_ppl_reset(int32_t S, double* nll_sum, int32_t* count, double* p
 eat_status_t eat_ppl_trend(const void* h, int32_t S, int32_t d, const void* w_vocab, int32_t V,
                            const int32_t* target, double* nll_sum, int32_t* count, double* ppl_prev,
                            int8_t* trend_out, float* nll_out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---- packed expert weights -------------------------------------------------
+ *
+ * Write the PACKED form (eat_layout_t) of `groups` row-major bf16 matrices
+ * [groups][M][K] (device src) into dst (device, groups * M * K bf16, must not
+ * overlap src); e.g. w1 as (E, d_ffn, d_model), w2 as (E, d_model, d_ffn),
+ * ws1 as (1, d_shared, d_model).  M a multiple of 16, K of 32, both > 0;
+ * groups >= 1; 16-byte aligned pointers.  A permutation: a layer created with
+ * weight_layout = PACKED on the packed copies computes bit-identical results.
+ * Enqueues on `stream` only.  Errors: EAT_ERR_INVALID_ARG, EAT_ERR_HIP. */
+eat_status_t eat_pack_weights(const void* src, int32_t groups, int32_t M, int32_t K, void* dst,
+                              hipStream_t stream);
 
 /* Static description of a status code (never NULL). */
 const char* eat_status_string(eat_status_t s);

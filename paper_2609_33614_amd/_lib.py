@@ -17,6 +17,7 @@ LIB_PATH = os.environ.get("EAT_LIB_PATH") or os.path.join(_HERE, "libeat.so")
 EAT_OK, EAT_ERR_INVALID_ARG, EAT_ERR_UNSUPPORTED, EAT_ERR_WORKSPACE, EAT_ERR_HIP, EAT_ERR_INTERNAL = range(6)
 EAT_MODE_EAT, EAT_MODE_TOPK, EAT_MODE_TOPP = 0, 1, 2
 EAT_F32, EAT_BF16 = 0, 1
+EAT_LAYOUT_ROWS, EAT_LAYOUT_PACKED = 0, 1
 (EAT_STAGE_BEGIN, EAT_STAGE_ROUTED, EAT_STAGE_PERMUTED, EAT_STAGE_UP, EAT_STAGE_DOWN, EAT_STAGE_SHARED,
  EAT_STAGE_COMBINED, EAT_STAGE_END, EAT_NUM_STAGE_EVENTS) = range(9)
 MODES = {"eat": EAT_MODE_EAT, "topk": EAT_MODE_TOPK, "topp": EAT_MODE_TOPP}
@@ -37,7 +38,7 @@ class eat_params_t(C.Structure):
         ("kappa1", C.c_float), ("kappa2", C.c_float), ("ppl_up", C.c_float), ("ppl_down", C.c_float),
         ("q_lo", C.c_float), ("q_hi", C.c_float), ("eps", C.c_float), ("inv_temperature", C.c_float),
         ("cs_mode", C.c_int32), ("act_dtype", C.c_int32), ("expert_dtype", C.c_int32),
-        ("d_shared", C.c_int32), ("expert_scale", C.c_void_p),
+        ("d_shared", C.c_int32), ("expert_scale", C.c_void_p), ("weight_layout", C.c_int32),
     ]
 
 
@@ -83,12 +84,14 @@ def load() -> C.CDLL:
         lib.eat_ppl_workspace_size.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_size_t)]
         lib.eat_ppl_reset.argtypes = [C.c_int32, P, P, P, P]
         lib.eat_ppl_trend.argtypes = [P, C.c_int32, C.c_int32, P, C.c_int32, P, P, P, P, P, P, P, C.c_size_t, P]
+    if hasattr(lib, "eat_pack_weights"):
+        lib.eat_pack_weights.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, P, P]
     lib.eat_status_string.argtypes = [C.c_int]
     lib.eat_status_string.restype = C.c_char_p
     for name in ("eat_params_default", "eat_create", "eat_destroy", "eat_workspace_size", "eat_route_workspace_size",
                  "eat_reset_accounts", "eat_route", "eat_moe_forward", "eat_moe_forward_profiled",
                  "eat_stack_workspace_size", "eat_stack_forward", "eat_ppl_workspace_size", "eat_ppl_reset",
-                 "eat_ppl_trend"):
+                 "eat_ppl_trend", "eat_pack_weights"):
         if hasattr(lib, name):
             getattr(lib, name).restype = st
     _lib = lib
@@ -236,3 +239,8 @@ def eat_ppl_trend(h, S: int, d: int, w_vocab, V: int, target, nll_sum, count, pp
     _check(load().eat_ppl_trend(_ptr(h), int(S), int(d), _ptr(w_vocab), int(V), _ptr(target), _ptr(nll_sum),
                                 _ptr(count), _ptr(ppl_prev), _ptr(trend_out), _ptr(nll_out), _ptr(ws), int(ws_bytes),
                                 _stream(stream)), "eat_ppl_trend")
+
+
+def eat_pack_weights(src, groups: int, M: int, K: int, dst, stream=None) -> None:
+    _check(load().eat_pack_weights(_ptr(src), int(groups), int(M), int(K), _ptr(dst), _stream(stream)),
+           "eat_pack_weights")

@@ -41,7 +41,12 @@ eat_status_t check_params(const eat_params_t& p) {
     // supported shapes and dtype pairs
     if (p.E > eat::kMaxExperts) return EAT_ERR_UNSUPPORTED;
     if (p.d_model % 64 || p.d_ffn % 64 || p.d_shared % 64) return EAT_ERR_UNSUPPORTED;
+    // one expert matrix is addressed with 32-bit element offsets
+    if (static_cast<int64_t>(p.d_model) * std::max(p.d_ffn, p.d_shared) >= (int64_t{1} << 31))
+        return EAT_ERR_UNSUPPORTED;
     if (p.act_dtype != p.expert_dtype) return EAT_ERR_UNSUPPORTED;
+    if (p.weight_layout != EAT_LAYOUT_ROWS && p.weight_layout != EAT_LAYOUT_PACKED) return EAT_ERR_INVALID_ARG;
+    if (p.weight_layout == EAT_LAYOUT_PACKED && p.expert_dtype != EAT_BF16) return EAT_ERR_UNSUPPORTED;
     return EAT_OK;
 }
 
@@ -110,6 +115,7 @@ eat_status_t eat_params_default(eat_params_t* out) {
     out->expert_dtype = EAT_BF16;
     out->d_shared = 0;
     out->expert_scale = nullptr;
+    out->weight_layout = EAT_LAYOUT_ROWS;
     return EAT_OK;
 }
 
@@ -420,8 +426,23 @@ eat_status_t eat_moe_forward(eat_handle_t h, const void* x, int32_t T, const flo
                                     expert_load_out, ws, ws_bytes, stream, nullptr, 0);
 }
 
+eat_status_t eat_pack_weights(const void* src, int32_t groups, int32_t M, int32_t K, void* dst,
+                              hipStream_t stream) {
+    if (!src || !dst || groups < 1 || M < 16 || K < 32 || M % 16 || K % 32) return EAT_ERR_INVALID_ARG;
+    if (!aligned(src, 16) || !aligned(dst, 16)) return EAT_ERR_INVALID_ARG;
+    const uintptr_t bytes = static_cast<uintptr_t>(groups) * M * K * 2;
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+    if (s0 < d0 + bytes && d0 < s0 + bytes) return EAT_ERR_INVALID_ARG;     // overlapping buffers
+    (void)hipGetLastError();
+    return eat::launch_pack(static_cast<const uint16_t*>(src), groups, M, K, static_cast<uint16_t*>(dst), stream) ==
+                   hipSuccess
+               ? EAT_OK
+               : EAT_ERR_HIP;
+}
+
 eat_status_t eat_ppl_workspace_size(int32_t S, int32_t d, int32_t V, size_t* bytes) {
     if (!bytes || S < 0 || S > kMaxTokens || d < 64 || d % 64 || V < 64 || V % 64) return EAT_ERR_INVALID_ARG;
+    if (static_cast<int64_t>(d) * V >= (int64_t{1} << 31)) return EAT_ERR_INVALID_ARG;
     *bytes = align256(static_cast<size_t>(eat::ppl_splits(S, d, V)) * S * V * 4) +
              align256(static_cast<size_t>(S) * eat::ppl_chunks(V) * 8);
     return EAT_OK;

@@ -129,11 +129,16 @@ int up_splits(const eat_params_t& p, int32_t T);
 // gated = H = bf16(silu(x W1^T) * (x W3^T)) over 128-feature tiles, plain =
 // fp32 out = src W^T over 256-row tiles.  Rows are the expert segments given
 // by offsets (gather maps them to source rows), or nrows identity rows when
-// offsets is null.  wide_fits tells whether M and K suit the tiling.
+// offsets is null.  wide_fits tells whether M and K suit the tiling; `packed`
+// reads wa / wb in the packed layout.
 bool wide_fits(bool gated, int M, int K);
 hipError_t launch_wide(bool gated, const uint16_t* wa, const uint16_t* wb, const uint16_t* src,
                        const int32_t* gather, const int32_t* offsets, int groups, int nrows, int M,
-                       int K, void* out, int64_t rows_cap, hipStream_t s);
+                       int K, void* out, int64_t rows_cap, bool packed, hipStream_t s);
+
+// Packed weight layout (pack.hip): dst = the 1 KB-block form of the
+// row-major bf16 [groups][M][K] src (M % 16 == 0, K % 32 == 0).
+hipError_t launch_pack(const uint16_t* src, int32_t groups, int32_t M, int32_t K, uint16_t* dst, hipStream_t s);
 
 // Perplexity signal (ppl.hip): z [S][V] fp32 LM-head rows -> NLL of target,
 // running per-sequence state (fp64 NLL sum, count, previous perplexity) and

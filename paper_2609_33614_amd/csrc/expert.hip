@@ -111,6 +111,15 @@ struct StreamArgs {
 __device__ __forceinline__ bf16x8 ld16(const uint16_t* p) {
     return *reinterpret_cast<const bf16x8*>(p);
 }
+// Weight bytes are streamed once per launch.  Read as whole kilobytes (the
+// packed layout), non-temporal loads (streaming cache policy) reach a
+// measured ~6.3 TB/s against ~5.5 TB/s for plain loads of the same 512 MiB;
+// on row-major rows, where one load instruction covers 64 bytes of each of
+// 16 rows, they are slower than plain loads (~5.0 against ~5.2-5.4 TB/s),
+// so only the packed path uses them.
+__device__ __forceinline__ bf16x8 ld16_stream(const uint16_t* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(p));
+}
 
 // One workgroup = 4 waves = 64 consecutive weight rows (16 per wave) of one
 // expert, applied to one tile of up to 16*NSUB of that expert's tokens.
@@ -123,8 +132,11 @@ __device__ __forceinline__ bf16x8 ld16(const uint16_t* p) {
 // 16*KS*(GATED ? 2 : 1) bytes per lane of weights in flight.
 // Token sub-tiles beyond the tile's row count are skipped (uniform branch),
 // so a tile of 1 token costs one MFMA per k-step and matrix.
-template <bool GATED, int NSUB, int KS, int WPB>
-__global__ __launch_bounds__(WPB * 64) void stream_kernel(StreamArgs a) {
+// At least 3 waves per SIMD: the register budget then keeps the MFMA
+// accumulators in VGPRs (no AGPR copies) and the 64-token gated variant
+// holds 3 waves per SIMD instead of 2 (measured: more weight bytes in flight).
+template <bool GATED, int NSUB, int KS, int WPB, bool PACKED>
+__global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))) void stream_kernel(StreamArgs a) {
     constexpr int NT = WPB * 64;                      // threads per workgroup
     constexpr int BN = 16 * NSUB;
     constexpr int KC = 32 * KS;
@@ -172,7 +184,11 @@ __global__ __launch_bounds__(WPB * 64) void stream_kernel(StreamArgs a) {
             n = min(BN, a.nrows - r0);
         }
         const int nsub = (n + 15) >> 4;
-        const size_t wrow = (static_cast<size_t>(e) * a.M + m0 + i) * a.K + 8 * g;
+        // Row-major weights: this lane's 8 elements of row m0 + i at k-offset
+        // 8 g of each 32-wide k-step.  Packed weights: the wave's 16 rows form
+        // one 1 KB block per k-step, lane l's fragment at 16 l bytes.
+        const size_t wrow = PACKED ? (static_cast<size_t>(e) * (a.M / 16) + m0 / 16) * (a.K / 32) * 512 + 8 * lane
+                                   : (static_cast<size_t>(e) * a.M + m0 + i) * a.K + 8 * g;
         const uint16_t* pa = a.wa + wrow;
         const uint16_t* pb = GATED ? a.wb + wrow : nullptr;
 
@@ -207,8 +223,14 @@ __global__ __launch_bounds__(WPB * 64) void stream_kernel(StreamArgs a) {
             const int k = kbeg + c * KC;
 #pragma unroll
             for (int j = 0; j < KS; ++j) {
-                A[j] = ld16(pa + k + 32 * j);
-                if constexpr (GATED) B[j] = ld16(pb + k + 32 * j);
+                if constexpr (PACKED) {
+                    const size_t o = static_cast<size_t>(k / 32 + j) * 512;
+                    A[j] = ld16_stream(pa + o);
+                    if constexpr (GATED) B[j] = ld16_stream(pb + o);
+                } else {
+                    A[j] = ld16(pa + k + 32 * j);
+                    if constexpr (GATED) B[j] = ld16(pb + k + 32 * j);
+                }
             }
         };
 
@@ -362,15 +384,15 @@ constexpr int stream_wpb() { return (!GATED && NSUB >= 4) ? 8 : 4; }
 
 // Workgroups of one stream-kernel instance the whole chip keeps resident
 // (occupancy per CU x CUs), asked once per instance.
-template <bool GATED, int NSUB, int KS, int WPB>
+template <bool GATED, int NSUB, int KS, int WPB, bool PACKED>
 int64_t stream_resident() {
     static const int64_t v = [] {
         int dev = 0, cus = 0, per_cu = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
             cus = 256;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, stream_kernel<GATED, NSUB, KS, WPB>, WPB * 64, 0) !=
-                hipSuccess ||
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, stream_kernel<GATED, NSUB, KS, WPB, PACKED>,
+                                                         WPB * 64, 0) != hipSuccess ||
             per_cu < 1)
             per_cu = 1;
         return static_cast<int64_t>(cus) * per_cu;
@@ -380,46 +402,55 @@ int64_t stream_resident() {
 
 // Grid: as many workgroups as there can be work items (max_tiles token
 // tiles x slices x row blocks), at most what the chip keeps resident.
-template <bool GATED, int NSUB, int KS, int WPB>
+template <bool GATED, int NSUB, int KS, int WPB, bool PACKED>
 hipError_t launch_stream_w(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
     const int64_t items = max_tiles * a.splits * (a.M / (16 * WPB));
     if (items >= (int64_t{1} << 31)) return hipErrorInvalidValue;
-    const int64_t blocks = std::max<int64_t>(1, std::min(items, stream_resident<GATED, NSUB, KS, WPB>()));
-    stream_kernel<GATED, NSUB, KS, WPB><<<dim3(static_cast<unsigned>(blocks)), dim3(WPB * 64), 0, s>>>(a);
+    const int64_t blocks = std::max<int64_t>(1, std::min(items, stream_resident<GATED, NSUB, KS, WPB, PACKED>()));
+    stream_kernel<GATED, NSUB, KS, WPB, PACKED><<<dim3(static_cast<unsigned>(blocks)), dim3(WPB * 64), 0, s>>>(a);
     return hipGetLastError();
 }
 
-template <bool GATED, int NSUB, int KS>
+template <bool GATED, int NSUB, int KS, bool PACKED>
 hipError_t launch_stream_k(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
-    if constexpr (KS <= max_ks<GATED, NSUB>()) {
-        if (stream_wpb<GATED, NSUB>() == 8 && a.M % 128 == 0) return launch_stream_w<GATED, NSUB, KS, 8>(a, max_tiles, s);
-        return launch_stream_w<GATED, NSUB, KS, 4>(a, max_tiles, s);
-    } else {
+    if constexpr (KS > max_ks<GATED, NSUB>()) {
         return hipErrorInvalidValue;
+    } else if constexpr (stream_wpb<GATED, NSUB>() == 8) {
+        if (a.M % 128 == 0) return launch_stream_w<GATED, NSUB, KS, 8, PACKED>(a, max_tiles, s);
+        return launch_stream_w<GATED, NSUB, KS, 4, PACKED>(a, max_tiles, s);
+    } else {
+        return launch_stream_w<GATED, NSUB, KS, 4, PACKED>(a, max_tiles, s);
     }
 }
 
-template <bool GATED, int NSUB>
+template <bool GATED, int NSUB, bool PACKED>
 hipError_t launch_stream_n(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
     const int ks = std::min(pick_ks(a.ksplit), max_ks<GATED, NSUB>());
     switch (ks) {
-        case 8: return launch_stream_k<GATED, NSUB, 8>(a, max_tiles, s);
-        case 4: return launch_stream_k<GATED, NSUB, 4>(a, max_tiles, s);
-        case 2: return launch_stream_k<GATED, NSUB, 2>(a, max_tiles, s);
-        default: return launch_stream_k<GATED, NSUB, 1>(a, max_tiles, s);
+        case 8: return launch_stream_k<GATED, NSUB, 8, PACKED>(a, max_tiles, s);
+        case 4: return launch_stream_k<GATED, NSUB, 4, PACKED>(a, max_tiles, s);
+        case 2: return launch_stream_k<GATED, NSUB, 2, PACKED>(a, max_tiles, s);
+        default: return launch_stream_k<GATED, NSUB, 1, PACKED>(a, max_tiles, s);
+    }
+}
+
+template <bool GATED, bool PACKED>
+hipError_t launch_stream_p(const StreamArgs& a, int nsub, int64_t max_tiles, hipStream_t s) {
+    switch (nsub) {
+        case 1: return launch_stream_n<GATED, 1, PACKED>(a, max_tiles, s);
+        case 2: return launch_stream_n<GATED, 2, PACKED>(a, max_tiles, s);
+        case 4: return launch_stream_n<GATED, 4, PACKED>(a, max_tiles, s);
+        default: return launch_stream_n<GATED, 8, PACKED>(a, max_tiles, s);
     }
 }
 
 // `a.splits` slices of `a.ksplit` each; max_tiles bounds the token tiles a
-// call can hold (their count is only known on the device).
+// call can hold (their count is only known on the device); `packed` selects
+// the packed weight layout (pack.hip).
 template <bool GATED>
-hipError_t launch_stream(const StreamArgs& a, int nsub, int64_t max_tiles, hipStream_t s) {
-    switch (nsub) {
-        case 1: return launch_stream_n<GATED, 1>(a, max_tiles, s);
-        case 2: return launch_stream_n<GATED, 2>(a, max_tiles, s);
-        case 4: return launch_stream_n<GATED, 4>(a, max_tiles, s);
-        default: return launch_stream_n<GATED, 8>(a, max_tiles, s);
-    }
+hipError_t launch_stream(const StreamArgs& a, int nsub, int64_t max_tiles, bool packed, hipStream_t s) {
+    return packed ? launch_stream_p<GATED, true>(a, nsub, max_tiles, s)
+                  : launch_stream_p<GATED, false>(a, nsub, max_tiles, s);
 }
 
 }  // namespace
@@ -504,14 +535,15 @@ int dense_splits(int M, int K, int32_t T) {
 
 hipError_t launch_dense_bf16(const uint16_t* src, int32_t T, const uint16_t* w, int M, int K, float* out,
                              int splits, int64_t split_stride, hipStream_t s) {
-    if (dense_wide(M, K, T)) return launch_wide(false, w, nullptr, src, nullptr, nullptr, 1, T, M, K, out, T, s);
+    if (dense_wide(M, K, T))
+        return launch_wide(false, w, nullptr, src, nullptr, nullptr, 1, T, M, K, out, T, false, s);
     const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;
     const int tiles = (T + bn - 1) / bn;
     StreamArgs a{};
     a.wa = w; a.src = src; a.nrows = T; a.groups = 1; a.M = M; a.K = K; a.splits = splits; a.ksplit = K / splits;
     a.split_stride = split_stride; a.out = out;
-    return launch_stream<false>(a, nsub, tiles, s);
+    return launch_stream<false>(a, nsub, tiles, false, s);
 }
 
 hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap, const float* x,
@@ -541,11 +573,14 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     const int64_t per_expert = (T + bn - 1) / bn;
     const int64_t max_tiles = std::min<int64_t>({rows_cap, per_expert * p.E, (rows_cap + bn - 1) / bn + p.E});
 
+    const bool packed = p.weight_layout == EAT_LAYOUT_PACKED;
     if (use_wide(p, T)) {
-        hipError_t err = launch_wide(true, w1, w3, x, tok_idx, offsets, p.E, 0, p.d_ffn, p.d_model, h, rows_cap, s);
+        hipError_t err =
+            launch_wide(true, w1, w3, x, tok_idx, offsets, p.E, 0, p.d_ffn, p.d_model, h, rows_cap, packed, s);
         if (err != hipSuccess) return err;
         if (between) between();
-        return launch_wide(false, w2, nullptr, h, nullptr, offsets, p.E, 0, p.d_model, p.d_ffn, yp, rows_cap, s);
+        return launch_wide(false, w2, nullptr, h, nullptr, offsets, p.E, 0, p.d_model, p.d_ffn, yp, rows_cap, packed,
+                           s);
     }
     const int usplits = up_splits(p, T);
     StreamArgs up{};
@@ -555,7 +590,7 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     up.partial = usplits > 1;
     up.out = up.partial ? static_cast<void*>(gu) : static_cast<void*>(h);
     up.out2 = up.partial ? gu + usplits * up.split_stride : nullptr;
-    hipError_t err = launch_stream<true>(up, nsub, max_tiles, s);
+    hipError_t err = launch_stream<true>(up, nsub, max_tiles, packed, s);
     if (err != hipSuccess) return err;
     if (up.partial) {
         const int64_t vec = rows_cap * (p.d_ffn / 4);
@@ -571,16 +606,18 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     dn.wa = w2; dn.wb = nullptr; dn.src = h; dn.gather = nullptr; dn.offsets = offsets;
     dn.groups = p.E; dn.M = p.d_model; dn.K = p.d_ffn; dn.splits = splits; dn.ksplit = p.d_ffn / splits;
     dn.split_stride = rows_cap * p.d_model; dn.out = yp;
-    return launch_stream<false>(dn, nsub, max_tiles, s);
+    return launch_stream<false>(dn, nsub, max_tiles, packed, s);
 }
 
 hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* x, const uint16_t* ws1,
                               const uint16_t* ws3, const uint16_t* ws2, uint16_t* hs, float* ys,
                               hipStream_t s) {
+    const bool packed = p.weight_layout == EAT_LAYOUT_PACKED;
     if (shared_wide(p, T)) {
-        hipError_t err = launch_wide(true, ws1, ws3, x, nullptr, nullptr, 1, T, p.d_shared, p.d_model, hs, T, s);
+        hipError_t err =
+            launch_wide(true, ws1, ws3, x, nullptr, nullptr, 1, T, p.d_shared, p.d_model, hs, T, packed, s);
         if (err != hipSuccess) return err;
-        return launch_wide(false, ws2, nullptr, hs, nullptr, nullptr, 1, T, p.d_model, p.d_shared, ys, T, s);
+        return launch_wide(false, ws2, nullptr, hs, nullptr, nullptr, 1, T, p.d_model, p.d_shared, ys, T, packed, s);
     }
     const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;
@@ -588,13 +625,13 @@ hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* 
     StreamArgs up{};
     up.wa = ws1; up.wb = ws3; up.src = x; up.gather = nullptr; up.offsets = nullptr; up.nrows = T;
     up.groups = 1; up.M = p.d_shared; up.K = p.d_model; up.splits = 1; up.ksplit = p.d_model; up.out = hs;
-    hipError_t err = launch_stream<true>(up, nsub, tiles, s);
+    hipError_t err = launch_stream<true>(up, nsub, tiles, packed, s);
     if (err != hipSuccess) return err;
     StreamArgs dn{};
     dn.wa = ws2; dn.wb = nullptr; dn.src = hs; dn.gather = nullptr; dn.offsets = nullptr; dn.nrows = T;
     dn.groups = 1; dn.M = p.d_model; dn.K = p.d_shared; dn.splits = 1; dn.ksplit = p.d_shared; dn.split_stride = 0;
     dn.out = ys;
-    return launch_stream<false>(dn, nsub, tiles, s);
+    return launch_stream<false>(dn, nsub, tiles, packed, s);
 }
 
 }  // namespace eat

@@ -55,50 +55,68 @@ __device__ __forceinline__ int wswz(int r, int v) {
     return r * 128 + ((v ^ ((r >> 1) & 7)) << 4);
 }
 
-template <bool GATED>
+template <bool GATED, bool PACKED>
 __device__ __forceinline__ void wide_tile(const WideArgs& a, uint8_t* ring, int e, int r0, int n, int m0) {
     constexpr int NB = (kWM + kWN) / 8;       // 1 KB DMA blocks (8 rows each) per stage
     constexpr int BPW = NB / kWaves;          // per wave
     static_assert(NB % kWaves == 0, "blocks split evenly over the waves");
+    static_assert(kWM / 8 == kWaves * (BPW / 2), "a wave's first half of blocks are token rows");
     const int lane = lane_id(), wave = threadIdx.x / kWave;
     const int l32 = lane & 31, lh = lane >> 5;
     const int wm = wave >> 2, wn = wave & 3;  // token quarter, weight quarter (SIMD = wave % 4)
 
     // Lane l of a DMA instruction writes LDS bytes [16 l, 16 l + 16) of its
     // 1 KB block = row l / 8, slot l % 8; it fetches the global vector that
-    // belongs in that slot under the swizzle.
-    const uint16_t* srcp[BPW];
-    int dst[BPW];
+    // belongs in that slot under the swizzle.  Blocks j < BPW / 2 hold token
+    // rows (a 64-bit source per lane: rows are gathered), the others weight
+    // rows of expert e: W1 for j = BPW / 2 and W3 for j = BPW / 2 + 1 in the
+    // gated tile, so their base is uniform and each lane keeps a 32-bit
+    // element offset into the expert's matrix (M K < 2^31, checked on the host).
+    constexpr int BT = BPW / 2;
+    const uint16_t* srct[BT];
+    uint32_t woff[BPW - BT];
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
         const int b = wave + kWaves * j;
         const int slot = lane & 7;
-        if (b < kWM / 8) {
+        if (j < BT) {
             const int r = 8 * b + (lane >> 3);
             const int v = slot ^ ((r >> 1) & 7);
             // rows past the expert's segment load a valid row (results unused)
             const int srow = r < n ? (a.gather ? a.gather[r0 + r] : r0 + r) : (a.gather ? a.gather[r0] : r0);
-            srcp[j] = a.src + static_cast<size_t>(srow) * a.K + 8 * v;
-            dst[j] = 1024 * b;
+            srct[j] = a.src + static_cast<size_t>(srow) * a.K + 8 * v;
         } else {
             const int r = 8 * (b - kWM / 8) + (lane >> 3);
             const int v = slot ^ ((r >> 1) & 7);
-            const uint16_t* base = GATED && r >= kWN / 2 ? a.wb : a.wa;
             const int row = m0 + (GATED ? (r & (kWN / 2 - 1)) : r);
-            srcp[j] = base + (static_cast<size_t>(e) * a.M + row) * a.K + 8 * v;
-            dst[j] = kRegion + 1024 * (b - kWM / 8);
+            // packed: vector v of a 64-wide chunk is k-step v / 4 of the chunk,
+            // fragment (v % 4, row % 16) of that step's block (pack.hip)
+            woff[j - BT] = PACKED ? static_cast<uint32_t>(((row / 16) * (a.K / 32) + (v >> 2)) * 512 +
+                                                          8 * (16 * (v & 3) + (row & 15)))
+                                  : static_cast<uint32_t>(row * a.K + 8 * v);
         }
     }
+    const size_t emat = static_cast<size_t>(e) * a.M * a.K;
+    const uint16_t* wbase[BPW - BT];
+#pragma unroll
+    for (int j = 0; j < BPW - BT; ++j) wbase[j] = (GATED && j == 1 ? a.wb : a.wa) + emat;
+    static_assert(!GATED || BPW - BT == 2, "gated tiles: one W1 and one W3 block per wave");
+    // elements a lane's source moves per chunk: token rows and row-major
+    // weights by the chunk width, packed weights by two 512-element blocks
+    constexpr int wstep = PACKED ? 2 * 512 : kWK;
     // asm keeps the compiler from adding waits of its own for these loads;
     // the ring's waits and barriers order them.
     auto issue = [&](uint8_t* st, int c) __attribute__((always_inline)) {
-        const int kc = c * kWK;
 #pragma unroll
         for (int j = 0; j < BPW; ++j) {
-            const uint32_t lds = __builtin_amdgcn_readfirstlane(
-                static_cast<uint32_t>(reinterpret_cast<uintptr_t>(st + dst[j])));
+            const uint16_t* src = j < BT ? srct[j < BT ? j : 0] + static_cast<size_t>(c) * kWK
+                                         : wbase[j < BT ? 0 : j - BT] + woff[j < BT ? 0 : j - BT] +
+                                               static_cast<size_t>(c) * wstep;
+            const int b = wave + kWaves * j;
+            const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+                reinterpret_cast<uintptr_t>(st + (j < BT ? 1024 * b : kRegion + 1024 * (b - kWM / 8)))));
             asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-                         :: "v"(srcp[j] + kc), "s"(lds) : "memory", "m0");
+                         :: "v"(src), "s"(lds) : "memory", "m0");
         }
     };
 
@@ -184,7 +202,7 @@ __device__ __forceinline__ void wide_tile(const WideArgs& a, uint8_t* ring, int 
     }
 }
 
-template <bool GATED>
+template <bool GATED, bool PACKED>
 __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
     __shared__ __attribute__((aligned(1024))) uint8_t ring[2 * kStage];
     __shared__ int tstart[kMaxExperts + 1];
@@ -219,7 +237,7 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
             r0 = tile * kWM;
             n = min(kWM, a.nrows - r0);
         }
-        wide_tile<GATED>(a, ring, e, r0, n, xt * kOut);
+        wide_tile<GATED, PACKED>(a, ring, e, r0, n, xt * kOut);
     }
 }
 
@@ -231,7 +249,7 @@ bool wide_fits(bool gated, int M, int K) {
 
 hipError_t launch_wide(bool gated, const uint16_t* wa, const uint16_t* wb, const uint16_t* src,
                        const int32_t* gather, const int32_t* offsets, int groups, int nrows, int M, int K,
-                       void* out, int64_t rows_cap, hipStream_t s) {
+                       void* out, int64_t rows_cap, bool packed, hipStream_t s) {
     WideArgs a{wa, wb, src, gather, offsets, groups, nrows, M, K, out};
     // every group may end in a partial tile
     const int64_t tiles = offsets ? std::min<int64_t>(rows_cap, (rows_cap + kWM - 1) / kWM + groups)
@@ -241,8 +259,11 @@ hipError_t launch_wide(bool gated, const uint16_t* wa, const uint16_t* wb, const
     // 16 waves fill the SIMDs), a multiple of the XCD count
     int64_t blocks = std::min<int64_t>(work, 256);
     blocks = std::max<int64_t>(kXcd, (blocks + kXcd - 1) / kXcd * kXcd);
-    if (gated) wide_kernel<true><<<static_cast<int>(blocks), kThreads, 0, s>>>(a);
-    else wide_kernel<false><<<static_cast<int>(blocks), kThreads, 0, s>>>(a);
+    const int nb = static_cast<int>(blocks);
+    if (gated && packed) wide_kernel<true, true><<<nb, kThreads, 0, s>>>(a);
+    else if (gated) wide_kernel<true, false><<<nb, kThreads, 0, s>>>(a);
+    else if (packed) wide_kernel<false, true><<<nb, kThreads, 0, s>>>(a);
+    else wide_kernel<false, false><<<nb, kThreads, 0, s>>>(a);
     return hipGetLastError();
 }
 

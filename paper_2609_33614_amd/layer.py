@@ -205,3 +205,26 @@ def to_device(weights: Dict, device: str = "cuda") -> Dict[str, torch.Tensor]:
             t = t.view(torch.bfloat16)
         out[k] = t.to(device)
     return out
+
+
+# expert matrices and the (groups, M, K) view eat_pack_weights takes of each
+_PACK_SHAPES = {"w1": ("E", "F", "d"), "w3": ("E", "F", "d"), "w2": ("E", "d", "F"),
+                "ws1": (1, "Fs", "d"), "ws3": (1, "Fs", "d"), "ws2": (1, "d", "Fs")}
+
+
+def pack_weights(weights: Dict[str, torch.Tensor], stream=None) -> Dict[str, torch.Tensor]:
+    """Device weight dict -> the same dict with the bf16 expert matrices
+    (w1, w3, w2 and the shared ws1, ws3, ws2) in the packed layout (new
+    tensors, written by eat_pack_weights); for layers created with
+    weight_layout = EAT_LAYOUT_PACKED.  Other entries are passed through."""
+    out = dict(weights)
+    for name, w in weights.items():
+        if name not in _PACK_SHAPES or w is None:
+            continue
+        if w.dtype != torch.bfloat16 or w.dim() not in (2, 3):
+            raise ValueError(f"{name}: packing needs a bf16 [groups][M][K] or [M][K] tensor")
+        g, M, K = (1, *w.shape) if w.dim() == 2 else tuple(w.shape)
+        dst = torch.empty_like(w)
+        L.eat_pack_weights(w.contiguous(), g, M, K, dst, stream)
+        out[name] = dst
+    return out

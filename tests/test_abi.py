@@ -104,9 +104,12 @@ def _params(**kw):
     ("expert_dtype", 1, L.EAT_ERR_UNSUPPORTED),
     ("top_p_cap", 9, L.EAT_ERR_INVALID_ARG),
     ("expert_scale", (1 << 20) + 2, L.EAT_ERR_INVALID_ARG),     # misaligned scale vector
+    ("weight_layout", 2, L.EAT_ERR_INVALID_ARG),
+    ("weight_layout", L.EAT_LAYOUT_PACKED, L.EAT_ERR_UNSUPPORTED),  # packed needs bf16 experts
+    ("d_ffn", 32768 * 2, L.EAT_ERR_UNSUPPORTED),                   # d * F >= 2^31 with d = 32768 below
 ])
 def test_create_rejects_bad_params(field, value, status):
-    p = _params(**{field: value})
+    p = _params(**({field: value, "d_model": 32768} if field == "d_ffn" and value > 4096 else {field: value}))
     with pytest.raises(eat.EatError) as ei:
         eat.eat_create(p, 32)
     assert ei.value.status == status
@@ -321,3 +324,21 @@ def test_ppl_validation_happens_on_the_host():
     eat.eat_ppl_trend(**args)
     with pytest.raises(eat.EatError):
         eat.eat_ppl_reset(4, None, FAKE, FAKE, stream=0)
+
+
+def test_packed_layout_accepted_for_bf16_experts():
+    h = eat.eat_create(_params(act_dtype=eat.EAT_BF16, expert_dtype=eat.EAT_BF16, weight_layout=L.EAT_LAYOUT_PACKED),
+                       16)
+    eat.eat_destroy(h)
+
+
+def test_pack_validation_happens_on_the_host():
+    ok = dict(src=FAKE, groups=2, M=64, K=128, dst=FAKE + (1 << 24), stream=0)
+    cases = [dict(src=None), dict(dst=None), dict(groups=0), dict(M=40), dict(K=48), dict(M=0),
+             dict(src=FAKE + 8), dict(dst=FAKE + (1 << 24) + 2),
+             dict(dst=FAKE + 1024)]                                   # overlaps src
+    for kw in cases:
+        args = dict(ok); args.update(kw)
+        with pytest.raises(eat.EatError) as ei:
+            eat.eat_pack_weights(**args)
+        assert ei.value.status == L.EAT_ERR_INVALID_ARG, kw
