@@ -132,6 +132,11 @@ __device__ __forceinline__ bf16x8 ld16_stream(const uint16_t* p) {
 // 16*KS*(GATED ? 2 : 1) bytes per lane of weights in flight.
 // Token sub-tiles beyond the tile's row count are skipped (uniform branch),
 // so a tile of 1 token costs one MFMA per k-step and matrix.
+// Token rows two chunks ahead (see the main loop) in the gated projection
+// with up to 64-token tiles; measured: the plain projection gains nothing.
+template <bool GATED, int NSUB>
+constexpr bool stream_deep() { return GATED && NSUB <= 4; }
+
 // At least 3 waves per SIMD: the register budget then keeps the MFMA
 // accumulators in VGPRs (no AGPR copies) and the 64-token gated variant
 // holds 3 waves per SIMD instead of 2 (measured: more weight bytes in flight).
@@ -143,6 +148,7 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
     constexpr int LDS_ROW = KC + 8;                   // +16 B per row against bank conflicts
     constexpr int VPR = KC / 8;                       // 16-byte vectors per token row per chunk
     constexpr int RMAX = (BN * VPR + NT - 1) / NT;    // vectors per thread per chunk
+    constexpr bool DEEP = stream_deep<GATED, NSUB>();
     __shared__ __attribute__((aligned(16))) uint16_t xs[2][BN * LDS_ROW];
     __shared__ int tstart[kMaxExperts + 1];
     const int tid = threadIdx.x;
@@ -210,15 +216,17 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
         // (native vector type: HIP's uint4 struct would be copied with
         // memcpy and kept in private memory)
         bf16x8 xr[RMAX];
-        auto load_x = [&](int c) __attribute__((always_inline)) {
+        auto load_xr = [&](int c, bf16x8 (&R)[RMAX]) __attribute__((always_inline)) {
 #pragma unroll
-            for (int r = 0; r < RMAX; ++r) xr[r] = ld16(xsrc[r] + c * KC);
+            for (int r = 0; r < RMAX; ++r) R[r] = ld16(xsrc[r] + c * KC);
         };
-        auto store_x = [&](int buf) __attribute__((always_inline)) {
+        auto store_xr = [&](int buf, const bf16x8 (&R)[RMAX]) __attribute__((always_inline)) {
 #pragma unroll
             for (int r = 0; r < RMAX; ++r)
-                if (xon[r]) *reinterpret_cast<bf16x8*>(&xs[buf][xdst[r]]) = xr[r];
+                if (xon[r]) *reinterpret_cast<bf16x8*>(&xs[buf][xdst[r]]) = R[r];
         };
+        auto load_x = [&](int c) __attribute__((always_inline)) { load_xr(c, xr); };
+        auto store_x = [&](int buf) __attribute__((always_inline)) { store_xr(buf, xr); };
         auto load_w = [&](int c, bf16x8 (&A)[KS], bf16x8 (&B)[KS]) __attribute__((always_inline)) {
             const int k = kbeg + c * KC;
 #pragma unroll
@@ -256,6 +264,54 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
             }
         };
 
+        if constexpr (DEEP) {
+            // Token rows two chunks ahead: chunk c + 2's rows are loaded into
+            // one of two register sets while chunk c + 1's (loaded a chunk
+            // earlier) go to LDS, so no chunk waits on a token-row load it
+            // issued itself; weights one chunk ahead in two register sets.
+            // Every load is issued unconditionally (a conditional load leaves
+            // a merge the register allocator resolves with copies, and a copy
+            // waits for its load): past the last chunk the weight loads read
+            // a token row instead and the token loads read the last chunk
+            // again (valid, L2-resident, unused).
+            auto load_w_at = [&](int c, bf16x8 (&A)[KS], bf16x8 (&B)[KS]) __attribute__((always_inline)) {
+                const bool in = c < nch;
+                const int k = kbeg + (in ? c : 0) * KC;
+#pragma unroll
+                for (int j = 0; j < KS; ++j) {
+                    const size_t o = PACKED ? static_cast<size_t>(k / 32 + j) * 512 : static_cast<size_t>(k + 32 * j);
+                    const uint16_t* qa = in ? pa + o : xsrc[0];
+                    A[j] = PACKED ? ld16_stream(qa) : ld16(qa);
+                    if constexpr (GATED) {
+                        const uint16_t* qb = in ? pb + o : xsrc[0];
+                        B[j] = PACKED ? ld16_stream(qb) : ld16(qb);
+                    }
+                }
+            };
+            bf16x8 A0[KS], B0[KS], A1[KS], B1[KS], X0[RMAX], X1[RMAX];
+            load_xr(0, X0);
+            load_w_at(0, A0, B0);
+            load_xr(min(1, nch - 1), X1);
+            store_xr(0, X0);
+            lds_barrier();
+            // chunk c: weights in set c % 2, token rows in LDS buffer c % 2;
+            // issue token rows c + 2 into set c % 2 and weights c + 1 into set
+            // (c + 1) % 2, then move token set (c + 1) % 2 to LDS (c + 1) % 2
+            auto stage = [&](int c, const bf16x8 (&Ac)[KS], const bf16x8 (&Bc)[KS], bf16x8 (&An)[KS],
+                             bf16x8 (&Bn)[KS], bf16x8 (&Xn2)[RMAX], const bf16x8 (&Xn1)[RMAX],
+                             int cur) __attribute__((always_inline)) {
+                load_xr(min(c + 2, nch - 1), Xn2);
+                load_w_at(c + 1, An, Bn);
+                compute(cur, Ac, Bc);
+                if (c + 1 < nch) store_xr(cur ^ 1, Xn1);
+                lds_barrier();
+            };
+            for (int c = 0; c < nch; c += 2) {
+                stage(c, A0, B0, A1, B1, X0, X1, 0);
+                if (c + 1 >= nch) break;
+                stage(c + 1, A1, B1, A0, B0, X1, X0, 1);
+            }
+        } else {
         // Two register sets in ping-pong: while the MFMAs consume one chunk's
         // weights, the next chunk's are in flight in the other set (no
         // register copies, so the loads are not waited for early).
@@ -282,6 +338,7 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
             compute(1, A1, B1);
             if (has2) store_x(0);
             lds_barrier();
+        }
         }
 
         // result: lane holds weight rows m0 + 4g + q (q < 4) for token column s*16 + i
@@ -352,6 +409,9 @@ static int pick_ks(int ksplit) {
 // weight fragments in flight, so the bytes in flight per CU are about
 // waves/SIMD x 4 x KS x 1 KB (x2 when gated); the table maximises that
 // product for the register and LDS footprint of each variant, spill-free.
+// The gated 64-token variant keeps a second token-row register set (two
+// chunks ahead) and is faster with 2 k-steps at 4 waves per SIMD than with
+// 4 at 3 (measured on the Mixtral-shaped decode layer).
 #ifndef EAT_KS_G1
 #define EAT_KS_G1 4
 #endif
@@ -359,7 +419,7 @@ static int pick_ks(int ksplit) {
 #define EAT_KS_G2 4
 #endif
 #ifndef EAT_KS_G4
-#define EAT_KS_G4 4
+#define EAT_KS_G4 2
 #endif
 #ifndef EAT_KS_P1
 #define EAT_KS_P1 8

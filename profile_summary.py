@@ -3,9 +3,9 @@
 
 Inputs (directories written by the commands below, CSV output format):
   TRACE   rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run --
-              python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --modes eat
+              python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --modes eat
   FETCH   rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH -o run --
-              python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --modes eat --calibrate-copy 1024
+              python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --modes eat --calibrate-copy 1024
   WRITE   the same with --pmc WRITE_SIZE
 
 Writes profiles/<name>.md (kernel table, the dominant kernel's per-launch
@@ -76,8 +76,9 @@ def prefill_summary(args) -> int:
     rows = []
     shared = pf.get("d_shared", 0)
     per_fwd = 2 if shared else 1          # routed (+ always-on) launches per forward
-    for key, label, fl, ev_us in (("wide_kernel<true>", "up/gate (gated)", 4.0 * d * F * sk, r["up_gate"]["us"]),
-                                  ("wide_kernel<false>", "down (plain)", 2.0 * d * F * sk, r["down"]["us"])):
+    # the kernel name carries <gated, packed-weights>
+    for key, label, fl, ev_us in (("wide_kernel<true,", "up/gate (gated)", 4.0 * d * F * sk, r["up_gate"]["us"]),
+                                  ("wide_kernel<false,", "down (plain)", 2.0 * d * F * sk, r["down"]["us"])):
         durs = launches(key)
         routed = durs[0::per_fwd][-args.reps:]
         us = statistics.mean(routed)
@@ -154,12 +155,12 @@ def main(argv=None) -> int:
                 f"{bench['steps']} timed steps (+{bench['warmup']} warm-up), MI355X.\n\n")
         f.write("Commands (from the repository root):\n\n```\n")
         f.write("rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run -- "
-                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --modes eat\n")
+                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --modes eat\n")
         f.write("rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH -o run -- "
-                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --modes eat "
+                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --modes eat "
                 "--calibrate-copy 1024\n")
         f.write("rocprofv3 --pmc WRITE_SIZE --output-format csv -d WRITE -o run -- "
-                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --modes eat "
+                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --modes eat "
                 "--calibrate-copy 1024\n")
         f.write(f"python3 profile_summary.py --trace TRACE --fetch FETCH --write WRITE "
                 f"--bench-json TRACED_BENCH.json --name {args.name}\n```\n\n")
