@@ -41,46 +41,87 @@ struct CombineArgs {
 };
 
 // One workgroup per (token, 1024-element slice of d): 4 elements per
-// thread.  Each expert row's slice adds its split partials in slice order;
-// the slice's sum of squares goes to nrm2[row][slice] (added up, in slice
-// order, by the account kernel).
+// thread.  The token's experts are taken in increasing index order, up to
+// kBatch at a time: every row slice of a batch is loaded (its split partials
+// added in slice order) before any reduction, then the batch's sums of
+// squares are reduced together (per wave by butterfly, over the waves in
+// order, one barrier pair per batch) into nrm2[row][slice] (added up, in
+// slice order, by the account kernel).
+constexpr int kBatch = 8;
+constexpr int kMaxSplits = 8;                  // the down projection uses at most 8 slices
+
 template <typename YT>
 __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
-    __shared__ float red[kWaves];
+    __shared__ float red[kBatch][kWaves];
     const int t = blockIdx.x, chunk = blockIdx.y;
     const int lane = lane_id(), wave = threadIdx.x / kWave;
     const int j = chunk * kThreads + threadIdx.x;      // float4 index within the row
     const bool on = 4 * j < a.d;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    const uint64_t* mt = a.mask + static_cast<size_t>(t) * a.words;
 
-    for (int w = 0; w < a.words; ++w)
-    for (uint64_t rest = a.mask[static_cast<size_t>(t) * a.words + w]; rest; rest &= rest - 1) {
-        const int e = 64 * w + __builtin_ctzll(rest);
-        const int64_t row = a.inv[static_cast<size_t>(t) * a.E + e];
-        const float g = a.gate[static_cast<size_t>(t) * a.E + e];
-        float ss = 0.f;
-        if (on) {
-            const float* src = a.yp + row * a.d + 4 * j;
-            float4 o = *reinterpret_cast<const float4*>(src);
-            for (int sp = 1; sp < a.splits; ++sp) {
-                const float4 q = *reinterpret_cast<const float4*>(src + sp * a.split_stride);
-                o.x += q.x; o.y += q.y; o.z += q.z; o.w += q.w;
+    int w = 0;
+    uint64_t rest = mt[0];
+    for (;;) {
+        // next batch of selected experts (uniform across the workgroup)
+        int64_t rows[kBatch];
+        float gs[kBatch];
+        int nb = 0;
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            while (rest == 0 && w + 1 < a.words) rest = mt[++w];
+            rows[b] = 0;
+            gs[b] = 0.f;
+            if (rest != 0) {
+                const int e = 64 * w + __builtin_ctzll(rest);
+                rest &= rest - 1;
+                rows[b] = a.inv[static_cast<size_t>(t) * a.E + e];
+                gs[b] = a.gate[static_cast<size_t>(t) * a.E + e];
+                nb = b + 1;
             }
-            ss = fmaf(o.x, o.x, ss); ss = fmaf(o.y, o.y, ss);
-            ss = fmaf(o.z, o.z, ss); ss = fmaf(o.w, o.w, ss);
-            acc.x = fmaf(g, o.x, acc.x); acc.y = fmaf(g, o.y, acc.y);
-            acc.z = fmaf(g, o.z, acc.z); acc.w = fmaf(g, o.w, acc.w);
         }
-        ss = wave_sum(ss);
-        if (lane == 0) red[wave] = ss;
+        if (nb == 0) break;
+        float ss[kBatch];
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            ss[b] = 0.f;
+            if (b < nb && on) {
+                // all of the row slice's partials in flight at once, added in slice order
+                const float* src = a.yp + rows[b] * a.d + 4 * j;
+                float4 q[kMaxSplits];
+#pragma unroll
+                for (int sp = 0; sp < kMaxSplits; ++sp)
+                    if (sp < a.splits) q[sp] = *reinterpret_cast<const float4*>(src + sp * a.split_stride);
+                float4 o = q[0];
+#pragma unroll
+                for (int sp = 1; sp < kMaxSplits; ++sp)
+                    if (sp < a.splits) { o.x += q[sp].x; o.y += q[sp].y; o.z += q[sp].z; o.w += q[sp].w; }
+                ss[b] = fmaf(o.x, o.x, ss[b]); ss[b] = fmaf(o.y, o.y, ss[b]);
+                ss[b] = fmaf(o.z, o.z, ss[b]); ss[b] = fmaf(o.w, o.w, ss[b]);
+                const float g = gs[b];
+                acc.x = fmaf(g, o.x, acc.x); acc.y = fmaf(g, o.y, acc.y);
+                acc.z = fmaf(g, o.z, acc.z); acc.w = fmaf(g, o.w, acc.w);
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            if (b >= nb) break;
+            const float v = wave_sum(ss[b]);
+            if (lane == 0) red[b][wave] = v;
+        }
         __syncthreads();
         if (threadIdx.x == 0) {
-            float tot = 0.f;
 #pragma unroll
-            for (int w = 0; w < kWaves; ++w) tot += red[w];
-            a.nrm2[row * a.nchunk + chunk] = tot;
+            for (int b = 0; b < kBatch; ++b) {
+                if (b >= nb) break;
+                float tot = 0.f;
+#pragma unroll
+                for (int q = 0; q < kWaves; ++q) tot += red[b][q];
+                a.nrm2[rows[b] * a.nchunk + chunk] = tot;
+            }
         }
         __syncthreads();
+        if (nb < kBatch) break;
     }
     if (!on) return;
     if (a.ys) {
@@ -214,6 +255,7 @@ int combine_chunks(const eat_params_t& p) { return (p.d_model / 4 + kThreads - 1
 hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask, const float* gate,
                           const int32_t* inv, const float* yp, const float* ys, const uint16_t* residual,
                           void* y, float* nrm2, int splits, int64_t split_stride, hipStream_t s) {
+    if (splits < 1 || splits > kMaxSplits) return hipErrorInvalidValue;
     const int nchunk = combine_chunks(p);
     CombineArgs a{mask,   gate,   inv, yp,  ys,        residual, y,     nrm2, split_stride,
                   splits, T,      p.E, p.d_model, nchunk, mask_words(p.E)};

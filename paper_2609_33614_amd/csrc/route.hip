@@ -30,6 +30,7 @@ namespace eat {
 namespace {
 
 constexpr int kLogitWaves = 4;
+constexpr int kMaxRouteSlices = 16;     // d slices of the router scores
 
 struct RouteArgs {
     const void* x;
@@ -200,6 +201,20 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
 #pragma unroll
     for (int j = 0; j < J; ++j) valid[j] = 64 * j + lane < E;
 
+    // ---- this token's partial router scores: every slice's load issued
+    // before the history score below, summed (in slice order) after it ----
+    const int t = blockIdx.x * kSelWaves + wave;
+    const bool tok = t < a.T;
+    float zp[J][kMaxRouteSlices];
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        const float* src = a.part + static_cast<size_t>(tok ? t : 0) * E + 64 * j + lane;
+        const size_t stride = static_cast<size_t>(a.T) * E;
+#pragma unroll
+        for (int sl = 0; sl < kMaxRouteSlices; ++sl)
+            zp[j][sl] = (valid[j] && sl < a.slices) ? src[sl * stride] : 0.f;
+    }
+
     // ---- history score from the account snapshot (Eq. 1) --------------
     if (a.mode == EAT_MODE_EAT && wave == 0) {
         double n[J], pt[J], c[J];
@@ -227,28 +242,15 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
     __syncthreads();
 
     // ---- per-token softmax, selection, renormalisation ----------------
-    const int t = blockIdx.x * kSelWaves + wave;
-    if (t >= a.T) return;
+    if (!tok) return;
     float z[J];
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-        z[j] = -INFINITY;
-        if (valid[j]) {
-            // slices added in slice order; loads issued 8 at a time
-            const float* src = a.part + static_cast<size_t>(t) * E + 64 * j + lane;
-            const size_t stride = static_cast<size_t>(a.T) * E;
-            float sum = 0.f;
-            int sl = 0;
-            for (; sl + 8 <= a.slices; sl += 8) {
-                float v[8];
+        float sum = 0.f;
 #pragma unroll
-                for (int u = 0; u < 8; ++u) v[u] = src[(sl + u) * stride];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) sum += v[u];
-            }
-            for (; sl < a.slices; ++sl) sum += src[sl * stride];
-            z[j] = sum * a.inv_temp;
-        }
+        for (int sl = 0; sl < kMaxRouteSlices; ++sl)
+            if (sl < a.slices) sum += zp[j][sl];
+        z[j] = valid[j] ? sum * a.inv_temp : -INFINITY;
     }
     float zl = z[0];
 #pragma unroll
@@ -464,11 +466,15 @@ int route_token_tiles(int32_t T) { return T >= 1024 ? 4 : 1; }
 
 int route_slices(const eat_params_t& p, int32_t T) {
     // enough (token tile, d slice) workgroups to spread the router weights
-    // over the chip: about 512, each wave keeping at least one k-step
+    // over the chip: about 512, each wave keeping at least one k-step, and
+    // at most kMaxRouteSlices (the selection reads every slice of a score in
+    // one round of loads)
     const int tiles = (T + 16 * route_token_tiles(T) - 1) / (16 * route_token_tiles(T));
     const int nsteps = p.d_model / 16;
     int sl = 1;
-    while (2 * sl * tiles <= 512 && nsteps % (2 * sl) == 0 && nsteps / (2 * sl) >= kLogitWaves) sl *= 2;
+    while (2 * sl <= kMaxRouteSlices && 2 * sl * tiles <= 512 && nsteps % (2 * sl) == 0 &&
+           nsteps / (2 * sl) >= kLogitWaves)
+        sl *= 2;
     return sl;
 }
 
