@@ -536,6 +536,14 @@ static int pick_nsub(int64_t T) {
 #ifndef EAT_SPLIT_WAVES
 #define EAT_SPLIT_WAVES 4096
 #endif
+// Once the grid holds ~1024 wave tiles, a slice keeps at least
+// EAT_SPLIT_MIN_K reduction elements: shorter ones cost more in partial rows
+// than their extra waves gain (measured: 4 slices of a 1024-wide down
+// projection over 8 experts are slower than 2); smaller grids split down
+// to 128 (the same projection over 2 experts gains from 4 slices).
+#ifndef EAT_SPLIT_MIN_K
+#define EAT_SPLIT_MIN_K 384
+#endif
 // The gated projection pays for its slices with fp32 partials and a reduce
 // pass, so it only splits grids that would leave most of the chip idle.
 #ifndef EAT_UP_SPLIT_WAVES
@@ -554,7 +562,9 @@ static int stream_splits(int64_t rows_m, int kdim, const eat_params_t& p, int32_
     const int64_t tiles = std::max<int64_t>(active, (assign + bn - 1) / bn);
     const int64_t waves = (rows_m / 16) * tiles;
     int s = 1;
-    while (s < max_splits && kdim % (64 * s) == 0 && waves * s < threshold) s *= 2;
+    while (s < max_splits && kdim % (64 * 2 * s) == 0 && waves * s < threshold &&
+           kdim / (2 * s) >= (waves * s < 1024 ? 128 : EAT_SPLIT_MIN_K))
+        s *= 2;
     return s;
 }
 
