@@ -30,11 +30,29 @@ namespace {
 
 constexpr int kWM = 256;                  // token rows per tile
 constexpr int kWN = 256;                  // weight rows per tile
-constexpr int kWK = 64;                   // reduction chunk (bf16 elements): 128-byte rows
-constexpr int kWaves = 16;                // 4 token quarters x 4 weight quarters
+// Reduction chunk per stage: 64 (128-byte rows, a 2-stage ring) measured a
+// few percent faster than 32 (64-byte rows, a 4-stage ring loading three
+// chunks ahead) on the three prefill layers, so load latency is not what
+// bounds these tiles.
+#ifndef EAT_WIDE_BK
+#define EAT_WIDE_BK 64
+#endif
+constexpr int kWK = EAT_WIDE_BK;          // reduction chunk per stage (bf16 elements)
+constexpr int kRB = kWK * 2;              // bytes per LDS row
+constexpr int kVPR = kWK / 8;             // 16-byte vectors per row
+constexpr int kRPB = 1024 / kRB;          // rows per 1 KB DMA block
+// Token fragments per wave: 2 (16 waves, 64 x 64 per wave) and 4 (8 waves,
+// 128 x 64, a quarter fewer LDS operand reads per MFMA) measured the same,
+// so LDS bandwidth does not bound them either.
+#ifndef EAT_WIDE_TF
+#define EAT_WIDE_TF 2
+#endif
+constexpr int kTF = EAT_WIDE_TF;          // 32-row token fragments per wave
+constexpr int kWaves = 4 * kWM / (32 * kTF);   // token groups x 4 weight quarters
 constexpr int kThreads = kWaves * kWave;
-constexpr int kRegion = kWM * kWK * 2;    // bytes of one operand's rows per stage (32 KB)
-constexpr int kStage = 2 * kRegion;       // tokens then weights (64 KB)
+constexpr int kRegion = kWM * kRB;        // bytes of one operand's rows per stage
+constexpr int kStage = 2 * kRegion;       // tokens then weights
+constexpr int kStages = (128 * 1024) / kStage;   // ring depth in 128 KB of LDS
 constexpr int kXcd = 8;
 static_assert(kWN * kWK * 2 == kRegion, "token and weight regions have the same size");
 
@@ -48,62 +66,62 @@ struct WideArgs {
     void* out;                 // gated: bf16 H [rows][M]; plain: fp32 [rows][M]
 };
 
-// Byte offset of 16-byte vector v (0..7) of row r in a region of 128-byte
-// rows; the XOR spreads the rows that one LDS cycle serves for an MFMA
-// operand read (consecutive rows, same vector) over distinct banks.
+// Byte offset of 16-byte vector v of row r in a region of kRB-byte rows;
+// the XOR spreads the rows that one LDS cycle serves for an MFMA operand
+// read (consecutive rows, same vector) over distinct banks.
 __device__ __forceinline__ int wswz(int r, int v) {
-    return r * 128 + ((v ^ ((r >> 1) & 7)) << 4);
+    return r * kRB + ((v ^ ((r >> 1) & (kVPR - 1))) << 4);
 }
 
 template <bool GATED, bool PACKED>
 __device__ __forceinline__ void wide_tile(const WideArgs& a, uint8_t* ring, int e, int r0, int n, int m0) {
-    constexpr int NB = (kWM + kWN) / 8;       // 1 KB DMA blocks (8 rows each) per stage
+    constexpr int NB = (kWM + kWN) / kRPB;    // 1 KB DMA blocks per stage
     constexpr int BPW = NB / kWaves;          // per wave
     static_assert(NB % kWaves == 0, "blocks split evenly over the waves");
-    static_assert(kWM / 8 == kWaves * (BPW / 2), "a wave's first half of blocks are token rows");
+    static_assert(kWM / kRPB == kWaves * (BPW / 2), "a wave's first half of blocks are token rows");
+    static_assert((kWN / 2) % kRPB == 0, "a DMA block holds rows of one gated matrix");
     const int lane = lane_id(), wave = threadIdx.x / kWave;
     const int l32 = lane & 31, lh = lane >> 5;
-    const int wm = wave >> 2, wn = wave & 3;  // token quarter, weight quarter (SIMD = wave % 4)
+    const int wm = wave >> 2, wn = wave & 3;  // token group, weight quarter (SIMD = wave % 4)
 
     // Lane l of a DMA instruction writes LDS bytes [16 l, 16 l + 16) of its
-    // 1 KB block = row l / 8, slot l % 8; it fetches the global vector that
-    // belongs in that slot under the swizzle.  Blocks j < BPW / 2 hold token
-    // rows (a 64-bit source per lane: rows are gathered), the others weight
-    // rows of expert e: W1 for j = BPW / 2 and W3 for j = BPW / 2 + 1 in the
-    // gated tile, so their base is uniform and each lane keeps a 32-bit
+    // 1 KB block = row l / kVPR, slot l % kVPR; it fetches the global vector
+    // that belongs in that slot under the swizzle.  Blocks j < BPW / 2 hold
+    // token rows (a 64-bit source per lane: rows are gathered), the others
+    // weight rows of expert e -- one matrix per block (W1 or W3 in the gated
+    // tile), so the block's base is uniform and each lane keeps a 32-bit
     // element offset into the expert's matrix (M K < 2^31, checked on the host).
     constexpr int BT = BPW / 2;
     const uint16_t* srct[BT];
     uint32_t woff[BPW - BT];
+    const uint16_t* wbase[BPW - BT];
+    const size_t emat = static_cast<size_t>(e) * a.M * a.K;
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
         const int b = wave + kWaves * j;
-        const int slot = lane & 7;
+        const int slot = lane % kVPR;
         if (j < BT) {
-            const int r = 8 * b + (lane >> 3);
-            const int v = slot ^ ((r >> 1) & 7);
+            const int r = kRPB * b + lane / kVPR;
+            const int v = slot ^ ((r >> 1) & (kVPR - 1));
             // rows past the expert's segment load a valid row (results unused)
             const int srow = r < n ? (a.gather ? a.gather[r0 + r] : r0 + r) : (a.gather ? a.gather[r0] : r0);
             srct[j] = a.src + static_cast<size_t>(srow) * a.K + 8 * v;
         } else {
-            const int r = 8 * (b - kWM / 8) + (lane >> 3);
-            const int v = slot ^ ((r >> 1) & 7);
+            const int rb0 = kRPB * (b - kWM / kRPB);          // the block's first weight row
+            const int r = rb0 + lane / kVPR;
+            const int v = slot ^ ((r >> 1) & (kVPR - 1));
             const int row = m0 + (GATED ? (r & (kWN / 2 - 1)) : r);
-            // packed: vector v of a 64-wide chunk is k-step v / 4 of the chunk,
+            // packed: vector v of a chunk is k-step v / 4 of the chunk,
             // fragment (v % 4, row % 16) of that step's block (pack.hip)
             woff[j - BT] = PACKED ? static_cast<uint32_t>(((row / 16) * (a.K / 32) + (v >> 2)) * 512 +
                                                           8 * (16 * (v & 3) + (row & 15)))
                                   : static_cast<uint32_t>(row * a.K + 8 * v);
+            wbase[j - BT] = (GATED && rb0 >= kWN / 2 ? a.wb : a.wa) + emat;
         }
     }
-    const size_t emat = static_cast<size_t>(e) * a.M * a.K;
-    const uint16_t* wbase[BPW - BT];
-#pragma unroll
-    for (int j = 0; j < BPW - BT; ++j) wbase[j] = (GATED && j == 1 ? a.wb : a.wa) + emat;
-    static_assert(!GATED || BPW - BT == 2, "gated tiles: one W1 and one W3 block per wave");
     // elements a lane's source moves per chunk: token rows and row-major
-    // weights by the chunk width, packed weights by two 512-element blocks
-    constexpr int wstep = PACKED ? 2 * 512 : kWK;
+    // weights by the chunk width, packed weights by its 512-element blocks
+    constexpr int wstep = PACKED ? (kWK / 32) * 512 : kWK;
     // asm keeps the compiler from adding waits of its own for these loads;
     // the ring's waits and barriers order them.
     auto issue = [&](uint8_t* st, int c) __attribute__((always_inline)) {
@@ -114,64 +132,83 @@ __device__ __forceinline__ void wide_tile(const WideArgs& a, uint8_t* ring, int 
                                                static_cast<size_t>(c) * wstep;
             const int b = wave + kWaves * j;
             const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
-                reinterpret_cast<uintptr_t>(st + (j < BT ? 1024 * b : kRegion + 1024 * (b - kWM / 8)))));
+                reinterpret_cast<uintptr_t>(st + (j < BT ? 1024 * b : kRegion + 1024 * (b - kWM / kRPB)))));
             asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
                          :: "v"(src), "s"(lds) : "memory", "m0");
         }
     };
 
-    f32x16 acc[2][2];                         // [weight fragment][token fragment]
+    f32x16 acc[2][kTF];                       // [weight fragment][token fragment]
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-    // this wave's token quarter holds rows of the expert
-    const bool active = 64 * wm < n;
-    const int brow = 64 * wm;
+        for (int j = 0; j < kTF; ++j) acc[i][j] = f32x16{};
+    // this wave's token group holds rows of the expert (its fragments past
+    // the tile's rows are skipped)
+    const int brow = 32 * kTF * wm;
+    const int ntf = min(kTF, max(0, (n - brow + 31) / 32));
+    const bool active = ntf > 0;
     const int arow0 = GATED ? 32 * wn : 64 * wn;
     const int arow1 = GATED ? kWN / 2 + 32 * wn : 64 * wn + 32;
     auto compute = [&](const uint8_t* st) __attribute__((always_inline)) {
 #pragma unroll
         for (int ks = 0; ks < kWK / 16; ++ks) {
             const int v = 2 * ks + lh;
-            bf16x8 B[2], A[2];
-            B[0] = *reinterpret_cast<const bf16x8*>(st + wswz(brow + l32, v));
-            B[1] = *reinterpret_cast<const bf16x8*>(st + wswz(brow + 32 + l32, v));
+            bf16x8 B[kTF], A[2];
+#pragma unroll
+            for (int j = 0; j < kTF; ++j)
+                B[j] = *reinterpret_cast<const bf16x8*>(st + wswz(brow + 32 * j + l32, v));
             A[0] = *reinterpret_cast<const bf16x8*>(st + kRegion + wswz(arow0 + l32, v));
             A[1] = *reinterpret_cast<const bf16x8*>(st + kRegion + wswz(arow1 + l32, v));
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int j = 0; j < kTF; ++j) {
+                if (kTF > 2 && j >= ntf) break;
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int i = 0; i < 2; ++i)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[i], B[j], acc[i][j], 0, 0, 0);
+            }
         }
     };
-    const int nch = a.K / kWK;               // a multiple of 2 (K % 128 == 0)
-    uint8_t* st0 = ring;
-    uint8_t* st1 = ring + kStage;
-    // One ring step: wait for this wave's loads of chunk c, barrier (every
-    // wave's loads have landed and every wave is done with the other stage),
-    // refill the other stage with chunk c + 1, compute chunk c.
-    auto step = [&](int c, uint8_t* cur, uint8_t* nxt) __attribute__((always_inline)) {
-        wait_vm<0>();
+    const int nch = a.K / kWK;               // a multiple of kStages (K % 128 == 0)
+    static_assert(128 % (kWK * kStages) == 0 || (kWK * kStages) % 128 == 0, "ring covers whole 128-wide steps");
+    // Ring of kStages stages, chunk c in stage c % kStages, loads issued
+    // kStages - 1 chunks ahead.  One step: wait for this wave's loads of
+    // chunk c (the later chunks' loads may stay in flight), barrier (every
+    // wave's loads of chunk c have landed and every wave is done with chunk
+    // c - 1's stage), refill that stage with chunk c + kStages - 1, compute
+    // chunk c.
+    constexpr int P = kStages - 1;
+    auto stage_of = [&](int c) __attribute__((always_inline)) { return ring + (c % kStages) * kStage; };
+    auto step = [&](int c) __attribute__((always_inline)) {
+        const int after = min(P - 1, nch - 1 - c);          // chunks issued after c
+        if constexpr (P >= 3) {
+            if (after >= 2) wait_vm<2 * BPW>();
+            else if (after == 1) wait_vm<BPW>();
+            else wait_vm<0>();
+        } else if constexpr (P == 2) {
+            if (after >= 1) wait_vm<BPW>();
+            else wait_vm<0>();
+        } else {
+            wait_vm<0>();
+        }
         lds_barrier();
-        if (c + 1 < nch) issue(nxt, c + 1);
-        if (active) compute(cur);
+        if (c + P < nch) issue(stage_of(c + P), c + P);
+        if (active) compute(stage_of(c));
     };
+    static_assert(P <= 3, "wait counts cover up to three chunks in flight");
 
     // the previous tile's last reads must finish before the ring refills
     lds_barrier();
-    issue(st0, 0);
-    for (int c = 0; c < nch; c += 2) {
-        step(c, st0, st1);
-        step(c + 1, st1, st0);
-    }
+#pragma unroll
+    for (int c = 0; c < P; ++c)
+        if (c < nch) issue(stage_of(c), c);
+    for (int c = 0; c < nch; ++c) step(c);
     if (!active) return;
 
     // lane holds weight rows 8 (q / 4) + 4 lh + q % 4 of each 32-row
     // fragment, for token row brow + 32 j + l32
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < kTF; ++j) {
         const int t = brow + 32 * j + l32;
         if (t >= n) continue;
         const size_t orow = static_cast<size_t>(r0 + t) * a.M;
@@ -204,7 +241,7 @@ __device__ __forceinline__ void wide_tile(const WideArgs& a, uint8_t* ring, int 
 
 template <bool GATED, bool PACKED>
 __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
-    __shared__ __attribute__((aligned(1024))) uint8_t ring[2 * kStage];
+    __shared__ __attribute__((aligned(1024))) uint8_t ring[kStages * kStage];
     __shared__ int tstart[kMaxExperts + 1];
     const int tid = threadIdx.x;
 
@@ -244,7 +281,7 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
 }  // namespace
 
 bool wide_fits(bool gated, int M, int K) {
-    return M % (gated ? kWN / 2 : kWN) == 0 && K % (2 * kWK) == 0;
+    return M % (gated ? kWN / 2 : kWN) == 0 && K % 128 == 0;
 }
 
 hipError_t launch_wide(bool gated, const uint16_t* wa, const uint16_t* wb, const uint16_t* src,
