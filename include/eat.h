@@ -44,6 +44,10 @@
  *               (one word for E <= 64): bit i % 64 of word i / 64 set
  *               <=> expert i selected
  *      gates    [T][E] fp32, renormalised gate (0 for unselected experts)
+ *  - Non-finite inputs: a token whose row holds NaN or +-Inf gets NaN router
+ *    scores; EAT then selects no expert for it, Top-K the K lowest-index
+ *    experts, Top-P every expert up to top_p_cap; the other tokens of the
+ *    call are unaffected.
  *  - Thread safety: a handle is immutable after eat_create; calls that use
  *    different workspaces and account buffers may run concurrently.
  *    Calls sharing an account buffer must be ordered on one stream.
