@@ -10,6 +10,10 @@
 // read from HBM exactly once per token tile, which is what bounds decode.
 // The down projection may split its reduction dimension into slices;
 // the partial tiles are added, in split order, by the combine kernel.
+// The grid is persistent: a flat list of (token tile, slice, row block)
+// work items over about as many workgroups as the chip keeps resident.
+// Weights may be in the packed layout (pack.hip), read one contiguous
+// kilobyte per load instruction with the streaming cache policy.
 // Prefill-sized calls (hundreds of rows per expert) go to the wide MFMA
 // tiles of wide.hip instead.
 //
@@ -443,7 +447,9 @@ template <bool GATED, int NSUB>
 constexpr int stream_wpb() { return (!GATED && NSUB >= 4) ? 8 : 4; }
 
 // Workgroups of one stream-kernel instance the whole chip keeps resident
-// (occupancy per CU x CUs), asked once per instance.
+// (occupancy per CU x CUs), asked once per instance on the device current
+// at the first call (every device a process uses is assumed to be the same
+// part; a smaller grid on a larger part is still correct, only less full).
 template <bool GATED, int NSUB, int KS, int WPB, bool PACKED>
 int64_t stream_resident() {
     static const int64_t v = [] {
