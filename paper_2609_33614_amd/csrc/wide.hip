@@ -18,10 +18,10 @@
 // fewer rows of its expert, the waves of the empty quarters skip their
 // MFMAs and every SIMD's work shrinks with the tile.
 //
-// The grid is persistent: the work list (token tile x weight tile, token
-// tiles of one expert adjacent) is cut into 8 contiguous parts, one per XCD
-// (workgroups are dealt to XCDs round-robin), so the workgroups that share an
-// expert's weight tiles share one L2.
+// The grid is persistent: the work list (per expert, its weight tiles in
+// turn and each one's token tiles adjacent) is cut into 8 contiguous parts,
+// one per XCD (workgroups are dealt to XCDs round-robin), so the workgroups
+// that share an expert's weight tiles share one L2 and read them together.
 #include "eat_device.h"
 #include "eat_internal.h"
 
@@ -123,7 +123,10 @@ __device__ __forceinline__ void wide_tile(const WideArgs& a, uint8_t* ring, int 
     // weights by the chunk width, packed weights by its 512-element blocks
     constexpr int wstep = PACKED ? (kWK / 32) * 512 : kWK;
     // asm keeps the compiler from adding waits of its own for these loads;
-    // the ring's waits and barriers order them.
+    // the ring's waits and barriers order them.  Weight blocks load at device
+    // scope (sc1: no allocation in the CU's vector L1, which they would only
+    // churn -- a weight line is read once per workgroup); token rows keep the
+    // default policy.
     auto issue = [&](uint8_t* st, int c) __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < BPW; ++j) {
@@ -133,8 +136,12 @@ __device__ __forceinline__ void wide_tile(const WideArgs& a, uint8_t* ring, int 
             const int b = wave + kWaves * j;
             const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
                 reinterpret_cast<uintptr_t>(st + (j < BT ? 1024 * b : kRegion + 1024 * (b - kWM / kRPB)))));
-            asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-                         :: "v"(src), "s"(lds) : "memory", "m0");
+            if (j < BT)
+                asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                             :: "v"(src), "s"(lds) : "memory", "m0");
+            else
+                asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off sc1"
+                             :: "v"(src), "s"(lds) : "memory", "m0");
         }
     };
 
@@ -264,10 +271,18 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
     // the previous tile's ended
     int e = 0;
     for (int wid = wbeg + slot; wid < wend; wid += per_xcd) {
-        const int tile = wid / nx, xt = wid % nx;
+        int tile = wid / nx, xt = wid % nx;
         int r0, n;
         if (a.offsets) {
+            // an expert's items (the same range of wid as in tile-major
+            // order) go weight tile by weight tile, its token tiles adjacent:
+            // the workgroups that read one weight tile run in the same round,
+            // even where the expert straddles a round of the XCD's slots
             while (tstart[e + 1] <= tile) ++e;
+            const int nt = tstart[e + 1] - tstart[e];
+            const int local = wid - tstart[e] * nx;
+            xt = local / nt;
+            tile = tstart[e] + local % nt;
             r0 = a.offsets[e] + (tile - tstart[e]) * kWM;
             n = min(kWM, a.offsets[e + 1] - r0);
         } else {
