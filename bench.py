@@ -18,6 +18,8 @@ Prints one JSON line: EAT tokens/s (``value``), the Top-K (K=2) and Top-P
 the experts touched per step, the up/gate kernel's achieved HBM bandwidth
 against the MI355X peak (timed per launch with HIP events on the launch
 stream), a batch sweep, and the CPU oracle timed on a bounded sample.
+An ``eat_cs_share`` object repeats the EAT decode with the other reading of
+C_s's scale in S_h (its share C_s,i / sum C_s instead of the raw norm).
 A ``stack`` object times the 16-layer workload (16 fine-grained layers,
 RMSNorm and a residual mixing matrix between them, decode batch 64) per
 routing mode, with every layer's mean activated experts, and EAT with
@@ -125,19 +127,22 @@ def union_sizes(masks: np.ndarray, words: int = 1) -> np.ndarray:
     return c.sum(axis=-1) if words > 1 else c
 
 
-def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bool, graph: bool = False):
+def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bool, graph: bool = False,
+             cs_mode: int = 0):
     """`steps` timed decode steps after `warmup` untimed ones on scratch
     accounts.  profile: eager launches with HIP events around the expert
     kernels of every step.  graph: one step captured in a HIP graph and
     replayed per step (the step's input copied into the captured buffer and
-    its masks copied out, both inside the timed region)."""
+    its masks copied out, both inside the timed region).  cs_mode: how C_s
+    enters S_h (0 raw norm, 1 share of the total)."""
     import torch
 
     from paper_2609_33614_amd import _lib as L
     from paper_2609_33614_amd.layer import EatLayer, capture
 
     p = L.eat_params_default(mode=mode, E=shape.E, d_model=shape.d, d_ffn=shape.F, top_k=shape.K,
-                             top_p=0.6, inv_temperature=shape.inv_temp, weight_layout=layout_code())
+                             top_p=0.6, inv_temperature=shape.inv_temp, weight_layout=layout_code(),
+                             cs_mode=cs_mode)
     lay = EatLayer(p, B, wdev)
     E = shape.E
     W = L.mask_words(E)
@@ -457,6 +462,8 @@ def main(argv=None) -> int:
                     help="expert-weight layout of every timed layer (default: packed)")
     ap.add_argument("--no-wide-experts", action="store_true",
                     help="skip the decode of the 128-expert (Qwen3-30B-A3B-shaped) layer")
+    ap.add_argument("--no-share", action="store_true",
+                    help="skip the EAT decode under the C_s-share reading (cs_mode 1)")
     ap.add_argument("--stack-steps", type=int, default=1024)
     ap.add_argument("--only-stack", action="store_true", help="time only the 16-layer stack and print its JSON")
     ap.add_argument("--only-prefill", default="", metavar="LAYER",
@@ -525,6 +532,10 @@ def main(argv=None) -> int:
         if args.graph:
             log(f"timing {name}: {K} steps (+{W} warm-up), HIP graph replay")
             graphed[name] = run_mode(L.MODES[name], shape, wdev, xs, B, K, W, ev, profile=False, graph=True)
+    share = None
+    if not args.no_share:
+        log(f"timing eat with the C_s-share reading: {K} steps (+{W} warm-up)")
+        share = run_mode(L.MODES["eat"], shape, wdev, xs, B, K, W, ev, profile=True, cs_mode=1)
     r = results["eat"]
     head = graphed.get("eat", r)
     ms_step = head["total_ms"] / K
@@ -616,6 +627,8 @@ def main(argv=None) -> int:
                      "us_per_launch": round(float(r["up_ms"].mean() * 1e3), 2)},
         "cpu_baseline": cpu,
         "modes": {name: summary(res, graphed.get(name)) for name, res in results.items()},
+        "eat_cs_share": dict(summary(share, None), reading="C_s enters S_h as C_s,i / sum C_s (cs_mode 1)")
+        if share is not None else None,
         "sweep": sweep,
         "prefill": prefill,
         "stack": stack,
