@@ -73,176 +73,116 @@ __device__ __forceinline__ int wswz(int r, int v) {
     return r * kRB + ((v ^ ((r >> 1) & (kVPR - 1))) << 4);
 }
 
-template <bool GATED, bool PACKED>
-__device__ __forceinline__ void wide_tile(const WideArgs& a, uint8_t* ring, int e, int r0, int n, int m0) {
-    constexpr int NB = (kWM + kWN) / kRPB;    // 1 KB DMA blocks per stage
-    constexpr int BPW = NB / kWaves;          // per wave
-    static_assert(NB % kWaves == 0, "blocks split evenly over the waves");
-    static_assert(kWM / kRPB == kWaves * (BPW / 2), "a wave's first half of blocks are token rows");
-    static_assert((kWN / 2) % kRPB == 0, "a DMA block holds rows of one gated matrix");
-    const int lane = lane_id(), wave = threadIdx.x / kWave;
-    const int l32 = lane & 31, lh = lane >> 5;
-    const int wm = wave >> 2, wn = wave & 3;  // token group, weight quarter (SIMD = wave % 4)
+constexpr int kNB = (kWM + kWN) / kRPB;       // 1 KB DMA blocks per stage
+constexpr int kBPW = kNB / kWaves;            // per wave
+constexpr int kBT = kBPW / 2;                 // a wave's token blocks (the rest are weights)
+constexpr int kP = kStages - 1;               // chunks in flight ahead of the one computed
+static_assert(kNB % kWaves == 0, "blocks split evenly over the waves");
+static_assert(kWM / kRPB == kWaves * kBT, "a wave's first half of blocks are token rows");
+static_assert((kWN / 2) % kRPB == 0, "a DMA block holds rows of one gated matrix");
+static_assert(kP <= 3, "wait counts cover up to three chunks in flight");
 
-    // Lane l of a DMA instruction writes LDS bytes [16 l, 16 l + 16) of its
-    // 1 KB block = row l / kVPR, slot l % kVPR; it fetches the global vector
-    // that belongs in that slot under the swizzle.  Blocks j < BPW / 2 hold
-    // token rows (a 64-bit source per lane: rows are gathered), the others
-    // weight rows of expert e -- one matrix per block (W1 or W3 in the gated
-    // tile), so the block's base is uniform and each lane keeps a 32-bit
-    // element offset into the expert's matrix (M K < 2^31, checked on the host).
-    constexpr int BT = BPW / 2;
-    const uint16_t* srct[BT];
-    uint32_t woff[BPW - BT];
-    const uint16_t* wbase[BPW - BT];
-    const size_t emat = static_cast<size_t>(e) * a.M * a.K;
+// One work item: token rows [r0, r0 + n) of expert e's segment against the
+// expert's weight rows from m0 (W1 and W3 rows m0.. in the gated tile).
+struct Item {
+    int e, r0, n, m0;
+};
+
+// Lane l of a DMA instruction writes LDS bytes [16 l, 16 l + 16) of its 1 KB
+// block = row l / kVPR, slot l % kVPR; it fetches the global vector that
+// belongs in that slot under the swizzle.  Blocks j < kBT hold token rows (a
+// 64-bit source per lane: rows are gathered), the others weight rows of
+// expert e -- one matrix per block (W1 or W3 in the gated tile), so the
+// block's base is uniform and each lane keeps a 32-bit element offset into
+// the expert's matrix (M K < 2^31, checked on the host).
+struct ItemLoads {
+    const uint16_t* srct[kBT];
+    uint32_t woff[kBPW - kBT];
+    const uint16_t* wbase[kBPW - kBT];
+};
+
+// The source row of each of this lane's token blocks (rows past the expert's
+// segment load a valid row; their results are unused).  Issued an item
+// ahead, so the index loads complete under the previous item's chunks.
+__device__ __forceinline__ void token_rows(const WideArgs& a, const Item& it, int (&srow)[kBT]) {
+    const int lane = lane_id(), wave = threadIdx.x / kWave;
 #pragma unroll
-    for (int j = 0; j < BPW; ++j) {
+    for (int j = 0; j < kBT; ++j) {
+        const int r = kRPB * (wave + kWaves * j) + lane / kVPR;
+        const int g = r < it.n ? it.r0 + r : it.r0;
+        srow[j] = a.gather ? a.gather[g] : g;
+    }
+}
+
+template <bool GATED, bool PACKED>
+__device__ __forceinline__ ItemLoads item_loads(const WideArgs& a, const Item& it, const int (&srow)[kBT]) {
+    const int lane = lane_id(), wave = threadIdx.x / kWave;
+    const int slot = lane % kVPR;
+    ItemLoads L;
+    const size_t emat = static_cast<size_t>(it.e) * a.M * a.K;
+#pragma unroll
+    for (int j = 0; j < kBPW; ++j) {
         const int b = wave + kWaves * j;
-        const int slot = lane % kVPR;
-        if (j < BT) {
+        if (j < kBT) {
             const int r = kRPB * b + lane / kVPR;
             const int v = slot ^ ((r >> 1) & (kVPR - 1));
-            // rows past the expert's segment load a valid row (results unused)
-            const int srow = r < n ? (a.gather ? a.gather[r0 + r] : r0 + r) : (a.gather ? a.gather[r0] : r0);
-            srct[j] = a.src + static_cast<size_t>(srow) * a.K + 8 * v;
+            L.srct[j] = a.src + static_cast<size_t>(srow[j]) * a.K + 8 * v;
         } else {
             const int rb0 = kRPB * (b - kWM / kRPB);          // the block's first weight row
             const int r = rb0 + lane / kVPR;
             const int v = slot ^ ((r >> 1) & (kVPR - 1));
-            const int row = m0 + (GATED ? (r & (kWN / 2 - 1)) : r);
+            const int row = it.m0 + (GATED ? (r & (kWN / 2 - 1)) : r);
             // packed: vector v of a chunk is k-step v / 4 of the chunk,
             // fragment (v % 4, row % 16) of that step's block (pack.hip)
-            woff[j - BT] = PACKED ? static_cast<uint32_t>(((row / 16) * (a.K / 32) + (v >> 2)) * 512 +
-                                                          8 * (16 * (v & 3) + (row & 15)))
-                                  : static_cast<uint32_t>(row * a.K + 8 * v);
-            wbase[j - BT] = (GATED && rb0 >= kWN / 2 ? a.wb : a.wa) + emat;
+            L.woff[j - kBT] = PACKED ? static_cast<uint32_t>(((row / 16) * (a.K / 32) + (v >> 2)) * 512 +
+                                                             8 * (16 * (v & 3) + (row & 15)))
+                                     : static_cast<uint32_t>(row * a.K + 8 * v);
+            L.wbase[j - kBT] = (GATED && rb0 >= kWN / 2 ? a.wb : a.wa) + emat;
         }
     }
+    return L;
+}
+
+// Chunk c of an item into LDS stage st.  asm keeps the compiler from adding
+// waits of its own for these loads; the ring's waits and barriers order
+// them.  Weight blocks load at device scope (sc1: no allocation in the CU's
+// vector L1, which they would only churn -- a weight line is read once per
+// workgroup); token rows keep the default policy.
+template <bool PACKED>
+__device__ __forceinline__ void issue_chunk(const ItemLoads& L, uint8_t* st, int c) {
     // elements a lane's source moves per chunk: token rows and row-major
     // weights by the chunk width, packed weights by its 512-element blocks
     constexpr int wstep = PACKED ? (kWK / 32) * 512 : kWK;
-    // asm keeps the compiler from adding waits of its own for these loads;
-    // the ring's waits and barriers order them.  Weight blocks load at device
-    // scope (sc1: no allocation in the CU's vector L1, which they would only
-    // churn -- a weight line is read once per workgroup); token rows keep the
-    // default policy.
-    auto issue = [&](uint8_t* st, int c) __attribute__((always_inline)) {
+    const int wave = threadIdx.x / kWave;
 #pragma unroll
-        for (int j = 0; j < BPW; ++j) {
-            const uint16_t* src = j < BT ? srct[j < BT ? j : 0] + static_cast<size_t>(c) * kWK
-                                         : wbase[j < BT ? 0 : j - BT] + woff[j < BT ? 0 : j - BT] +
-                                               static_cast<size_t>(c) * wstep;
-            const int b = wave + kWaves * j;
-            const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
-                reinterpret_cast<uintptr_t>(st + (j < BT ? 1024 * b : kRegion + 1024 * (b - kWM / kRPB)))));
-            if (j < BT)
-                asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-                             :: "v"(src), "s"(lds) : "memory", "m0");
-            else
-                asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off sc1"
-                             :: "v"(src), "s"(lds) : "memory", "m0");
-        }
-    };
+    for (int j = 0; j < kBPW; ++j) {
+        const uint16_t* src = j < kBT ? L.srct[j < kBT ? j : 0] + static_cast<size_t>(c) * kWK
+                                      : L.wbase[j < kBT ? 0 : j - kBT] + L.woff[j < kBT ? 0 : j - kBT] +
+                                            static_cast<size_t>(c) * wstep;
+        const int b = wave + kWaves * j;
+        const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+            reinterpret_cast<uintptr_t>(st + (j < kBT ? 1024 * b : kRegion + 1024 * (b - kWM / kRPB)))));
+        if (j < kBT)
+            asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                         :: "v"(src), "s"(lds) : "memory", "m0");
+        else
+            asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off sc1"
+                         :: "v"(src), "s"(lds) : "memory", "m0");
+    }
+}
 
-    f32x16 acc[2][kTF];                       // [weight fragment][token fragment]
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < kTF; ++j) acc[i][j] = f32x16{};
-    // this wave's token group holds rows of the expert (its fragments past
-    // the tile's rows are skipped)
-    const int brow = 32 * kTF * wm;
-    const int ntf = min(kTF, max(0, (n - brow + 31) / 32));
-    const bool active = ntf > 0;
-    const int arow0 = GATED ? 32 * wn : 64 * wn;
-    const int arow1 = GATED ? kWN / 2 + 32 * wn : 64 * wn + 32;
-    auto compute = [&](const uint8_t* st) __attribute__((always_inline)) {
-#pragma unroll
-        for (int ks = 0; ks < kWK / 16; ++ks) {
-            const int v = 2 * ks + lh;
-            bf16x8 B[kTF], A[2];
-#pragma unroll
-            for (int j = 0; j < kTF; ++j)
-                B[j] = *reinterpret_cast<const bf16x8*>(st + wswz(brow + 32 * j + l32, v));
-            A[0] = *reinterpret_cast<const bf16x8*>(st + kRegion + wswz(arow0 + l32, v));
-            A[1] = *reinterpret_cast<const bf16x8*>(st + kRegion + wswz(arow1 + l32, v));
-#pragma unroll
-            for (int j = 0; j < kTF; ++j) {
-                if (kTF > 2 && j >= ntf) break;
-#pragma unroll
-                for (int i = 0; i < 2; ++i)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[i], B[j], acc[i][j], 0, 0, 0);
-            }
-        }
-    };
-    const int nch = a.K / kWK;               // a multiple of kStages (K % 128 == 0)
-    static_assert(128 % (kWK * kStages) == 0 || (kWK * kStages) % 128 == 0, "ring covers whole 128-wide steps");
-    // Ring of kStages stages, chunk c in stage c % kStages, loads issued
-    // kStages - 1 chunks ahead.  One step: wait for this wave's loads of
-    // chunk c (the later chunks' loads may stay in flight), barrier (every
-    // wave's loads of chunk c have landed and every wave is done with chunk
-    // c - 1's stage), refill that stage with chunk c + kStages - 1, compute
-    // chunk c.
-    constexpr int P = kStages - 1;
-    auto stage_of = [&](int c) __attribute__((always_inline)) { return ring + (c % kStages) * kStage; };
-    auto step = [&](int c) __attribute__((always_inline)) {
-        const int after = min(P - 1, nch - 1 - c);          // chunks issued after c
-        if constexpr (P >= 3) {
-            if (after >= 2) wait_vm<2 * BPW>();
-            else if (after == 1) wait_vm<BPW>();
-            else wait_vm<0>();
-        } else if constexpr (P == 2) {
-            if (after >= 1) wait_vm<BPW>();
-            else wait_vm<0>();
-        } else {
-            wait_vm<0>();
-        }
-        lds_barrier();
-        if (c + P < nch) issue(stage_of(c + P), c + P);
-        if (active) compute(stage_of(c));
-    };
-    static_assert(P <= 3, "wait counts cover up to three chunks in flight");
-
-    // the previous tile's last reads must finish before the ring refills
-    lds_barrier();
-#pragma unroll
-    for (int c = 0; c < P; ++c)
-        if (c < nch) issue(stage_of(c), c);
-    for (int c = 0; c < nch; ++c) step(c);
-    if (!active) return;
-
-    // lane holds weight rows 8 (q / 4) + 4 lh + q % 4 of each 32-row
-    // fragment, for token row brow + 32 j + l32
-#pragma unroll
-    for (int j = 0; j < kTF; ++j) {
-        const int t = brow + 32 * j + l32;
-        if (t >= n) continue;
-        const size_t orow = static_cast<size_t>(r0 + t) * a.M;
-        if constexpr (GATED) {
-#pragma unroll
-            for (int qb = 0; qb < 4; ++qb) {
-                const int f = m0 + 32 * wn + 8 * qb + 4 * lh;
-                uint16_t hv[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    hv[q] = f32_to_bf16(silu(acc[0][j][4 * qb + q]) * acc[1][j][4 * qb + q]);
-                uint2 pk;
-                pk.x = static_cast<uint32_t>(hv[0]) | (static_cast<uint32_t>(hv[1]) << 16);
-                pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
-                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + orow + f) = pk;
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int qb = 0; qb < 4; ++qb) {
-                    const int f = m0 + 64 * wn + 32 * i + 8 * qb + 4 * lh;
-                    *reinterpret_cast<float4*>(static_cast<float*>(a.out) + orow + f) =
-                        make_float4(acc[i][j][4 * qb + 0], acc[i][j][4 * qb + 1],
-                                    acc[i][j][4 * qb + 2], acc[i][j][4 * qb + 3]);
-                }
-        }
+// Waits until at most `after` chunks' loads of this wave are still in flight
+// (loads complete in issue order).
+__device__ __forceinline__ void wait_chunks(int after) {
+    if constexpr (kP >= 3) {
+        if (after >= 2) wait_vm<2 * kBPW>();
+        else if (after == 1) wait_vm<kBPW>();
+        else wait_vm<0>();
+    } else if constexpr (kP == 2) {
+        if (after >= 1) wait_vm<kBPW>();
+        else wait_vm<0>();
+    } else {
+        wait_vm<0>();
     }
 }
 
@@ -250,11 +190,12 @@ template <bool GATED, bool PACKED>
 __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
     __shared__ __attribute__((aligned(1024))) uint8_t ring[kStages * kStage];
     __shared__ int tstart[kMaxExperts + 1];
-    const int tid = threadIdx.x;
+    __shared__ int soff[kMaxExperts + 1];     // the segment offsets, read per item without a memory wait
 
     int ntiles;
     if (a.offsets) {
-        tile_starts(a.offsets, a.groups, kWM, tstart);
+        for (int g = threadIdx.x; g <= a.groups; g += kThreads) soff[g] = a.offsets[g];
+        tile_starts(a.offsets, a.groups, kWM, tstart);   // ends with a barrier
         ntiles = tstart[a.groups];
     } else {
         ntiles = (a.nrows + kWM - 1) / kWM;
@@ -267,29 +208,159 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
     const int part = (work + kXcd - 1) / kXcd;
     const int wbeg = xcd * part, wend = min(work, wbeg + part);
 
-    // a workgroup's tiles only increase, so its segment search resumes where
-    // the previous tile's ended
-    int e = 0;
-    for (int wid = wbeg + slot; wid < wend; wid += per_xcd) {
+    // a workgroup's items only increase, so its segment search resumes where
+    // the previous item's ended
+    int es = 0;
+    auto item_at = [&](int wid) __attribute__((always_inline)) {
+        Item it;
         int tile = wid / nx, xt = wid % nx;
-        int r0, n;
         if (a.offsets) {
             // an expert's items (the same range of wid as in tile-major
             // order) go weight tile by weight tile, its token tiles adjacent:
             // the workgroups that read one weight tile run in the same round,
             // even where the expert straddles a round of the XCD's slots
-            while (tstart[e + 1] <= tile) ++e;
-            const int nt = tstart[e + 1] - tstart[e];
-            const int local = wid - tstart[e] * nx;
+            while (tstart[es + 1] <= tile) ++es;
+            const int nt = tstart[es + 1] - tstart[es];
+            const int local = wid - tstart[es] * nx;
             xt = local / nt;
-            tile = tstart[e] + local % nt;
-            r0 = a.offsets[e] + (tile - tstart[e]) * kWM;
-            n = min(kWM, a.offsets[e + 1] - r0);
+            tile = tstart[es] + local % nt;
+            it.e = es;
+            it.r0 = soff[es] + (tile - tstart[es]) * kWM;
+            it.n = min(kWM, soff[es + 1] - it.r0);
         } else {
-            r0 = tile * kWM;
-            n = min(kWM, a.nrows - r0);
+            it.e = 0;
+            it.r0 = tile * kWM;
+            it.n = min(kWM, a.nrows - it.r0);
         }
-        wide_tile<GATED, PACKED>(a, ring, e, r0, n, xt * kOut);
+        it.m0 = xt * kOut;
+        // uniform: keep the item in scalar registers
+        it.e = __builtin_amdgcn_readfirstlane(it.e);
+        it.r0 = __builtin_amdgcn_readfirstlane(it.r0);
+        it.n = __builtin_amdgcn_readfirstlane(it.n);
+        it.m0 = __builtin_amdgcn_readfirstlane(it.m0);
+        return it;
+    };
+
+    int wid = wbeg + slot;
+    if (wid >= wend) return;                  // uniform over the workgroup
+
+    const int lane = lane_id(), wave = threadIdx.x / kWave;
+    const int l32 = lane & 31, lh = lane >> 5;
+    const int wm = wave >> 2, wn = wave & 3;  // token group, weight quarter (SIMD = wave % 4)
+    const int brow = 32 * kTF * wm;           // this wave's first token row of the tile
+    const int arow0 = GATED ? 32 * wn : 64 * wn;
+    const int arow1 = GATED ? kWN / 2 + 32 * wn : 64 * wn + 32;
+    const int nch = a.K / kWK;                // a multiple of kStages (K % 128 == 0)
+    static_assert(128 % (kWK * kStages) == 0 || (kWK * kStages) % 128 == 0, "ring covers whole 128-wide steps");
+    auto stage_of = [&](int c) __attribute__((always_inline)) { return ring + (c % kStages) * kStage; };
+
+    // Ring of kStages stages, chunk c in stage c % kStages, loads issued kP
+    // chunks ahead.  One step: wait for this wave's loads of chunk c (later
+    // chunks' loads may stay in flight), barrier (every wave's loads of chunk
+    // c have landed and every wave is done with chunk c - 1's stage), refill
+    // that stage with chunk c + kP, compute chunk c.  The ring runs on across
+    // items: an item's last steps issue the next item's first chunks (nch is a
+    // multiple of kStages, so chunk c of every item sits in stage c % kStages),
+    // and the next item's source rows are loaded an item ahead, so neither the
+    // index loads nor the refill wait behind the item's output stores.
+    Item cur = item_at(wid);
+    int srow[kBT];
+    token_rows(a, cur, srow);
+    ItemLoads ld = item_loads<GATED, PACKED>(a, cur, srow);
+#pragma unroll
+    for (int c = 0; c < kP; ++c)
+        if (c < nch) issue_chunk<PACKED>(ld, stage_of(c), c);
+
+    for (;;) {
+        const int nwid = wid + per_xcd;
+        const bool more = nwid < wend;        // uniform
+        Item nxt = cur;
+        if (more) {
+            nxt = item_at(nwid);
+            token_rows(a, nxt, srow);
+        }
+        // this wave's token group holds rows of the expert (its fragments
+        // past the tile's rows are skipped)
+        const int ntf = min(kTF, max(0, (cur.n - brow + 31) / 32));
+        const bool active = ntf > 0;
+        f32x16 acc[2][kTF];                   // [weight fragment][token fragment]
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < kTF; ++j) acc[i][j] = f32x16{};
+
+        // one step of the ring; L/ci: the loads to issue after the barrier
+        // (ci < 0: none)
+        auto step = [&](int c, const ItemLoads& L, int ci) __attribute__((always_inline)) {
+            // chunks issued after c: the item's own, then the next item's
+            // (the previous item's output stores may sit between them; a
+            // wait that does not count them only waits longer)
+            wait_chunks(more ? kP - 1 : min(kP - 1, nch - 1 - c));
+            lds_barrier();
+            if (ci >= 0) issue_chunk<PACKED>(L, stage_of(ci), ci);
+            if (!active) return;
+            const uint8_t* st = stage_of(c);
+#pragma unroll
+            for (int ks = 0; ks < kWK / 16; ++ks) {
+                const int v = 2 * ks + lh;
+                bf16x8 B[kTF], A[2];
+#pragma unroll
+                for (int j = 0; j < kTF; ++j)
+                    B[j] = *reinterpret_cast<const bf16x8*>(st + wswz(brow + 32 * j + l32, v));
+                A[0] = *reinterpret_cast<const bf16x8*>(st + kRegion + wswz(arow0 + l32, v));
+                A[1] = *reinterpret_cast<const bf16x8*>(st + kRegion + wswz(arow1 + l32, v));
+#pragma unroll
+                for (int j = 0; j < kTF; ++j) {
+                    if (kTF > 2 && j >= ntf) break;
+#pragma unroll
+                    for (int i = 0; i < 2; ++i)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[i], B[j], acc[i][j], 0, 0, 0);
+                }
+            }
+        };
+        // steps that refill from this item, then (its loads all issued) the
+        // last kP steps, which start the next item
+        for (int c = 0; c + kP < nch; ++c) step(c, ld, c + kP);
+        if (more) ld = item_loads<GATED, PACKED>(a, nxt, srow);
+        for (int c = max(0, nch - kP); c < nch; ++c) step(c, ld, more ? c + kP - nch : -1);
+
+        if (active) {
+            // lane holds weight rows 8 (q / 4) + 4 lh + q % 4 of each 32-row
+            // fragment, for token row brow + 32 j + l32
+#pragma unroll
+            for (int j = 0; j < kTF; ++j) {
+                const int t = brow + 32 * j + l32;
+                if (t >= cur.n) continue;
+                const size_t orow = static_cast<size_t>(cur.r0 + t) * a.M;
+                if constexpr (GATED) {
+#pragma unroll
+                    for (int qb = 0; qb < 4; ++qb) {
+                        const int f = cur.m0 + 32 * wn + 8 * qb + 4 * lh;
+                        uint16_t hv[4];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            hv[q] = f32_to_bf16(silu(acc[0][j][4 * qb + q]) * acc[1][j][4 * qb + q]);
+                        uint2 pk;
+                        pk.x = static_cast<uint32_t>(hv[0]) | (static_cast<uint32_t>(hv[1]) << 16);
+                        pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
+                        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + orow + f) = pk;
+                    }
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 2; ++i)
+#pragma unroll
+                        for (int qb = 0; qb < 4; ++qb) {
+                            const int f = cur.m0 + 64 * wn + 32 * i + 8 * qb + 4 * lh;
+                            *reinterpret_cast<float4*>(static_cast<float*>(a.out) + orow + f) =
+                                make_float4(acc[i][j][4 * qb + 0], acc[i][j][4 * qb + 1],
+                                            acc[i][j][4 * qb + 2], acc[i][j][4 * qb + 3]);
+                        }
+                }
+            }
+        }
+        if (!more) break;
+        cur = nxt;
+        wid = nwid;
     }
 }
 
