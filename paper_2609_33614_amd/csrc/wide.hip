@@ -22,6 +22,10 @@
 // turn and each one's token tiles adjacent) is cut into 8 contiguous parts,
 // one per XCD (workgroups are dealt to XCDs round-robin), so the workgroups
 // that share an expert's weight tiles share one L2 and read them together.
+// A workgroup's ring runs on from one item to the next, so the refill after
+// an item overlaps its output stores.  What is left is set by the weight
+// lines a CU fetches for the first time: a weight tile serves only the few
+// token tiles of its expert, so each chunk brings 32 KB of L2 misses.
 #include "eat_device.h"
 #include "eat_internal.h"
 
