@@ -143,8 +143,11 @@ eat_status_t eat_params_default(eat_params_t* out);
 
 /* Validate params and build a handle for up to max_tokens tokens per call.
  * Host-only: no HIP call, no device memory.  Errors: INVALID_ARG for a null
- * pointer, a non-finite or out-of-range hyper-parameter or max_tokens < 1;
- * UNSUPPORTED for a shape or dtype outside the limits in the file header. */
+ * pointer, a non-finite or out-of-range hyper-parameter or max_tokens
+ * outside [1, 2^24]; UNSUPPORTED for a shape or dtype outside the limits in
+ * the file header, or when max_tokens times the most experts a token can
+ * select (top_k in Top-K, top_p_cap in capped Top-P, E otherwise) reaches
+ * 2^31 (selected rows are indexed with 32-bit integers). */
 eat_status_t eat_create(const eat_params_t* params, int32_t max_tokens, eat_handle_t* out);
 
 /* Release a handle (host memory only).  Null is accepted. */

@@ -125,13 +125,17 @@ eat_status_t eat_create(const eat_params_t* params, int32_t max_tokens, eat_hand
     if (max_tokens < 1 || max_tokens > kMaxTokens) return EAT_ERR_INVALID_ARG;
     const eat_status_t st = check_params(*params);
     if (st != EAT_OK) return st;
+    // most (token, expert) rows a call can select: rows, segment offsets and
+    // token indices are 32-bit
+    int32_t kmax = params->E;
+    if (params->mode == EAT_MODE_TOPK) kmax = params->top_k;
+    else if (params->mode == EAT_MODE_TOPP && params->top_p_cap > 0) kmax = params->top_p_cap;
+    if (static_cast<int64_t>(max_tokens) * kmax >= (int64_t{1} << 31)) return EAT_ERR_UNSUPPORTED;
     eat_ctx* c = new (std::nothrow) eat_ctx;
     if (!c) return EAT_ERR_INTERNAL;
     c->p = *params;
     c->max_tokens = max_tokens;
-    if (params->mode == EAT_MODE_TOPK) c->kmax = params->top_k;
-    else if (params->mode == EAT_MODE_TOPP && params->top_p_cap > 0) c->kmax = params->top_p_cap;
-    else c->kmax = params->E;
+    c->kmax = kmax;
     *out = c;
     return EAT_OK;
 }

@@ -136,6 +136,21 @@ def test_create_rejects_bad_top_p_and_token_limits():
             eat.eat_create(_params(), bad)
 
 
+def test_create_rejects_row_counts_past_32_bits():
+    # selected rows are indexed with int32: max_tokens * (most experts per token) < 2^31
+    with pytest.raises(eat.EatError) as ei:
+        eat.eat_create(_params(E=256, top_k=8), 1 << 23)          # EAT keeps up to E per token
+    assert ei.value.status == L.EAT_ERR_UNSUPPORTED
+    with pytest.raises(eat.EatError) as ei:
+        eat.eat_create(_params(mode=eat.EAT_MODE_TOPP, E=256, top_k=8), 1 << 23)
+    assert ei.value.status == L.EAT_ERR_UNSUPPORTED
+    for p in (_params(mode=eat.EAT_MODE_TOPK, E=256, top_k=8),     # K rows per token
+              _params(mode=eat.EAT_MODE_TOPP, E=256, top_k=8, top_p_cap=8),
+              _params(E=64, top_k=8)):
+        h = eat.eat_create(p, 1 << 23 if p.E == 256 else (1 << 24) - 1)
+        eat.eat_destroy(h)
+
+
 def test_workspace_grows_with_tokens_and_mode():
     h_eat = eat.eat_create(_params(), 1024)
     h_topk = eat.eat_create(_params(mode=eat.EAT_MODE_TOPK), 1024)
