@@ -197,6 +197,60 @@ def test_forward_parity(case, mode, T):
         assert (n == 0).all() and (pt == 0).all() and (cs == 0).all()
 
 
+# degenerate configurations: one expert (fp32 and bf16, the smallest d and
+# F), a cap equal to the expert count, Top-P with p = 1
+DEGENERATE = {
+    "one_expert_f32": (dict(shape="tiny", d=64, F=64, E=1, Fs=0), dict(K=1)),
+    "one_expert_bf16": (dict(shape="mixtral", d=64, F=64, E=1, Fs=0), dict(K=1)),
+    "cap_equals_e": (dict(shape="tiny", d=128, F=256, E=8, Fs=0), dict(K=8)),
+    "cap_equals_e_bf16": (dict(shape="finegrained", d=256, F=256, E=64, Fs=0), dict(K=64)),
+    "top_p_one": (dict(shape="tiny", d=128, F=256, E=8, Fs=0), dict(top_p=1.0)),
+}
+
+
+@pytest.mark.parametrize("name", list(DEGENERATE))
+@pytest.mark.parametrize("mode", ["eat", "topk", "topp"])
+@pytest.mark.parametrize("T", [1, 37])
+def test_forward_degenerate_shapes(name, mode, T):
+    c, kw = DEGENERATE[name]
+    shape, w, lay, prm = _layer(c, mode, **kw)
+    x = _x_host(shape, T, c["d"], seed=300 + T)
+    acc = make_accounts(c["E"], seed=13 + T, c_scale=0.05)
+    if mode == "eat":
+        lay.load_accounts(*acc)
+    mask = lay.mask_tensor(T)
+    y = lay.forward(_x_dev(x), mask_out=mask)
+    torch.cuda.synchronize()
+    ref = O.moe_step(x, w, acc if mode == "eat" else None, None, prm)
+    border = PT.borderline(ref.routing, prm)
+    gm = PT.masks_to_list(mask)
+    bad = [t for t in range(T) if not border[t] and gm[t] != ref.routing.masks[t]]
+    err = PT.row_rel_err(_y_host(y), ref.y)
+    ok = ~border
+    PT.report(f"degenerate {name} {mode} T={T}", borderline=int(border.sum()), mask_mismatch=len(bad),
+              max_rel_y=f"{err[ok].max() if ok.any() else 0:.2e}")
+    assert not bad
+    assert (err[ok] <= (PT.TOL_Y_BF16 if shape.bf16 else PT.TOL_Y_F32)).all()
+    if c["E"] == 1:
+        assert gm == [1] * T                  # every mode keeps the only expert
+    if mode == "topp":
+        # borderline Top-P tokens (p = 1 makes every token one) have several
+        # correct answers: the mask must still be a prefix of the token's
+        # descending-p order whose sum reaches p (to the band)
+        for t in np.flatnonzero(border):
+            pt_row = ref.routing.p[t]
+            order = np.argsort(-pt_row, kind="stable")
+            k = bin(gm[t]).count("1")
+            assert sum(1 << int(i) for i in order[:k]) == gm[t], t
+            assert pt_row[order[:k]].sum() >= prm.top_p - PT.EPS_B, t
+    n, pt, cs = lay.accounts_host()
+    if mode == "eat" and not border.any():
+        np.testing.assert_array_equal(n, ref.acc[0])
+        np.testing.assert_allclose(pt, ref.acc[1], rtol=PT.TOL_P_TOTAL, atol=1e-6)
+        np.testing.assert_allclose(cs, ref.acc[2], rtol=PT.TOL_C_BF16 if shape.bf16 else PT.TOL_C_F32, atol=1e-6)
+    lay.close()
+
+
 def test_forward_ppl_trend_and_share_reading():
     c = SMALL["finegrained"]
     T = 64
