@@ -33,7 +33,10 @@ expert of width 5632, K=4) and of the Qwen3-30B-A3B-shaped layer (4096
 tokens, 128 experts of width 768, K=8), each starting from zero accounts,
 with the expert stages' achieved bf16 TFLOP/s against the dense MFMA peak.
 A ``wide_experts`` object times decode (batch 64) of that 128-expert layer,
-whose selection masks take two 64-bit words per token.
+whose selection masks take two 64-bit words per token, and ``decode_layers``
+the decode of the fine-grained layer (batch 256, 512 steps) and of the
+shared-expert layer (batch 128, 256 steps), each with the whole layer's
+algorithmic HBM bandwidth.
 
     python bench.py [--steps K] [--warmup W] [--batch B] [--gpus 1]
 """
@@ -45,6 +48,7 @@ import json
 import os
 import sys
 import time
+from typing import Optional
 
 import numpy as np
 
@@ -141,8 +145,8 @@ def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bo
     from paper_2609_33614_amd.layer import EatLayer, capture
 
     p = L.eat_params_default(mode=mode, E=shape.E, d_model=shape.d, d_ffn=shape.F, top_k=shape.K,
-                             top_p=0.6, inv_temperature=shape.inv_temp, weight_layout=layout_code(),
-                             cs_mode=cs_mode)
+                             top_p=shape.top_p or 0.6, inv_temperature=shape.inv_temp, d_shared=shape.F_shared,
+                             weight_layout=layout_code(), cs_mode=cs_mode)
     lay = EatLayer(p, B, wdev)
     E = shape.E
     W = L.mask_words(E)
@@ -252,11 +256,13 @@ def run_prefill(shape_name: str, reps: int, ev: HipEvents, modes=("eat", "topk")
     return out
 
 
-def run_decode(shape_name: str, steps: int, warmup: int, ev: HipEvents, modes=("eat", "topk", "topp")):
+def run_decode(shape_name: str, steps: Optional[int], warmup: int, ev: HipEvents, modes=("eat", "topk", "topp")):
     """Decode steps of one more layer shape (its own decode batch, zero
-    accounts after warm-up) per routing mode: tokens/s, activated experts,
-    experts touched and the expert kernels' achieved HBM bandwidth on their
-    algorithmic bytes."""
+    accounts after warm-up; `steps` timed steps, or the layer's own count
+    when None) per routing mode: tokens/s, activated experts, experts
+    touched, the routed expert kernels' achieved HBM bandwidth on their
+    algorithmic bytes, and the whole layer's (experts touched, the always-on
+    expert, router, token rows in and out) against the step time."""
     import torch
 
     from paper_2609_33614_amd import _lib as L
@@ -265,16 +271,20 @@ def run_decode(shape_name: str, steps: int, warmup: int, ev: HipEvents, modes=("
 
     shape = SHAPES[shape_name]
     B = shape.decode_batches[0]
+    steps = shape.decode_steps if steps is None else steps
     wdev = device_weights(make_layer_weights(shape))
     xs = torch.from_numpy(HiddenStream(shape, B).steps(warmup + steps)).view(torch.bfloat16).cuda()
     out = {"workload": f"{shape_name} layer decode", "batch": B, "d_model": shape.d, "experts": shape.E,
-           "d_ffn": shape.F, "top_k": shape.K, "mask_words": L.mask_words(shape.E), "steps": steps}
+           "d_ffn": shape.F, "d_shared": shape.F_shared, "top_k": shape.K, "mask_words": L.mask_words(shape.E),
+           "steps": steps}
     for name in modes:
         r = run_mode(L.MODES[name], shape, wdev, xs, B, steps, warmup, ev, profile=True)
         up_b = sum(traffic_up(shape, B, r["k"][s], r["U"][s]) for s in range(steps))
         dn_b = sum(traffic_down(shape, r["k"][s], r["U"][s]) for s in range(steps))
         up_gbs = up_b / (r["up_ms"].sum() / 1e3) / 1e9
         dn_gbs = dn_b / (r["dn_ms"].sum() / 1e3) / 1e9
+        layer_b = (r["U"].sum() * 3.0 * shape.d * shape.F * 2 +
+                   steps * (3.0 * shape.d * shape.F_shared * 2 + shape.E * shape.d * 4 + 2.0 * B * shape.d * 2))
         out[name] = {"tokens_per_s": round(B * steps / (r["total_ms"] / 1e3), 1),
                      "ms_per_step": round(r["total_ms"] / steps, 4),
                      "mean_activated_experts": round(float(r["k"].mean()), 4),
@@ -282,7 +292,8 @@ def run_decode(shape_name: str, steps: int, warmup: int, ev: HipEvents, modes=("
                      "up_gate_us_per_launch": round(float(r["up_ms"].mean() * 1e3), 2),
                      "up_gate_hbm_frac": round(up_gbs / HBM_PEAK_GBS, 4),
                      "down_us_per_launch": round(float(r["dn_ms"].mean() * 1e3), 2),
-                     "down_hbm_frac": round(dn_gbs / HBM_PEAK_GBS, 4)}
+                     "down_hbm_frac": round(dn_gbs / HBM_PEAK_GBS, 4),
+                     "layer_hbm_frac": round(layer_b / (r["total_ms"] / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
         log(f"{shape_name} decode {name}: {out[name]['tokens_per_s']} tok/s")
     del wdev, xs
     torch.cuda.empty_cache()
@@ -464,6 +475,8 @@ def main(argv=None) -> int:
                     help="skip the decode of the 128-expert (Qwen3-30B-A3B-shaped) layer")
     ap.add_argument("--no-share", action="store_true",
                     help="skip the EAT decode under the C_s-share reading (cs_mode 1)")
+    ap.add_argument("--no-decode-layers", action="store_true",
+                    help="skip the decode of the fine-grained (B=256) and shared-expert (B=128) layers")
     ap.add_argument("--stack-steps", type=int, default=1024)
     ap.add_argument("--only-stack", action="store_true", help="time only the 16-layer stack and print its JSON")
     ap.add_argument("--only-prefill", default="", metavar="LAYER",
@@ -584,6 +597,14 @@ def main(argv=None) -> int:
             torch.cuda.empty_cache()
         log("qwen3-shaped layer decode (128 experts)")
         wide_e = run_decode("qwen3", K, W, ev)
+    decode_layers = []
+    if not args.no_decode_layers:
+        if "wdev" in locals():
+            del wdev
+            torch.cuda.empty_cache()
+        for name, dmodes in (("finegrained", ("eat", "topk", "topp")), ("shared", ("eat", "topk"))):
+            log(f"{name}-layer decode ({SHAPES[name].decode_steps} steps of B={SHAPES[name].decode_batches[0]})")
+            decode_layers.append(run_decode(name, None, W, ev, modes=dmodes))
     log("perplexity signal")
     ppl = run_ppl(ev)
     stack = None
@@ -634,6 +655,7 @@ def main(argv=None) -> int:
         "stack": stack,
         "ppl_signal": ppl,
         "wide_experts": wide_e,
+        "decode_layers": decode_layers,
     }
     print(json.dumps(out), flush=True)
     return 0

@@ -3,9 +3,9 @@
 
 Inputs (directories written by the commands below, CSV output format):
   TRACE   rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run --
-              python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-share --modes eat
+              python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers --no-share --modes eat
   FETCH   rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH -o run --
-              python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-share --modes eat --calibrate-copy 1024
+              python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers --no-share --modes eat --calibrate-copy 1024
   WRITE   the same with --pmc WRITE_SIZE
 
 Writes profiles/<name>.md (kernel table, the dominant kernel's per-launch
@@ -155,12 +155,12 @@ def main(argv=None) -> int:
                 f"{bench['steps']} timed steps (+{bench['warmup']} warm-up), MI355X.\n\n")
         f.write("Commands (from the repository root):\n\n```\n")
         f.write("rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run -- "
-                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-share --modes eat\n")
+                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers --no-share --modes eat\n")
         f.write("rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH -o run -- "
-                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-share --modes eat "
+                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers --no-share --modes eat "
                 "--calibrate-copy 1024\n")
         f.write("rocprofv3 --pmc WRITE_SIZE --output-format csv -d WRITE -o run -- "
-                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-share --modes eat "
+                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers --no-share --modes eat "
                 "--calibrate-copy 1024\n")
         f.write(f"python3 profile_summary.py --trace TRACE --fetch FETCH --write WRITE "
                 f"--bench-json TRACED_BENCH.json --name {args.name}\n```\n\n")
