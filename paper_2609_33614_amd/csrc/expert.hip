@@ -576,8 +576,15 @@ static int stream_splits(int64_t rows_m, int kdim, const eat_params_t& p, int32_
 
 // Prefill-sized calls (256 or more rows per expert on average; the
 // always-on expert from 384 tokens) go through the wide MFMA tiles.
+// Calls averaging at least this many rows per expert take the wide MFMA
+// tiles.  Measured at 32 (the fine-grained layer's 256-token decode then
+// goes wide): Top-K +4%, EAT -2% -- EAT's ~8 experts leave the wide tiles
+// ~66 work items for 256 CUs, and its down projection slows from 31 to 42 us.
+#ifndef EAT_WIDE_ROWS
+#define EAT_WIDE_ROWS 256
+#endif
 static bool use_wide(const eat_params_t& p, int32_t T) {
-    return p.expert_dtype == EAT_BF16 && static_cast<int64_t>(T) * p.top_k >= 256LL * p.E &&
+    return p.expert_dtype == EAT_BF16 && static_cast<int64_t>(T) * p.top_k >= int64_t{EAT_WIDE_ROWS} * p.E &&
            wide_fits(true, p.d_ffn, p.d_model) && wide_fits(false, p.d_model, p.d_ffn);
 }
 static bool shared_wide(const eat_params_t& p, int32_t T) {
