@@ -442,9 +442,15 @@ constexpr int max_ks() {
 
 // Waves per workgroup: the down projection with 64+-token tiles shares one
 // token slab between 8 waves (half the slab traffic per weight byte); the
-// gated kernel is faster with 4 (measured on the Mixtral-shaped layer).
+// gated kernel is faster with 4 (measured on the Mixtral-shaped layer).  8
+// waves for the gated 128-token tiles (EAT_WPB_G8): Top-K on the fine-grained
+// 256-token decode +7%, EAT -7% and the shared-expert layer -2 to -5% (EAT's
+// few experts want more, smaller workgroups).
+#ifndef EAT_WPB_G8
+#define EAT_WPB_G8 4
+#endif
 template <bool GATED, int NSUB>
-constexpr int stream_wpb() { return (!GATED && NSUB >= 4) ? 8 : 4; }
+constexpr int stream_wpb() { return (!GATED && NSUB >= 4) ? 8 : (GATED && NSUB >= 8) ? EAT_WPB_G8 : 4; }
 
 // Workgroups of one stream-kernel instance the whole chip keeps resident
 // (occupancy per CU x CUs), asked once per instance on the device current
