@@ -81,8 +81,12 @@ Workspace plan_workspace(const eat_ctx& c, int32_t T) {
     w.gu = take(w.up_splits > 1 ? 2 * static_cast<size_t>(w.up_splits) * rows * p.d_ffn * 4 : 0);
     w.yp = take(static_cast<size_t>(w.splits) * rows * p.d_model * 4);
     w.nrm = take(rows * static_cast<size_t>(combine_chunks(p)) * 4);
+    w.shared_splits = p.d_shared ? shared_splits(p, T) : 1;
+    w.shared_up_splits = p.d_shared ? shared_up_splits(p, T) : 1;
     w.hs = take(p.d_shared ? t * p.d_shared * es : 0);
     w.ys = take(p.d_shared ? t * p.d_model * 4 : 0);
+    w.gus = take(w.shared_up_splits > 1 ? 2 * static_cast<size_t>(w.shared_up_splits) * t * p.d_shared * 4 : 0);
+    w.ysp = take(w.shared_splits > 1 ? static_cast<size_t>(w.shared_splits) * t * p.d_model * 4 : 0);
     w.total = off;
     return w;
 }
@@ -245,6 +249,8 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
     b.nrm2 = reinterpret_cast<float*>(base + w.nrm);
     b.hs = base + w.hs;
     b.ys = reinterpret_cast<float*>(base + w.ys);
+    b.gus = reinterpret_cast<float*>(base + w.gus);
+    b.ysp = reinterpret_cast<float*>(base + w.ysp);
 
     hipError_t e = hipSuccess;
     auto mark = [&](int stage) {
@@ -277,7 +283,7 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
         if (p.expert_dtype == EAT_BF16)
             e = eat::launch_shared_bf16(p, T, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(ws1),
                                         static_cast<const uint16_t*>(ws3), static_cast<const uint16_t*>(ws2),
-                                        static_cast<uint16_t*>(b.hs), b.ys, stream);
+                                        static_cast<uint16_t*>(b.hs), b.ys, b.gus, b.ysp, stream);
         else
             e = eat::launch_shared_f32(p, T, static_cast<const float*>(x), static_cast<const float*>(ws1),
                                        static_cast<const float*>(ws3), static_cast<const float*>(ws2),

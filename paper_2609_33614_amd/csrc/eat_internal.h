@@ -26,12 +26,14 @@ inline int mask_words(int E) { return (E + 63) / 64; }
 // Offsets (bytes) of the workspace regions for T tokens.  Every region
 // starts on a 256-byte boundary.
 struct Workspace {
-    size_t lpart, prob, gate, mask, k, offsets, tok_idx, inv, row_expert, h, gu, yp, nrm, hs, ys;
+    size_t lpart, prob, gate, mask, k, offsets, tok_idx, inv, row_expert, h, gu, yp, nrm, hs, ys, gus, ysp;
     size_t route_total;      // bytes eat_route needs (the leading lpart region)
     size_t total;
     int64_t rows;            // capacity in (token, expert) rows = T * kmax
     int splits;              // down-projection slices held in yp
     int up_splits;           // up/gate slices held in gu (1: gu unused)
+    int shared_splits;       // always-on expert's down-projection slices held in ysp (1: ysp unused)
+    int shared_up_splits;    // its up/gate slices held in gus (1: gus unused)
 };
 Workspace plan_workspace(const eat_ctx& c, int32_t T);
 
@@ -52,6 +54,8 @@ struct Buffers {
     float* nrm2;             // [rows][combine_chunks] partial sums of squares of yp rows
     void* hs;                // [T][F_sh] shared-expert hidden
     float* ys;               // [T][d] shared-expert output
+    float* gus;              // [2][shared_up_splits][T][F_sh] its gate / up partial sums
+    float* ysp;              // [shared_splits][T][d] its down-projection partial sums
 };
 
 // ---- launchers (return hipGetLastError() after enqueueing) -------------
@@ -90,9 +94,14 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
 hipError_t launch_shared_f32(const eat_params_t& p, int32_t T, const float* x, const float* ws1,
                              const float* ws3, const float* ws2, float* hs, float* ys,
                              hipStream_t s);
+// bf16: the reduction dimensions split into shared_up_splits / shared_splits
+// slices (fp32 partials in gus / ysp, added in slice order) when the call is
+// too small to fill the chip with whole rows.
+int shared_up_splits(const eat_params_t& p, int32_t T);
+int shared_splits(const eat_params_t& p, int32_t T);
 hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* x,
                               const uint16_t* ws1, const uint16_t* ws3, const uint16_t* ws2,
-                              uint16_t* hs, float* ys, hipStream_t s);
+                              uint16_t* hs, float* ys, float* gus, float* ysp, hipStream_t s);
 
 // yp holds `splits` partial slices of the down projection, `split_stride`
 // floats apart; they are added in slice order.  `residual` (bf16 [T][d], or

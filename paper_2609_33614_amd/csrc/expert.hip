@@ -374,14 +374,28 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
     }
 }
 
+// out[i] = sum_s part[s][i] (float4 elements, slices added in slice order).
+__global__ __launch_bounds__(256) void sum_slices_kernel(const float* __restrict__ part, int splits, int64_t stride,
+                                                         int64_t n4, float* __restrict__ out) {
+    for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n4; v += int64_t(gridDim.x) * blockDim.x) {
+        float4 o = *reinterpret_cast<const float4*>(part + 4 * v);
+        for (int sp = 1; sp < splits; ++sp) {
+            const float4 q = *reinterpret_cast<const float4*>(part + sp * stride + 4 * v);
+            o.x += q.x; o.y += q.y; o.z += q.z; o.w += q.w;
+        }
+        *reinterpret_cast<float4*>(out + 4 * v) = o;
+    }
+}
+
 // H[r][f] = bf16(silu(sum_s G[s][r][f]) * sum_s U[s][r][f]) over the rows
-// in use (offsets[groups] of them), slices added in slice order.
+// in use (*rows_dev of them, or rows_host when rows_dev is null), slices
+// added in slice order.
 __global__ __launch_bounds__(256) void swiglu_reduce_kernel(const float* __restrict__ gp,
                                                             const float* __restrict__ up,
-                                                            const int32_t* __restrict__ rows_dev, int M,
-                                                            int splits, int64_t split_stride,
+                                                            const int32_t* __restrict__ rows_dev, int rows_host,
+                                                            int M, int splits, int64_t split_stride,
                                                             uint16_t* __restrict__ h) {
-    const int64_t total = static_cast<int64_t>(*rows_dev) * (M / 4);
+    const int64_t total = static_cast<int64_t>(rows_dev ? *rows_dev : rows_host) * (M / 4);
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < total;
          v += int64_t(gridDim.x) * blockDim.x) {
         const int64_t o = 4 * v;
@@ -587,8 +601,6 @@ static int stream_splits(int64_t rows_m, int kdim, const eat_params_t& p, int32_
     return s;
 }
 
-// Prefill-sized calls (256 or more rows per expert on average; the
-// always-on expert from 384 tokens) go through the wide MFMA tiles.
 // Calls averaging at least this many rows per expert take the wide MFMA
 // tiles.  Measured at 32 (the fine-grained layer's 256-token decode then
 // goes wide): Top-K +4%, EAT -2% -- EAT's ~8 experts leave the wide tiles
@@ -596,6 +608,8 @@ static int stream_splits(int64_t rows_m, int kdim, const eat_params_t& p, int32_
 #ifndef EAT_WIDE_ROWS
 #define EAT_WIDE_ROWS 256
 #endif
+// Prefill-sized calls (EAT_WIDE_ROWS or more rows per expert on average;
+// the always-on expert from 384 tokens) go through the wide MFMA tiles.
 static bool use_wide(const eat_params_t& p, int32_t T) {
     return p.expert_dtype == EAT_BF16 && static_cast<int64_t>(T) * p.top_k >= int64_t{EAT_WIDE_ROWS} * p.E &&
            wide_fits(true, p.d_ffn, p.d_model) && wide_fits(false, p.d_model, p.d_ffn);
@@ -692,7 +706,8 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     if (up.partial) {
         const int64_t vec = rows_cap * (p.d_ffn / 4);
         const int grid = static_cast<int>(std::min<int64_t>((vec + 255) / 256, 4096));
-        swiglu_reduce_kernel<<<grid, 256, 0, s>>>(gu, up.out2, offsets + p.E, p.d_ffn, usplits, up.split_stride, h);
+        swiglu_reduce_kernel<<<grid, 256, 0, s>>>(gu, up.out2, offsets + p.E, 0, p.d_ffn, usplits, up.split_stride,
+                                                  h);
         err = hipGetLastError();
         if (err != hipSuccess) return err;
     }
@@ -706,9 +721,27 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     return launch_stream<false>(dn, nsub, max_tiles, packed, s);
 }
 
+// The always-on expert below the wide-tile size: one tile row block per 64
+// weight rows is too few workgroups for the chip (88 for a 5632-wide expert,
+// 16 for its 2048-row down projection), so both projections split their
+// reduction dimension like a routed call whose tokens all go to one expert.
+int shared_up_splits(const eat_params_t& p, int32_t T) {
+    if (p.expert_dtype != EAT_BF16 || p.d_shared == 0 || shared_wide(p, T)) return 1;
+    eat_params_t one = p;
+    one.E = 1;
+    one.top_k = 1;
+    return stream_splits(p.d_shared, p.d_model, one, T, EAT_UP_SPLIT_MAX,
+                         pick_nsub(T) >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES);
+}
+
+int shared_splits(const eat_params_t& p, int32_t T) {
+    if (p.expert_dtype != EAT_BF16 || p.d_shared == 0 || shared_wide(p, T)) return 1;
+    return dense_splits(p.d_model, p.d_shared, T);
+}
+
 hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* x, const uint16_t* ws1,
-                              const uint16_t* ws3, const uint16_t* ws2, uint16_t* hs, float* ys,
-                              hipStream_t s) {
+                              const uint16_t* ws3, const uint16_t* ws2, uint16_t* hs, float* ys, float* gus,
+                              float* ysp, hipStream_t s) {
     const bool packed = p.weight_layout == EAT_LAYOUT_PACKED;
     if (shared_wide(p, T)) {
         hipError_t err =
@@ -719,16 +752,35 @@ hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* 
     const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;
     const int tiles = (T + bn - 1) / bn;
+    const int usplits = shared_up_splits(p, T);
     StreamArgs up{};
     up.wa = ws1; up.wb = ws3; up.src = x; up.gather = nullptr; up.offsets = nullptr; up.nrows = T;
-    up.groups = 1; up.M = p.d_shared; up.K = p.d_model; up.splits = 1; up.ksplit = p.d_model; up.out = hs;
+    up.groups = 1; up.M = p.d_shared; up.K = p.d_model; up.splits = usplits; up.ksplit = p.d_model / usplits;
+    up.split_stride = static_cast<int64_t>(T) * p.d_shared;
+    up.partial = usplits > 1;
+    up.out = up.partial ? static_cast<void*>(gus) : static_cast<void*>(hs);
+    up.out2 = up.partial ? gus + usplits * up.split_stride : nullptr;
     hipError_t err = launch_stream<true>(up, nsub, tiles, packed, s);
     if (err != hipSuccess) return err;
+    if (up.partial) {
+        const int64_t vec = static_cast<int64_t>(T) * (p.d_shared / 4);
+        const int grid = static_cast<int>(std::min<int64_t>((vec + 255) / 256, 4096));
+        swiglu_reduce_kernel<<<grid, 256, 0, s>>>(gus, up.out2, nullptr, T, p.d_shared, usplits, up.split_stride, hs);
+        err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
+    const int splits = shared_splits(p, T);
     StreamArgs dn{};
     dn.wa = ws2; dn.wb = nullptr; dn.src = hs; dn.gather = nullptr; dn.offsets = nullptr; dn.nrows = T;
-    dn.groups = 1; dn.M = p.d_model; dn.K = p.d_shared; dn.splits = 1; dn.ksplit = p.d_shared; dn.split_stride = 0;
-    dn.out = ys;
-    return launch_stream<false>(dn, nsub, tiles, packed, s);
+    dn.groups = 1; dn.M = p.d_model; dn.K = p.d_shared; dn.splits = splits; dn.ksplit = p.d_shared / splits;
+    dn.split_stride = static_cast<int64_t>(T) * p.d_model;
+    dn.out = splits > 1 ? ysp : ys;
+    err = launch_stream<false>(dn, nsub, tiles, packed, s);
+    if (err != hipSuccess || splits == 1) return err;
+    const int64_t n4 = dn.split_stride / 4;
+    const int grid = static_cast<int>(std::min<int64_t>((n4 + 255) / 256, 2048));
+    sum_slices_kernel<<<grid, 256, 0, s>>>(ysp, splits, dn.split_stride, n4, ys);
+    return hipGetLastError();
 }
 
 }  // namespace eat

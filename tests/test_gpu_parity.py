@@ -27,6 +27,9 @@ SMALL = {
     "mixtral": dict(shape="mixtral", d=512, F=768, E=8, Fs=0),
     "finegrained": dict(shape="finegrained", d=256, F=256, E=64, Fs=0),
     "shared": dict(shape="shared", d=256, F=192, E=60, Fs=320),
+    # an always-on expert wide enough that both of its projections split
+    # their reduction dimension (up/gate in 2 slices, down in 8)
+    "shared_split": dict(shape="shared", d=256, F=192, E=60, Fs=1024),
     # more than 64 experts: masks of 2-4 words, ragged last words
     "tiny_e100": dict(shape="tiny", d=128, F=128, E=100, Fs=0),
     "qwen3": dict(shape="qwen3", d=256, F=256, E=128, Fs=0),
@@ -160,7 +163,7 @@ def test_route_zero_input_takes_lowest_indices(case):
 
 # ------------------------------------------------------------------ forward --
 
-@pytest.mark.parametrize("case", ["tiny", "mixtral", "finegrained", "shared"] + WIDE_E)
+@pytest.mark.parametrize("case", ["tiny", "mixtral", "finegrained", "shared", "shared_split"] + WIDE_E)
 @pytest.mark.parametrize("mode", ["eat", "topk", "topp"])
 @pytest.mark.parametrize("T", [1, 33, 200])
 def test_forward_parity(case, mode, T):
