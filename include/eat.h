@@ -155,10 +155,15 @@ eat_status_t eat_destroy(eat_handle_t h);
 
 /* Bytes of device workspace a call with T tokens needs (0 <= T <=
  * max_tokens).  The workspace holds router probabilities, gates, masks,
- * the token permutation and the expert intermediates; its size is linear
- * in T and sized for the mode's largest possible number of
- * (token, expert) assignments (T*K for Top-K, T*E for EAT and uncapped
- * Top-P, since Eq. 6 keeps exact ties and the nucleus is unbounded). */
+ * the token permutation and the expert intermediates, including the fp32
+ * partial sums of projections whose reduction dimension is split (the
+ * number of slices depends on T); it grows with T and is sized for the
+ * mode's largest possible number of (token, expert) assignments (T*K for
+ * Top-K, T*E for EAT and uncapped Top-P, since Eq. 6 keeps exact ties and
+ * the nucleus is unbounded).  It is not monotonic in T: fewer tokens can
+ * mean more slices (e.g. the Mixtral-shaped EAT layer needs more at T = 128
+ * than at T = 129), so size a reused workspace by the largest value over the
+ * T a caller will pass. */
 eat_status_t eat_workspace_size(eat_handle_t h, int32_t T, size_t* bytes);
 
 /* Zero the account state N, P_total, C_s (Sec. 3.2: the statistics start
