@@ -157,7 +157,7 @@ eat_status_t eat_destroy(eat_handle_t h);
  * max_tokens).  The workspace holds router probabilities, gates, masks,
  * the token permutation and the expert intermediates, including the fp32
  * partial sums of projections whose reduction dimension is split (the
- * number of slices depends on T); it grows with T and is sized for the
+ * number of slices depends on T); it scales with T and is sized for the
  * mode's largest possible number of (token, expert) assignments (T*K for
  * Top-K, T*E for EAT and uncapped Top-P, since Eq. 6 keeps exact ties and
  * the nucleus is unbounded).  It is not monotonic in T: fewer tokens can
