@@ -101,11 +101,17 @@ def load() -> C.CDLL:
 # ------------------------------------------------------------ marshalling --
 
 def _ptr(t) -> Optional[int]:
-    """Device (or host) address of a tensor, an int address, or None."""
+    """Device address of a tensor (which must be a dense GPU tensor: the C
+    entry points take device pointers to densely packed arrays and cannot
+    check either), an int address, or None."""
     if t is None:
         return None
     if isinstance(t, int):
         return t
+    if not t.is_cuda:
+        raise ValueError("libeat takes device arrays: got a tensor on " + str(t.device))
+    if not t.is_contiguous():
+        raise ValueError("libeat takes densely packed arrays: got a non-contiguous tensor view")
     return t.data_ptr()
 
 

@@ -357,3 +357,12 @@ def test_pack_validation_happens_on_the_host():
         with pytest.raises(eat.EatError) as ei:
             eat.eat_pack_weights(**args)
         assert ei.value.status == L.EAT_ERR_INVALID_ARG, kw
+
+
+def test_binding_rejects_host_and_strided_tensors():
+    # the C entry points take dense device arrays; the binding refuses what
+    # they could not check (a host tensor would be read as a device address)
+    import torch
+    with pytest.raises(ValueError, match="device arrays"):
+        L._ptr(torch.zeros(4))
+    assert L._ptr(None) is None and L._ptr(FAKE) == FAKE
