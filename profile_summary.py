@@ -21,6 +21,13 @@ Prefill (MFMA-bound) summary of the wide tile kernels, from a trace of
               python3 bench.py --only-prefill LAYER --modes topk
 
     python profile_summary.py --prefill --trace T --bench-json B.json --name NAME
+
+Stacked-layer decode (per-layer kernel breakdown), from a trace of
+
+  TRACE   rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run --
+              python3 bench.py --only-stack --modes eat --stack-steps 128
+
+    python profile_summary.py --stack --trace T --bench-json B.json --name NAME
 """
 from __future__ import annotations
 
@@ -111,6 +118,52 @@ def prefill_summary(args) -> int:
     return 0
 
 
+def stack_summary(args) -> int:
+    """Average duration of every kernel of the traced stacked-layer decode
+    per launch and per layer of a timed step (16 warm-up steps, then the
+    timed steps; one traced routing mode)."""
+    bench = json.loads(open(args.bench_json).read().strip().splitlines()[-1])
+    st = bench["stack"]
+    modes = [m for m in ("eat", "topk", "topp", "eat_layerwise") if m in st]
+    assert len(modes) == 1, "trace one routing mode at a time"
+    r = st[modes[0]]
+    layers, steps = st["layers"], st["steps"]
+    trace = list(csv.DictReader(open(os.path.join(args.trace, "run_kernel_trace.csv"))))
+    trace.sort(key=lambda x: int(x["Start_Timestamp"]))
+    # the timed steps' launches are the last ones of the kernels a step runs
+    per = {}
+    for x in trace:
+        name = x["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0].replace("void ", "")
+        if name.startswith("eat::") and "pack_kernel" not in name and "reset_accounts" not in name:
+            per.setdefault(name, []).append((int(x["End_Timestamp"]) - int(x["Start_Timestamp"])) / 1e3)
+    total_steps = steps + 16
+    md = os.path.join(ROOT, "profiles", args.name + ".md")
+    with open(md, "w") as f:
+        f.write(f"# {args.name}\n\n")
+        f.write(f"Workload: {st['workload']}, {layers} layers, batch {st['batch']}, d_model {st['d_model']}, "
+                f"{st['experts']} experts of width {st['d_ffn']}, K={st['top_k']}, {modes[0]} routing, "
+                f"{steps} timed steps after 16 warm-up steps, MI355X.\n\n")
+        f.write("Commands (from the repository root):\n\n```\n")
+        f.write(f"rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run -- "
+                f"python3 bench.py --only-stack --modes {modes[0]} --stack-steps {steps}\n")
+        f.write(f"python3 profile_summary.py --stack --trace TRACE --bench-json TRACED_BENCH.json --name {args.name}\n```\n\n")
+        f.write(f"Step time in the traced run (HIP events): {r['ms_per_step'] * 1e3:.0f} us = "
+                f"{r['ms_per_step'] * 1e3 / layers:.1f} us per layer; {r['tokens_per_s']:.0f} tokens/s.\n\n")
+        f.write("| kernel | launches per layer and step | avg us per launch | us per layer and step |\n")
+        f.write("|---|---|---|---|\n")
+        rows = []
+        for name, durs in per.items():
+            n_per = len(durs) / (total_steps * layers)
+            timed = durs[-int(round(n_per * steps * layers)):] if n_per > 0 else durs
+            avg = statistics.mean(timed)
+            rows.append((avg * n_per, name, n_per, avg))
+        for tot, name, n_per, avg in sorted(rows, reverse=True):
+            f.write(f"| `{name}` | {n_per:.2f} | {avg:.2f} | {tot:.2f} |\n")
+        f.write(f"| **sum** | | | **{sum(x[0] for x in rows):.1f}** |\n")
+    print(open(md).read())
+    return 0
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", required=True)
@@ -122,9 +175,12 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=256)
     ap.add_argument("--prefill", action="store_true", help="summarise a prefill trace (wide tile kernels)")
     ap.add_argument("--reps", type=int, default=10, help="timed prefill calls in the traced run")
+    ap.add_argument("--stack", action="store_true", help="summarise a stacked-layer decode trace")
     args = ap.parse_args(argv)
     if args.prefill:
         return prefill_summary(args)
+    if args.stack:
+        return stack_summary(args)
     assert args.fetch and args.write, "--fetch and --write are needed for the decode summary"
 
     bench = json.loads(open(args.bench_json).read().strip().splitlines()[-1])
