@@ -54,7 +54,7 @@ def _y_host(y):
     return y.float().cpu().numpy().astype(np.float64)
 
 
-def _layer(case, mode, K=None, top_p=None, cs_mode=0, max_tokens=512, seed=None, scale=None):
+def _layer(case, mode, K=None, top_p=None, cs_mode=0, max_tokens=512, seed=None, scale=None, top_p_cap=0):
     shape = SHAPES[case["shape"]]
     w = make_layer_weights(shape, seed=seed, E=case["E"], d=case["d"], F=case["F"], F_shared=case["Fs"])
     dt = L.EAT_BF16 if shape.bf16 else L.EAT_F32
@@ -62,7 +62,7 @@ def _layer(case, mode, K=None, top_p=None, cs_mode=0, max_tokens=512, seed=None,
                              top_k=shape.K if K is None else K,
                              top_p=(shape.top_p or 0.6) if top_p is None else top_p,
                              inv_temperature=shape.inv_temp, cs_mode=cs_mode, act_dtype=dt,
-                             expert_dtype=dt, d_shared=case["Fs"])
+                             expert_dtype=dt, d_shared=case["Fs"], top_p_cap=top_p_cap)
     scale_dev = None
     if scale is not None:
         scale_dev = torch.from_numpy(scale).cuda()
@@ -71,6 +71,7 @@ def _layer(case, mode, K=None, top_p=None, cs_mode=0, max_tokens=512, seed=None,
     lay.scale_dev = scale_dev            # the handle keeps the pointer: keep the tensor alive
     prm = PT.oracle_params(shape, MODES[mode], K=K, top_p=top_p, cs_mode=cs_mode, shared=case["Fs"] > 0)
     prm.expert_scale = scale
+    prm.top_p_cap = top_p_cap
     return shape, w, lay, prm
 
 
@@ -251,6 +252,43 @@ def test_forward_degenerate_shapes(name, mode, T):
         np.testing.assert_array_equal(n, ref.acc[0])
         np.testing.assert_allclose(pt, ref.acc[1], rtol=PT.TOL_P_TOTAL, atol=1e-6)
         np.testing.assert_allclose(cs, ref.acc[2], rtol=PT.TOL_C_BF16 if shape.bf16 else PT.TOL_C_F32, atol=1e-6)
+    lay.close()
+
+
+# capped Top-P (top_p_cap): p = 0.9 so that the nucleus usually outgrows the
+# cap; caps of 1, one within a mask word and one spanning words (E = 200)
+@pytest.mark.parametrize("case,cap", [("tiny", 1), ("tiny", 3), ("finegrained", 3), ("finegrained", 8),
+                                      ("qwen3", 5), ("qwen3_e200", 70)])
+@pytest.mark.parametrize("T", [1, 37])
+def test_forward_parity_topp_cap(case, cap, T):
+    c = SMALL[case]
+    shape, w, lay, prm = _layer(c, "topp", top_p=0.9, top_p_cap=cap)
+    x = _x_host(shape, T, c["d"], seed=500 + T)
+    mask = lay.mask_tensor(T)
+    y = lay.forward(_x_dev(x), mask_out=mask)
+    torch.cuda.synchronize()
+    ref = O.moe_step(x, w, None, None, prm)
+    border = PT.borderline(ref.routing, prm)
+    gm = PT.masks_to_list(mask)
+    bad = [t for t in range(T) if not border[t] and gm[t] != ref.routing.masks[t]]
+    err = PT.row_rel_err(_y_host(y), ref.y)
+    ok = ~border
+    capped = int((ref.routing.k == cap).sum())
+    PT.report(f"top-p cap {case} cap={cap} T={T}", borderline=int(border.sum()), mask_mismatch=len(bad),
+              at_cap=capped, max_rel_y=f"{err[ok].max() if ok.any() else 0:.2e}")
+    assert not bad
+    assert all(bin(m).count("1") <= cap for m in gm)
+    # borderline tokens (near-equal probabilities decide the order) must still
+    # be valid capped nuclei: the selected experts outweigh the others (to the
+    # band), and the prefix stops at the cap or once its sum reaches p
+    for t in np.flatnonzero(border):
+        pr = ref.routing.p[t]
+        sel = np.array([(gm[t] >> e) & 1 for e in range(c["E"])], dtype=bool)
+        assert sel.any(), t
+        if (~sel).any():
+            assert pr[sel].min() >= pr[~sel].max() - PT.EPS_B, t
+        assert sel.sum() == cap or pr[sel].sum() >= prm.top_p - PT.EPS_B, t
+    assert (err[ok] <= (PT.TOL_Y_BF16 if shape.bf16 else PT.TOL_Y_F32)).all()
     lay.close()
 
 

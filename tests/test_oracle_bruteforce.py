@@ -105,6 +105,22 @@ def test_topp_cap_limits_prefix():
     assert O.select_topp(p, 0.9, cap=2) == [0, 1]
 
 
+@pytest.mark.parametrize("E", [3, 5, 8])
+@pytest.mark.parametrize("thr", [0.5, 0.9])
+def test_topp_cap_is_the_heaviest_subset_of_the_capped_size(E, thr):
+    # with a cap c the nucleus is the heaviest subset of size min(k*, c),
+    # k* the size of the smallest subset reaching thr (by enumeration)
+    rng = np.random.default_rng(10 * E + int(10 * thr))
+    for p in _vectors(E, rng)[:20]:
+        reaching = [s for r in range(1, E + 1) for s in itertools.combinations(range(E), r)
+                    if sum(p[i] for i in s) >= thr]
+        k_star = min(len(s) for s in reaching) if reaching else E
+        for cap in range(1, E + 1):
+            size = min(k_star, cap)
+            heaviest = max(itertools.combinations(range(E), size), key=lambda s: sum(p[i] for i in s))
+            assert O.select_topp(p, thr, cap) == sorted(heaviest), (cap, p)
+
+
 @pytest.mark.parametrize("E", [4, 8])
 def test_eat_route_against_enumeration_with_history(E):
     """Whole per-token EAT path with random non-zero accounts: the oracle's
