@@ -292,6 +292,64 @@ def test_forward_parity_topp_cap(case, cap, T):
     lay.close()
 
 
+# every EAT hyper-parameter away from the paper's value (both sides get the
+# same set), so a constant written into a kernel instead of its parameter
+# shows; with a perplexity trend and two steps from zero accounts (the first
+# step selects fewer than K experts for most of these sets, the EMA's alpha
+# acts on the second step's accounts)
+HYPER = [
+    dict(beta=0.25, w1=0.5, w2=0.2, w3=0.3, alpha1=0.8, alpha2=0.4, kappa1=0.45, kappa2=0.55,
+         ppl_up=1.5, ppl_down=0.75, q_lo=0.2, q_hi=0.8, alpha=0.7, eps=1e-6),
+    dict(beta=0.9, w1=0.1, w2=0.6, w3=0.3, alpha1=0.2, alpha2=2.0, kappa1=1.0, kappa2=0.0,
+         ppl_up=1.05, ppl_down=0.95, q_lo=0.0, q_hi=1.0, alpha=0.3, eps=1e-4),
+]
+
+
+@pytest.mark.parametrize("case", ["tiny", "finegrained", "qwen3"])
+@pytest.mark.parametrize("hp", range(len(HYPER)))
+def test_forward_parity_hyperparameters(case, hp):
+    c = SMALL[case]
+    shape = SHAPES[c["shape"]]
+    kw = HYPER[hp]
+    w = make_layer_weights(shape, E=c["E"], d=c["d"], F=c["F"], F_shared=c["Fs"])
+    dt = L.EAT_BF16 if shape.bf16 else L.EAT_F32
+    inv_t = 1.5
+    p = L.eat_params_default(mode=L.EAT_MODE_EAT, E=c["E"], d_model=c["d"], d_ffn=c["F"], top_k=shape.K,
+                             inv_temperature=inv_t, act_dtype=dt, expert_dtype=dt, **kw)
+    lay = EatLayer(p, 64, to_device(w))
+    prm = O.Params(mode=O.MODE_EAT, K=shape.K, inv_temp=inv_t, **kw)
+    T = 37
+    # zero accounts: the first step's importance is (1 - beta) p, so the
+    # threshold parameters decide how many experts (fewer than K) survive
+    acc = O.zero_accounts(c["E"])
+    lay.load_accounts(*acc)
+    for step in range(2):
+        x = _x_host(shape, T, c["d"], seed=600 + 10 * hp + step)
+        trend = make_trend(T, seed=700 + step)
+        mask = lay.mask_tensor(T)
+        y = lay.forward(_x_dev(x), trend=torch.from_numpy(trend).cuda(), mask_out=mask)
+        torch.cuda.synchronize()
+        ref = O.moe_step(x, w, acc, trend, prm)
+        border = PT.borderline(ref.routing, prm)
+        gm = PT.masks_to_list(mask)
+        bad = [t for t in range(T) if not border[t] and gm[t] != ref.routing.masks[t]]
+        err = PT.row_rel_err(_y_host(y), ref.y)
+        ok = ~border
+        PT.report(f"hyper-parameters {hp} {case} step {step}", borderline=int(border.sum()),
+                  mask_mismatch=len(bad), mean_k=f"{np.mean(ref.routing.k):.2f}",
+                  max_rel_y=f"{err[ok].max() if ok.any() else 0:.2e}")
+        assert not bad
+        assert (err[ok] <= (PT.TOL_Y_BF16 if shape.bf16 else PT.TOL_Y_F32)).all()
+        n, pt, cs = lay.accounts_host()
+        if border.any():
+            break                           # the accounts may then differ legitimately
+        np.testing.assert_array_equal(n, ref.acc[0])
+        np.testing.assert_allclose(pt, ref.acc[1], rtol=PT.TOL_P_TOTAL, atol=1e-6)
+        np.testing.assert_allclose(cs, ref.acc[2], rtol=PT.TOL_C_BF16 if shape.bf16 else PT.TOL_C_F32, atol=1e-6)
+        acc = ref.acc
+    lay.close()
+
+
 def test_forward_ppl_trend_and_share_reading():
     c = SMALL["finegrained"]
     T = 64
