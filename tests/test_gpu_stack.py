@@ -169,3 +169,55 @@ def test_stack_reset_clears_every_layer():
     torch.cuda.synchronize()
     assert all(lay.accounts_host()[0].sum() == 0 for lay in stack.layers)
     stack.close()
+
+
+@pytest.mark.parametrize("mode", ["topk", "eat"])
+def test_stack_mixed_expert_counts(mode):
+    """Layers with different expert counts (16, 100, 16: one, two and one
+    64-bit mask words per token): each layer's masks and probabilities land at
+    its own offset of masks_out / probs_out (T * words_l and T * E_l after the
+    layers before it), checked layer by layer against the oracle."""
+    shape = SHAPES["stack16"]
+    Es, d, F, B = [16, 100, 16], 256, 128, 32
+    nl = len(Es)
+    w_host = [make_layer_weights(shape, layer=l, E=E, d=d, F=F) for l, E in enumerate(Es)]
+    mixes = [make_mixing(shape, l, d=d) for l in range(nl)]
+    params = [L.eat_params_default(mode=L.MODES[mode], E=E, d_model=d, d_ffn=F, top_k=4, top_p=shape.top_p,
+                                   inv_temperature=shape.inv_temp) for E in Es]
+    stack = EatStack(params, B, [to_device(w) for w in w_host],
+                     [torch.from_numpy(m).view(torch.bfloat16).cuda() for m in mixes])
+    prms = []
+    for _ in range(nl):
+        prm = PT.oracle_params(shape, L.MODES[mode], K=4)
+        prm.round_h = True
+        prms.append(prm)
+    words = [L.mask_words(E) for E in Es]
+    x = HiddenStream(shape, B, d=d).next()
+    masks = torch.zeros(B * sum(words), dtype=torch.int64, device="cuda")
+    probs = torch.zeros(B * sum(Es), dtype=torch.float32, device="cuda")
+    h = stack.forward(torch.from_numpy(x).view(torch.bfloat16).cuda(), masks_out=masks, probs_out=probs)
+    torch.cuda.synchronize()
+    ref = O.stack_step(x, w_host, mixes, [O.zero_accounts(E) for E in Es], None, prms)
+    mg, pg = masks.cpu(), probs.cpu().numpy()
+    taint = np.zeros(B, dtype=bool)
+    moff = poff = 0
+    for l, (E, W) in enumerate(zip(Es, words)):
+        r = ref.layers[l].routing
+        pl = pg[poff:poff + B * E].reshape(B, E)
+        ml = mg[moff:moff + B * W].reshape(B, W) if W > 1 else mg[moff:moff + B]
+        dp_t = np.abs(pl - r.p).max(axis=1)
+        assert float(dp_t[~taint].max()) <= DP_CEIL, f"layer {l}"
+        border = PT.borderline(r, prms[l], eps_b=np.maximum(PT.EPS_B, 4.0 * dp_t)) & ~taint
+        gm = PT.masks_to_list(ml)
+        bad = [t for t in range(B) if not taint[t] and not border[t] and gm[t] != r.masks[t]]
+        assert not bad, f"layer {l} (E={E}): {len(bad)} mask mismatches"
+        taint |= border
+        moff += B * W
+        poff += B * E
+    assert taint.mean() <= 0.5
+    hg = h.view(torch.int16).cpu().numpy().view(np.uint16)
+    err = PT.row_rel_err(O.widen(hg), ref.h)[~taint]
+    PT.report(f"stack mixed E {mode}", layers=nl, T=B, excluded=int(taint.sum()),
+              max_rel_h=f"{err.max():.2e}" if err.size else "n/a")
+    assert err.size == 0 or err.max() <= TOL_H
+    stack.close()
