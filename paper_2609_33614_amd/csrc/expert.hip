@@ -125,7 +125,7 @@ __device__ __forceinline__ bf16x8 ld16_stream(const uint16_t* p) {
     return __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(p));
 }
 
-// One workgroup = 4 waves = 64 consecutive weight rows (16 per wave) of one
+// One workgroup = WPB waves = 16 WPB consecutive weight rows (16 per wave) of one
 // expert, applied to one tile of up to 16*NSUB of that expert's tokens.
 // The reduction dimension is walked in chunks of 32*KS:
 //   * the tile's token rows for the next chunk are fetched into registers
@@ -455,16 +455,19 @@ constexpr int max_ks() {
 }
 
 // Waves per workgroup: the down projection with 64+-token tiles shares one
-// token slab between 8 waves (half the slab traffic per weight byte); the
-// gated kernel is faster with 4 (measured on the Mixtral-shaped layer).  8
-// waves for the gated 128-token tiles (EAT_WPB_G8): Top-K on the fine-grained
-// 256-token decode +7%, EAT -7% and the shared-expert layer -2 to -5% (EAT's
-// few experts want more, smaller workgroups).
+// token slab between 8 waves (half the slab traffic per weight byte).  The
+// gated kernel with up to 64-token tiles runs 2 waves (32 weight rows) per
+// workgroup: twice the work items of 4 waves, so the last ones spread more
+// evenly over the CUs (Mixtral-shaped decode +1%, its Top-K +4%, the 16-layer
+// stack's Top-K +6%).  8 waves for the gated 128-token tiles (EAT_WPB_G8):
+// Top-K on the fine-grained 256-token decode +7%, EAT -7% and the
+// shared-expert layer -2 to -5% (EAT's few experts want more, smaller
+// workgroups); they keep 4.
 #ifndef EAT_WPB_G8
 #define EAT_WPB_G8 4
 #endif
 template <bool GATED, int NSUB>
-constexpr int stream_wpb() { return (!GATED && NSUB >= 4) ? 8 : (GATED && NSUB >= 8) ? EAT_WPB_G8 : 4; }
+constexpr int stream_wpb() { return (!GATED && NSUB >= 4) ? 8 : (GATED && NSUB >= 8) ? EAT_WPB_G8 : GATED ? 2 : 4; }
 
 // Workgroups of one stream-kernel instance the whole chip keeps resident
 // (occupancy per CU x CUs), asked once per instance on the device current
@@ -503,6 +506,9 @@ hipError_t launch_stream_k(const StreamArgs& a, int64_t max_tiles, hipStream_t s
         return hipErrorInvalidValue;
     } else if constexpr (stream_wpb<GATED, NSUB>() == 8) {
         if (a.M % 128 == 0) return launch_stream_w<GATED, NSUB, KS, 8, PACKED>(a, max_tiles, s);
+        return launch_stream_w<GATED, NSUB, KS, 4, PACKED>(a, max_tiles, s);
+    } else if constexpr (stream_wpb<GATED, NSUB>() == 2) {
+        if (a.M % 32 == 0) return launch_stream_w<GATED, NSUB, KS, 2, PACKED>(a, max_tiles, s);
         return launch_stream_w<GATED, NSUB, KS, 4, PACKED>(a, max_tiles, s);
     } else {
         return launch_stream_w<GATED, NSUB, KS, 4, PACKED>(a, max_tiles, s);
