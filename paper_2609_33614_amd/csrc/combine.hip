@@ -59,12 +59,20 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     const bool on = 4 * j < a.d;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     const uint64_t* mt = a.mask + static_cast<size_t>(t) * a.words;
+    // the shared-expert and residual slices do not depend on the routing, so
+    // they are loaded first, from in-bounds stand-ins when absent (slice 0 of
+    // the partials; element 0 for threads past d), and used after the loop
+    const int jc = on ? j : 0;
+    const float4 ysv =
+        *reinterpret_cast<const float4*>((a.ys ? a.ys + static_cast<size_t>(t) * a.d : a.yp) + 4 * jc);
+    const uint2 rsv = *reinterpret_cast<const uint2*>(
+        (a.res ? a.res + static_cast<size_t>(t) * a.d : reinterpret_cast<const uint16_t*>(a.yp)) + 4 * jc);
 
     int w = 0;
     uint64_t rest = mt[0];
     for (;;) {
         // next batch of selected experts (uniform across the workgroup)
-        int64_t rows[kBatch];
+        int rows[kBatch];                     // < 2^31: the row count is checked at creation
         float gs[kBatch];
         int nb = 0;
 #pragma unroll
@@ -87,7 +95,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
             ss[b] = 0.f;
             if (b < nb && on) {
                 // all of the row slice's partials in flight at once, added in slice order
-                const float* src = a.yp + rows[b] * a.d + 4 * j;
+                const float* src = a.yp + static_cast<int64_t>(rows[b]) * a.d + 4 * j;
                 float4 q[kMaxSplits];
 #pragma unroll
                 for (int sp = 0; sp < kMaxSplits; ++sp)
@@ -117,7 +125,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
                 float tot = 0.f;
 #pragma unroll
                 for (int q = 0; q < kWaves; ++q) tot += red[b][q];
-                a.nrm2[rows[b] * a.nchunk + chunk] = tot;
+                a.nrm2[static_cast<int64_t>(rows[b]) * a.nchunk + chunk] = tot;
             }
         }
         __syncthreads();
@@ -125,11 +133,11 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     }
     if (!on) return;
     if (a.ys) {
-        const float4 q = *reinterpret_cast<const float4*>(a.ys + static_cast<size_t>(t) * a.d + 4 * j);
+        const float4 q = ysv;
         acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
     }
     if (a.res) {
-        const uint2 q = *reinterpret_cast<const uint2*>(a.res + static_cast<size_t>(t) * a.d + 4 * j);
+        const uint2 q = rsv;
         acc.x += bf16_to_f32(static_cast<uint16_t>(q.x & 0xffffu));
         acc.y += bf16_to_f32(static_cast<uint16_t>(q.x >> 16));
         acc.z += bf16_to_f32(static_cast<uint16_t>(q.y & 0xffffu));

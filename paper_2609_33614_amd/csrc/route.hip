@@ -122,15 +122,15 @@ __global__ __launch_bounds__(256) void logits_kernel(RouteArgs a) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) acc[tt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // Every load is unconditional: token rows past T and experts past E read
+    // row 0, which exists, and their scores are never written.  (A load under
+    // a per-lane branch makes the compiler wait for it inside the branch, one
+    // round trip per group of k-steps.)
     auto load = [&](int k, float (&xv)[TT][4], float4 (&wv)[NT]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int tt = 0; tt < TT; ++tt) {
-            xv[tt][0] = xv[tt][1] = xv[tt][2] = xv[tt][3] = 0.f;
-            if (row_ok[tt]) load_x4<XT>(xrow[tt], k + kq, xv[tt]);
-        }
+        for (int tt = 0; tt < TT; ++tt) load_x4<XT>(xrow[tt], k + kq, xv[tt]);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-            wv[nt] = e_ok[nt] ? *reinterpret_cast<const float4*>(wrow[nt] + k + kq) : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int nt = 0; nt < NT; ++nt) wv[nt] = *reinterpret_cast<const float4*>(wrow[nt] + k + kq);
     };
     auto step = [&](const float (&xv)[TT][4], const float4 (&wv)[NT]) __attribute__((always_inline)) {
 #pragma unroll
@@ -203,27 +203,42 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
 
     // ---- this token's partial router scores: every slice's load issued
     // before the history score below, summed (in slice order) after it ----
+    // The kernel's loads are all issued here, before any of them is waited
+    // for, from clamped in-bounds addresses (token 0, expert 0, slice 0, or the
+    // partial-score buffer standing in for an absent trend or scale); values
+    // read for lanes past E or slices past the call's are never used.  (A load
+    // under a per-lane branch makes the compiler wait for it inside the
+    // branch, a round trip each.)
     const int t = blockIdx.x * kSelWaves + wave;
     const bool tok = t < a.T;
+    const int tc = tok ? t : 0;
     float zp[J][kMaxRouteSlices];
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-        const float* src = a.part + static_cast<size_t>(tok ? t : 0) * E + 64 * j + lane;
+        const float* src = a.part + static_cast<size_t>(tc) * E + (valid[j] ? 64 * j + lane : 0);
         const size_t stride = static_cast<size_t>(a.T) * E;
 #pragma unroll
-        for (int sl = 0; sl < kMaxRouteSlices; ++sl)
-            zp[j][sl] = (valid[j] && sl < a.slices) ? src[sl * stride] : 0.f;
+        for (int sl = 0; sl < kMaxRouteSlices; ++sl) zp[j][sl] = src[(sl < a.slices ? sl : 0) * stride];
     }
+    const int8_t trend_t = *(a.trend ? a.trend + tc : reinterpret_cast<const int8_t*>(a.part));
+    float scale[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) scale[j] = (a.scale ? a.scale : a.part)[valid[j] ? 64 * j + lane : 0];
 
     // ---- history score from the account snapshot (Eq. 1) --------------
     if (a.mode == EAT_MODE_EAT && wave == 0) {
         double n[J], pt[J], c[J];
 #pragma unroll
         for (int j = 0; j < J; ++j) {
-            const int e = 64 * j + lane;
-            n[j] = valid[j] ? static_cast<double>(a.acc_n[e]) : 0.0;
-            pt[j] = valid[j] ? static_cast<double>(a.acc_p[e]) : 0.0;
-            c[j] = valid[j] ? static_cast<double>(a.acc_c[e]) : 0.0;
+            // relaxed loads: plain loads that the compiler does not move
+            // under the lane test below (and then wait for one by one)
+            const int e = valid[j] ? 64 * j + lane : 0;
+            const int64_t nv = __hip_atomic_load(a.acc_n + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            const float pv = __hip_atomic_load(a.acc_p + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            const float cv = __hip_atomic_load(a.acc_c + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            n[j] = valid[j] ? static_cast<double>(nv) : 0.0;
+            pt[j] = valid[j] ? static_cast<double>(pv) : 0.0;
+            c[j] = valid[j] ? static_cast<double>(cv) : 0.0;
         }
         double ln = n[0], lc = c[0];
 #pragma unroll
@@ -268,7 +283,7 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
         // Sec. 3.5: OPD reweighting, p'_i = s_i p_i / sum_j s_j p_j, used for
         // everything below (importance, threshold, selection, gates, P_total)
 #pragma unroll
-        for (int j = 0; j < J; ++j) p[j] = valid[j] ? a.scale[64 * j + lane] * p[j] : 0.f;
+        for (int j = 0; j < J; ++j) p[j] = valid[j] ? scale[j] * p[j] : 0.f;
         const float den = wave_sum_j<J>(p);
 #pragma unroll
         for (int j = 0; j < J; ++j) p[j] = p[j] / den;
@@ -291,7 +306,7 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
         const float sigma = sqrtf(wave_sum_j<J>(tmp) / static_cast<float>(E));
         const float tau = fmaxf(a.alpha1 * mu, mu - a.alpha2 * sigma);
         // perplexity adjustment and smoothing (Sec. 3.3)
-        const float f = (a.trend != nullptr && a.trend[t] > 0) ? a.ppl_up : a.ppl_down;
+        const float f = (a.trend != nullptr && trend_t > 0) ? a.ppl_up : a.ppl_down;
         const float tau_s = a.kappa1 * (f * tau) + a.kappa2 * tau;
         // bounds: q_lo / q_hi points of the sorted routing weights
         int rank[J];
