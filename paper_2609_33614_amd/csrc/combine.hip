@@ -89,26 +89,35 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
             }
         }
         if (nb == 0) break;
+        // each row slice's partials are all loaded at once and added in slice
+        // order; the next row's loads are issued before this row is added up
+        // (threads past d read the row's first elements and discard them)
+        float4 q[2][kMaxSplits];
+        auto issue = [&](float4 (&dst)[kMaxSplits], int row) __attribute__((always_inline)) {
+            const float* src = a.yp + static_cast<int64_t>(row) * a.d + 4 * jc;
+#pragma unroll
+            for (int sp = 0; sp < kMaxSplits; ++sp)
+                if (sp < a.splits) dst[sp] = *reinterpret_cast<const float4*>(src + sp * a.split_stride);
+        };
+        issue(q[0], rows[0]);
         float ss[kBatch];
 #pragma unroll
         for (int b = 0; b < kBatch; ++b) {
             ss[b] = 0.f;
-            if (b < nb && on) {
-                // all of the row slice's partials in flight at once, added in slice order
-                const float* src = a.yp + static_cast<int64_t>(rows[b]) * a.d + 4 * j;
-                float4 q[kMaxSplits];
-#pragma unroll
-                for (int sp = 0; sp < kMaxSplits; ++sp)
-                    if (sp < a.splits) q[sp] = *reinterpret_cast<const float4*>(src + sp * a.split_stride);
-                float4 o = q[0];
+            if (b < nb) {
+                if (b + 1 < nb) issue(q[(b + 1) & 1], rows[b + 1]);
+                const float4 (&c)[kMaxSplits] = q[b & 1];
+                float4 o = c[0];
 #pragma unroll
                 for (int sp = 1; sp < kMaxSplits; ++sp)
-                    if (sp < a.splits) { o.x += q[sp].x; o.y += q[sp].y; o.z += q[sp].z; o.w += q[sp].w; }
-                ss[b] = fmaf(o.x, o.x, ss[b]); ss[b] = fmaf(o.y, o.y, ss[b]);
-                ss[b] = fmaf(o.z, o.z, ss[b]); ss[b] = fmaf(o.w, o.w, ss[b]);
-                const float g = gs[b];
-                acc.x = fmaf(g, o.x, acc.x); acc.y = fmaf(g, o.y, acc.y);
-                acc.z = fmaf(g, o.z, acc.z); acc.w = fmaf(g, o.w, acc.w);
+                    if (sp < a.splits) { o.x += c[sp].x; o.y += c[sp].y; o.z += c[sp].z; o.w += c[sp].w; }
+                if (on) {
+                    ss[b] = fmaf(o.x, o.x, ss[b]); ss[b] = fmaf(o.y, o.y, ss[b]);
+                    ss[b] = fmaf(o.z, o.z, ss[b]); ss[b] = fmaf(o.w, o.w, ss[b]);
+                    const float g = gs[b];
+                    acc.x = fmaf(g, o.x, acc.x); acc.y = fmaf(g, o.y, acc.y);
+                    acc.z = fmaf(g, o.z, acc.z); acc.w = fmaf(g, o.w, acc.w);
+                }
             }
         }
 #pragma unroll
@@ -190,12 +199,14 @@ __global__ __launch_bounds__(kThreads) void update_accounts_kernel(
 // (written when h_out is set), then u = bf16(h * (1 / sqrt(mean(h^2) + eps)))
 // with the sum of squares taken over the bf16 values, per thread then per
 // wave (butterfly) then over the waves in order.
+// S = the number of split partials (a template argument, so that every
+// slice's load is issued before the first add; 0 = read the bf16 source row).
 constexpr int kMixVec = 4;                                  // floats per thread and group
 constexpr int kMixGroups = 8;                               // d <= 256 * 4 * 8 = 8192
-__global__ __launch_bounds__(kThreads) void mix_norm_kernel(const float* __restrict__ part, int splits,
-                                                            int64_t split_stride, const uint16_t* __restrict__ src,
-                                                            int d, float eps, uint16_t* __restrict__ h_out,
-                                                            uint16_t* __restrict__ u_out) {
+template <int S>
+__global__ __launch_bounds__(kThreads) void mix_norm_kernel(const float* __restrict__ part, int64_t split_stride,
+                                                            const uint16_t* __restrict__ src, int d, float eps,
+                                                            uint16_t* __restrict__ h_out, uint16_t* __restrict__ u_out) {
     __shared__ float red[kWaves];
     const int t = blockIdx.x;
     const int lane = lane_id(), wave = threadIdx.x / kWave;
@@ -206,12 +217,13 @@ __global__ __launch_bounds__(kThreads) void mix_norm_kernel(const float* __restr
         const int j = (g * kThreads + threadIdx.x) * kMixVec;
         if (j >= d) continue;
         const size_t o = static_cast<size_t>(t) * d + j;
-        if (splits > 0) {
-            float4 q = *reinterpret_cast<const float4*>(part + o);
-            for (int sp = 1; sp < splits; ++sp) {
-                const float4 r = *reinterpret_cast<const float4*>(part + sp * split_stride + o);
-                q.x += r.x; q.y += r.y; q.z += r.z; q.w += r.w;
-            }
+        if constexpr (S > 0) {
+            float4 r[S];
+#pragma unroll
+            for (int sp = 0; sp < S; ++sp) r[sp] = *reinterpret_cast<const float4*>(part + sp * split_stride + o);
+            float4 q = r[0];
+#pragma unroll
+            for (int sp = 1; sp < S; ++sp) { q.x += r[sp].x; q.y += r[sp].y; q.z += r[sp].z; q.w += r[sp].w; }
             v[g][0] = bf16_to_f32(f32_to_bf16(q.x)); v[g][1] = bf16_to_f32(f32_to_bf16(q.y));
             v[g][2] = bf16_to_f32(f32_to_bf16(q.z)); v[g][3] = bf16_to_f32(f32_to_bf16(q.w));
         } else {
@@ -284,7 +296,14 @@ bool mix_norm_fits(int d) { return d % (kMixVec * 2) == 0 && d <= kThreads * kMi
 
 hipError_t launch_mix_norm(const float* part, int splits, int64_t split_stride, const uint16_t* src, int32_t T,
                            int d, float eps, uint16_t* h_out, uint16_t* u_out, hipStream_t s) {
-    mix_norm_kernel<<<T, kThreads, 0, s>>>(part, splits, split_stride, src, d, eps, h_out, u_out);
+    switch (splits) {
+        case 0: mix_norm_kernel<0><<<T, kThreads, 0, s>>>(part, split_stride, src, d, eps, h_out, u_out); break;
+        case 1: mix_norm_kernel<1><<<T, kThreads, 0, s>>>(part, split_stride, src, d, eps, h_out, u_out); break;
+        case 2: mix_norm_kernel<2><<<T, kThreads, 0, s>>>(part, split_stride, src, d, eps, h_out, u_out); break;
+        case 4: mix_norm_kernel<4><<<T, kThreads, 0, s>>>(part, split_stride, src, d, eps, h_out, u_out); break;
+        case 8: mix_norm_kernel<8><<<T, kThreads, 0, s>>>(part, split_stride, src, d, eps, h_out, u_out); break;
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
