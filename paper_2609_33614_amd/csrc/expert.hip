@@ -559,12 +559,12 @@ static int pick_nsub(int64_t T) {
 
 // Reduction-dimension slices of a stream launch: double them while the
 // number of 16-row wave tiles over the experts a call may be left with is
-// below EAT_SPLIT_WAVES.  Only K experts are counted (the union of a call
-// can be that small: EAT concentrates its picks), so short launches still
-// spread over the whole chip and end without a long tail.  Each slice costs
-// the combine one more fp32 row per assignment to read: calls whose union
-// really is K experts (EAT) gain from 4096, calls that touch every expert
-// (Top-K at B=64) would prefer 2048; the union is only known on the device.
+// below EAT_SPLIT_WAVES.  The union is only known on the device, so the host
+// counts the experts a call is expected to touch: in EAT mode only K (EAT
+// concentrates its picks, and short launches must still spread over the
+// whole chip and end without a long tail); with Top-K and Top-P routing
+// min(E, T K), since their tokens spread over the experts (each slice costs
+// the combine one more fp32 row per assignment to read).
 #ifndef EAT_SPLIT_WAVES
 #define EAT_SPLIT_WAVES 4096
 #endif
@@ -596,7 +596,8 @@ static int pick_nsub(int64_t T);
 static int stream_splits(int64_t rows_m, int kdim, const eat_params_t& p, int32_t T, int max_splits,
                          int64_t threshold) {
     const int64_t assign = std::max<int64_t>(1, static_cast<int64_t>(T) * p.top_k);
-    const int64_t active = std::min<int64_t>({static_cast<int64_t>(p.E), assign, static_cast<int64_t>(p.top_k)});
+    const int64_t active = std::min<int64_t>(
+        {static_cast<int64_t>(p.E), assign, p.mode == EAT_MODE_EAT ? static_cast<int64_t>(p.top_k) : assign});
     const int64_t bn = 16 * pick_nsub(T);
     const int64_t tiles = std::max<int64_t>(active, (assign + bn - 1) / bn);
     const int64_t waves = (rows_m / 16) * tiles;
