@@ -159,6 +159,14 @@ def test_stack_parity_layer_shape(mode):
     _run(mode, n_layers=2, d=2048, E=64, F=1024, B=64, steps=1, name="d2048")
 
 
+@pytest.mark.parametrize("d", [192, 384])
+def test_stack_parity_mixing_slices(d):
+    # d = 192 leaves the mixing GEMM one reduction slice and d = 384 two (the
+    # other cases take four or eight), so every instance of the split-summing
+    # RMSNorm pass runs; EAT, 3 layers, 2 steps
+    _run("eat", n_layers=3, d=d, E=16, F=128, B=32, steps=2, name=f"d{d}")
+
+
 def test_stack_reset_clears_every_layer():
     shape, w_host, mixes, stack, prms = _build("eat", 2, 256, 16, 128, 8)
     x = torch.from_numpy(HiddenStream(shape, 8, d=256).next()).view(torch.bfloat16).cuda()
