@@ -75,7 +75,7 @@ def widen(a: np.ndarray) -> np.ndarray:
     a = np.asarray(a)
     if a.dtype == np.uint16:
         return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
-    return a.astype(np.float64)
+    return np.asarray(a, dtype=np.float64)       # no copy when already float64
 
 
 # ------------------------------------------------------- router (Sec 3.1) --

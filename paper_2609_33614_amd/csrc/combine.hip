@@ -263,9 +263,14 @@ __global__ __launch_bounds__(kThreads) void mix_norm_kernel(const float* __restr
     }
 }
 
-__global__ __launch_bounds__(kWave) void reset_accounts_kernel(int E, int64_t* n, float* p, float* c) {
-    const int e = lane_id();
-    if (e < E) { n[e] = 0; p[e] = 0.f; c[e] = 0.f; }
+// One thread per expert, grid-stride, so every one of the E <= kMaxExperts
+// entries is cleared whatever the launch shape.
+__global__ __launch_bounds__(kThreads) void reset_accounts_kernel(int E, int64_t* n, float* p, float* c) {
+    for (int e = blockIdx.x * kThreads + threadIdx.x; e < E; e += gridDim.x * kThreads) {
+        n[e] = 0;
+        p[e] = 0.f;
+        c[e] = 0.f;
+    }
 }
 
 }  // namespace
@@ -308,7 +313,7 @@ hipError_t launch_mix_norm(const float* part, int splits, int64_t split_stride, 
 }
 
 hipError_t launch_reset_accounts(const eat_params_t& p, eat_accounts_t acc, hipStream_t s) {
-    reset_accounts_kernel<<<1, kWave, 0, s>>>(p.E, acc.n, acc.p_total, acc.c_s);
+    reset_accounts_kernel<<<(p.E + kThreads - 1) / kThreads, kThreads, 0, s>>>(p.E, acc.n, acc.p_total, acc.c_s);
     return hipGetLastError();
 }
 

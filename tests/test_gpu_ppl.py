@@ -106,15 +106,17 @@ def test_ppl_trend_drives_the_next_step():
     g = sig.trend.cpu().numpy()
     assert (g[keep] == trend_o[keep]).all()
     assert (trend_o[keep] > 0).any() and (trend_o[keep] < 0).any()
-    # the routed step: both sides use their own trend
+    # the routed step: the trend of a sequence whose perplexity change lies
+    # within the band may legitimately differ; there the oracle takes the
+    # GPU's (either value is a correct trend), everywhere else its own
+    trend_g = sig.trend.clone()
     mask = torch.empty(S, dtype=torch.int64, device="cuda")
-    lay.forward(torch.from_numpy(x2).view(torch.bfloat16).cuda(), trend=sig.trend.clone(), mask_out=mask)
+    lay.forward(torch.from_numpy(x2).view(torch.bfloat16).cuda(), trend=trend_g, mask_out=mask)
     torch.cuda.synchronize()
-    ref = O.moe_step(x2, wl, acc, trend_o, prm)
-    border = PT.borderline(ref.routing, prm)
-    gm = PT.masks_to_list(mask)
+    trend_use = np.where(keep, trend_o, trend_g.cpu().numpy()).astype(np.int8)
+    ref = O.moe_step(x2, wl, acc, trend_use, prm)
+    border, _ = PT.compare_masks("ppl -> routing", PT.masks_to_list(mask), ref.routing, prm, PT.EPS_B)
     cmp = keep & ~border
-    assert all(gm[t] == ref.routing.masks[t] for t in range(S) if cmp[t])
     assert cmp.mean() > 0.8
     PT.report("ppl -> routing", compared=int(cmp.sum()), rising=int((trend_o > 0).sum()))
     lay.close()
