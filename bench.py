@@ -162,7 +162,7 @@ def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bo
     torch.cuda.synchronize()
 
     stage = [None] * L.EAT_NUM_STAGE_EVENTS
-    evs = ev.create(3 * steps) if profile else []
+    evs = ev.create(4 * steps) if profile else []
     t0, t1 = ev.create(2)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
@@ -175,26 +175,68 @@ def run_mode(mode, shape, wdev, xs, B, steps, warmup, ev: HipEvents, profile: bo
             g.replay()
             masks[s].copy_(scratch)
         elif profile:
-            stage[L.EAT_STAGE_PERMUTED] = evs[3 * s]
-            stage[L.EAT_STAGE_UP] = evs[3 * s + 1]
-            stage[L.EAT_STAGE_DOWN] = evs[3 * s + 2]
+            stage[L.EAT_STAGE_BEGIN] = evs[4 * s + 3]
+            stage[L.EAT_STAGE_PERMUTED] = evs[4 * s]
+            stage[L.EAT_STAGE_UP] = evs[4 * s + 1]
+            stage[L.EAT_STAGE_DOWN] = evs[4 * s + 2]
             lay.forward(x, y=y, mask_out=masks[s], events=stage)
         else:
             lay.forward(x, y=y, mask_out=masks[s])
     ev.hip.hipEventRecord(t1, stream.cuda_stream)
     torch.cuda.synchronize()
     total_ms = ev.elapsed_ms(t0, t1)
-    up_ms = dn_ms = None
+    up_ms = dn_ms = step_ms = None
     if profile:
-        up_ms = np.array([ev.elapsed_ms(evs[3 * s], evs[3 * s + 1]) for s in range(steps)])
-        dn_ms = np.array([ev.elapsed_ms(evs[3 * s + 1], evs[3 * s + 2]) for s in range(steps)])
+        up_ms = np.array([ev.elapsed_ms(evs[4 * s], evs[4 * s + 1]) for s in range(steps)])
+        dn_ms = np.array([ev.elapsed_ms(evs[4 * s + 1], evs[4 * s + 2]) for s in range(steps)])
+        # a step runs from its first event to the next step's (the last one to the end event)
+        begins = [evs[4 * s + 3] for s in range(steps)] + [t1]
+        step_ms = np.array([ev.elapsed_ms(begins[s], begins[s + 1]) for s in range(steps)])
     m = masks.cpu().numpy().astype(np.int64).view(np.uint64)
     k = popcounts(m, W)
     U = union_sizes(m, W)
     acc = lay.accounts_host()
     del g
     lay.close()
-    return dict(total_ms=total_ms, up_ms=up_ms, dn_ms=dn_ms, k=k, U=U, E=E, accounts=acc)
+    return dict(total_ms=total_ms, up_ms=up_ms, dn_ms=dn_ms, step_ms=step_ms, k=k, U=U, E=E, accounts=acc,
+                masks=m, words=W)
+
+
+def routing_stats(res, K: int) -> dict:
+    """Routing statistics of a decode run: how many tokens activated each
+    number of experts, the tokens above the cap K (Eq. 6 keeps every exact
+    tie at the K-th value, so EAT may exceed K only on exact ties), each
+    expert's share of the (token, expert) assignments, and the experts
+    touched per step."""
+    k, m, W, E = res["k"], res["masks"], res["words"], res["E"]
+    hist = np.bincount(k.ravel())
+    load = np.zeros(E, dtype=np.int64)
+    for e in range(E):
+        word = m[..., e // 64] if W > 1 else m
+        load[e] = int(((word >> np.uint64(e % 64)) & np.uint64(1)).sum())
+    U = res["U"]
+    return {"k_histogram": {str(i): int(c) for i, c in enumerate(hist) if c},
+            "tokens_above_cap": int((k > K).sum()),
+            "expert_load_share": [round(float(v), 4) for v in load / max(1, load.sum())],
+            "experts_touched_min_mean_max": [int(U.min()), round(float(U.mean()), 3), int(U.max())]}
+
+
+def trajectory(res, B: int, first: int = 20, settle: int = 64) -> dict:
+    """Per-step view of a decode run from zero accounts: the experts touched
+    at every step, and tokens/s over the first `first` steps (the history
+    still building up) against the steps after `settle`."""
+    sm, U = res["step_ms"], res["U"]
+    n = len(sm)
+    out = {"steps": n, "experts_touched_per_step": [int(u) for u in U]}
+    f = min(first, n)
+    out[f"first_{f}_steps"] = {"tokens_per_s": round(B * f / (sm[:f].sum() / 1e3), 1),
+                               "ms_per_step": round(float(sm[:f].mean()), 4),
+                               "mean_experts_touched": round(float(U[:f].mean()), 3)}
+    if n > settle:
+        out[f"steps_{settle}_to_{n}"] = {"tokens_per_s": round(B * (n - settle) / (sm[settle:].sum() / 1e3), 1),
+                                          "ms_per_step": round(float(sm[settle:].mean()), 4),
+                                          "mean_experts_touched": round(float(U[settle:].mean()), 3)}
+    return out
 
 
 def run_prefill(shape_name: str, reps: int, ev: HipEvents, modes=("eat", "topk")):
@@ -414,30 +456,28 @@ def traffic_down(shape, k_row, U):
     return U * d * F * 2 + k_row.sum() * F * 2 + k_row.sum() * d * 4
 
 
-def measured_traffic(name: str):
-    """HBM bytes per launch of the dominant kernel from the committed counter
-    summary profiles/<name>.traffic.txt, or None when it is missing or was
-    measured on a different version of the expert kernel source."""
+def measured_traffic(prefix: str, batch: int, steps: int, warmup: int):
+    """HBM bytes per launch of the dominant kernel from a committed counter
+    summary profiles/<prefix>*.traffic.txt taken on a run with this batch and
+    these timed and warm-up steps (the experts a step touches, and so the
+    bytes per launch, depend on how far the account history has built up),
+    or None when there is none or it was measured on a different version of
+    the expert kernel source."""
+    import glob
     import hashlib
-    path = os.path.join(ROOT, "profiles", name + ".traffic.txt")
-    src = os.path.join(ROOT, "paper_2609_33614_amd", "csrc", "expert.hip")
-    if not os.path.exists(path):
-        return None
-    kv = dict(line.split(": ", 1) for line in open(path).read().splitlines() if ": " in line)
-    if kv.get("source_sha1") != hashlib.sha1(open(src, "rb").read()).hexdigest():
-        return None
-    return float(kv["traffic_bytes_per_launch"])
+    sha = hashlib.sha1(open(os.path.join(ROOT, "paper_2609_33614_amd", "csrc", "expert.hip"), "rb").read()).hexdigest()
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", prefix + "*.traffic.txt"))):
+        kv = dict(line.split(": ", 1) for line in open(path).read().splitlines() if ": " in line)
+        if (kv.get("source_sha1") == sha and kv.get("batch") == str(batch) and kv.get("steps") == str(steps)
+                and kv.get("warmup") == str(warmup)):
+            return float(kv["traffic_bytes_per_launch"])
+    return None
 
 
-def cpu_baseline(shape, w_host, xs_host, B, max_seconds: float):
-    """The oracle, unchanged, on the first steps of the same EAT workload."""
+def _oracle_rate(shape, w_host, xs_host, B, max_seconds: float):
+    """Steps of the oracle (unchanged) on the same EAT decode from zero
+    accounts until `max_seconds` have passed: (steps, seconds)."""
     import oracle as O
-    try:
-        from threadpoolctl import threadpool_info
-        blas = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
-        cores = int(max(blas)) if blas else 1
-    except Exception:
-        cores = 1
     prm = O.Params(mode=O.MODE_EAT, K=shape.K, inv_temp=shape.inv_temp)
     acc = O.zero_accounts(shape.E)
     t = time.time()
@@ -448,10 +488,28 @@ def cpu_baseline(shape, w_host, xs_host, B, max_seconds: float):
         n += 1
         if time.time() - t >= max_seconds or n >= xs_host.shape[0]:
             break
-    dt = time.time() - t
-    return {"value": round(n * B / dt, 3), "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{n} EAT decode step(s) of B={B} on the same layer and inputs "
-                      f"({n * B} tokens, {dt:.1f} s; numpy fp64, BLAS threads={cores})"}
+    return n, time.time() - t
+
+
+def cpu_baseline(shape, w_host, xs_host, B, max_seconds: float, single_seconds: float):
+    """The oracle, unchanged, on the first steps of the same EAT workload:
+    with the BLAS threads the host gives it, and again with one thread."""
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        blas = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+        cores = int(max(blas)) if blas else 1
+    except Exception:
+        threadpool_limits, cores = None, 1
+    n, dt = _oracle_rate(shape, w_host, xs_host, B, max_seconds)
+    out = {"value": round(n * B / dt, 3), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+           "sample": f"{n} EAT decode step(s) of B={B} on the same layer and inputs "
+                     f"({n * B} tokens, {dt:.1f} s; numpy fp64, BLAS threads={cores})"}
+    if threadpool_limits is not None and single_seconds > 0:
+        with threadpool_limits(limits=1, user_api="blas"):
+            n1, dt1 = _oracle_rate(shape, w_host, xs_host, B, single_seconds)
+        out["single_thread"] = {"value": round(n1 * B / dt1, 3), "unit": "tokens/s", "cores": 1,
+                                "sample": f"{n1} step(s), {n1 * B} tokens, {dt1:.1f} s, BLAS threads=1"}
+    return out
 
 
 def main(argv=None) -> int:
@@ -463,6 +521,8 @@ def main(argv=None) -> int:
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--cpu-single-seconds", type=float, default=10.0,
+                    help="seconds of the one-BLAS-thread oracle timing (0 = skip)")
     ap.add_argument("--modes", default="eat,topk,topp", help="routing modes to time (eat first)")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill (MFMA-bound) measurement")
     ap.add_argument("--prefill-reps", type=int, default=10)
@@ -473,6 +533,8 @@ def main(argv=None) -> int:
                     help="expert-weight layout of every timed layer (default: packed)")
     ap.add_argument("--no-wide-experts", action="store_true",
                     help="skip the decode of the 128-expert (Qwen3-30B-A3B-shaped) layer")
+    ap.add_argument("--no-trajectory", action="store_true",
+                    help="skip the 256-step EAT trajectory object (taken from the timed run when --steps >= 256)")
     ap.add_argument("--no-share", action="store_true",
                     help="skip the EAT decode under the C_s-share reading (cs_mode 1)")
     ap.add_argument("--no-decode-layers", action="store_true",
@@ -520,8 +582,9 @@ def main(argv=None) -> int:
     t = time.time()
     w_host = make_layer_weights(shape)
     wdev = device_weights(w_host)
-    log(f"weights ready in {time.time() - t:.1f} s; generating {W + K} steps of B={B}")
-    xs_host = HiddenStream(shape, B).steps(W + K)
+    TRAJ = 256                        # steps of the from-zero EAT trajectory object
+    log(f"weights ready in {time.time() - t:.1f} s; generating {W + max(K, TRAJ)} steps of B={B}")
+    xs_host = HiddenStream(shape, B).steps(W + max(K, TRAJ))
     xs = torch.from_numpy(xs_host).view(torch.bfloat16).cuda()
     ev = HipEvents()
 
@@ -545,6 +608,12 @@ def main(argv=None) -> int:
         if args.graph:
             log(f"timing {name}: {K} steps (+{W} warm-up), HIP graph replay")
             graphed[name] = run_mode(L.MODES[name], shape, wdev, xs, B, K, W, ev, profile=False, graph=True)
+    # the same EAT decode over 256 steps: how the step time follows the
+    # experts touched as the account history builds up
+    traj = results["eat"] if K >= TRAJ else None
+    if traj is None and not args.no_trajectory:
+        log(f"timing eat: {TRAJ} steps (+{W} warm-up) for the per-step trajectory")
+        traj = run_mode(L.MODES["eat"], shape, wdev, xs, B, TRAJ, W, ev, profile=True)
     share = None
     if not args.no_share:
         log(f"timing eat with the C_s-share reading: {K} steps (+{W} warm-up)")
@@ -567,7 +636,8 @@ def main(argv=None) -> int:
                 "mean_activated_experts": round(float(res["k"].mean()), 4),
                 "mean_experts_touched_per_step": round(float(res["U"].mean()), 3),
                 "up_gate_us_per_launch": round(float(res["up_ms"].mean() * 1e3), 2),
-                "down_us_per_launch": round(float(res["dn_ms"].mean() * 1e3), 2)}
+                "down_us_per_launch": round(float(res["dn_ms"].mean() * 1e3), 2),
+                "routing": routing_stats(res, shape.K)}
 
     sweep = []
     if not args.no_sweep:
@@ -618,7 +688,7 @@ def main(argv=None) -> int:
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
-        cpu = cpu_baseline(shape, w_host, xs_host[W:], B, args.cpu_seconds)
+        cpu = cpu_baseline(shape, w_host, xs_host[W:], B, args.cpu_seconds, args.cpu_single_seconds)
 
     out = {
         "metric": METRIC,
@@ -641,8 +711,7 @@ def main(argv=None) -> int:
         "roofline": {"bound": "hbm", "kernel": "expert up/gate (stream_kernel<gated>)",
                      "achieved": round(up_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(up_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("up_gate_mixtral_decode_b64_eat")
-                     if (B == 64 and K == 256 and W == 16) else None,
+                     "traffic": measured_traffic("up_gate_mixtral_decode_b64_eat", B, K, W),
                      "down_achieved": round(dn_gbs, 1),
                      "bytes_per_launch": round(float(up_bytes.mean()), 0),
                      "us_per_launch": round(float(r["up_ms"].mean() * 1e3), 2)},
@@ -650,6 +719,7 @@ def main(argv=None) -> int:
         "modes": {name: summary(res, graphed.get(name)) for name, res in results.items()},
         "eat_cs_share": dict(summary(share, None), reading="C_s enters S_h as C_s,i / sum C_s (cs_mode 1)")
         if share is not None else None,
+        "eat_trajectory": trajectory(traj, B) if traj is not None else None,
         "sweep": sweep,
         "prefill": prefill,
         "stack": stack,

@@ -3,10 +3,11 @@
 
 Inputs (directories written by the commands below, CSV output format):
   TRACE   rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run --
-              python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers --no-share --modes eat
+              python3 bench.py DECODE_ONLY --steps K --warmup W
   FETCH   rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH -o run --
-              python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers --no-share --modes eat --calibrate-copy 1024
+              python3 bench.py DECODE_ONLY --steps K --warmup W --calibrate-copy 1024
   WRITE   the same with --pmc WRITE_SIZE
+  with DECODE_ONLY = the flags in DECODE_ONLY below (the EAT decode alone)
 
 Writes profiles/<name>.md (kernel table, the dominant kernel's per-launch
 duration and HBM traffic) and profiles/<name>.traffic.txt (key: value lines
@@ -14,6 +15,9 @@ that bench.py reads for roofline.traffic, with the SHA-1 of the expert
 kernel source they were measured on).
 
     python profile_summary.py --trace T --fetch F --write W --bench-json B.json --name NAME
+
+The traffic file records the batch, timed steps and warm-up steps of the
+run; bench.py reports the figure only for a run with the same three.
 
 Prefill (MFMA-bound) summary of the wide tile kernels, from a trace of
 
@@ -41,6 +45,8 @@ import statistics
 ROOT = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_33614_amd", "csrc", "expert.hip")
 DOMINANT = "stream_kernel<true"
+DECODE_ONLY = ("--no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers "
+               "--no-share --no-trajectory --modes eat")
 COPY = "__amd_rocclr_copyBuffer"
 
 
@@ -172,7 +178,7 @@ def main(argv=None) -> int:
     ap.add_argument("--bench-json", required=True, help="JSON line printed by the traced bench run")
     ap.add_argument("--name", required=True)
     ap.add_argument("--copy-mib", type=int, default=1024)
-    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--steps", type=int, default=256, help="timed steps of the traced decode run")
     ap.add_argument("--prefill", action="store_true", help="summarise a prefill trace (wide tile kernels)")
     ap.add_argument("--reps", type=int, default=10, help="timed prefill calls in the traced run")
     ap.add_argument("--stack", action="store_true", help="summarise a stacked-layer decode trace")
@@ -210,14 +216,11 @@ def main(argv=None) -> int:
         f.write(f"Workload: {bench['config']['workload']}, batch {bench['config']['batch']}, "
                 f"{bench['steps']} timed steps (+{bench['warmup']} warm-up), MI355X.\n\n")
         f.write("Commands (from the repository root):\n\n```\n")
-        f.write("rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run -- "
-                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers --no-share --modes eat\n")
-        f.write("rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH -o run -- "
-                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers --no-share --modes eat "
-                "--calibrate-copy 1024\n")
-        f.write("rocprofv3 --pmc WRITE_SIZE --output-format csv -d WRITE -o run -- "
-                "python3 bench.py --no-sweep --no-cpu-baseline --no-prefill --no-stack --no-wide-experts --no-decode-layers --no-share --modes eat "
-                "--calibrate-copy 1024\n")
+        run = (f"python3 bench.py {DECODE_ONLY} --batch {bench['config']['batch']} --steps {bench['steps']} "
+               f"--warmup {bench['warmup']}")
+        f.write(f"rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run -- {run}\n")
+        f.write(f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH -o run -- {run} --calibrate-copy 1024\n")
+        f.write(f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d WRITE -o run -- {run} --calibrate-copy 1024\n")
         f.write(f"python3 profile_summary.py --trace TRACE --fetch FETCH --write WRITE "
                 f"--bench-json TRACED_BENCH.json --name {args.name}\n```\n\n")
         f.write("## Kernel time (rocprofv3 --stats, whole traced run incl. warm-up)\n\n")
@@ -239,7 +242,9 @@ def main(argv=None) -> int:
     with open(txt, "w") as f:
         f.write(f"kernel: {DOMINANT}\n")
         f.write(f"source_sha1: {source_sha1()}\n")
+        f.write(f"batch: {bench['config']['batch']}\n")
         f.write(f"steps: {len(timed)}\n")
+        f.write(f"warmup: {bench['warmup']}\n")
         f.write(f"fetch_factor: {f_fac:.6f}\n")
         f.write(f"write_factor: {w_fac:.6f}\n")
         f.write(f"fetch_bytes_per_launch: {fetch_b:.0f}\n")
