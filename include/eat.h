@@ -18,7 +18,9 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - Ownership: the caller owns every device buffer, including the account
- *    state and the workspace.  The library never allocates device memory.
+ *    state and the workspace.  No call allocates device memory; the only
+ *    device memory of the library's own is the fixed array that
+ *    eat_moe_forward_noalloc uses in place of a workspace.
  *  - Asynchrony: every call that takes a stream only enqueues kernels on it
  *    and returns; inputs must stay alive and unmodified until the stream
  *    has passed the enqueued work.  No call synchronises the device.
@@ -69,7 +71,9 @@ typedef enum {
     EAT_ERR_UNSUPPORTED = 2,   /* a shape or dtype outside the limits above   */
     EAT_ERR_WORKSPACE = 3,     /* workspace missing or smaller than required  */
     EAT_ERR_HIP = 4,           /* a HIP runtime call or kernel launch failed  */
-    EAT_ERR_INTERNAL = 5
+    EAT_ERR_INTERNAL = 5,
+    EAT_ERR_SCRATCH_LIMIT = 6  /* eat_moe_forward_noalloc: the call needs more
+                                  than EAT_NOALLOC_SCRATCH_BYTES              */
 } eat_status_t;
 
 typedef enum {
@@ -348,6 +352,36 @@ eat_status_t eat_ppl_trend(const void* h, int32_t S, int32_t d, const void* w_vo
  * Enqueues on `stream` only.  Errors: EAT_ERR_INVALID_ARG, EAT_ERR_HIP. */
 eat_status_t eat_pack_weights(const void* src, int32_t groups, int32_t M, int32_t K, void* dst,
                               hipStream_t stream);
+
+/* ---- allocation-free forward -----------------------------------------------
+ *
+ * For callers that cannot allocate device memory at call time: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * eat_moe_forward_noalloc is eat_moe_forward (same arguments, results
+ * bit-identical to it) without the workspace arguments: its intermediates
+ * live in a fixed device array of EAT_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every GPU it runs this entry point on, until the process
+ * ends.  The caller still owns and passes every input, output and the
+ * account state.  The call allocates and frees nothing; the array's device
+ * address is looked up once per device, on the first call with that device
+ * current (make that first call outside graph capture).
+ *   Limit: a call whose eat_workspace_size(h, T) exceeds
+ *   EAT_NOALLOC_SCRATCH_BYTES returns EAT_ERR_SCRATCH_LIMIT and enqueues
+ *   nothing (e.g. the Mixtral-shaped EAT layer fits up to T = 64 tokens).
+ *   Sharing: every call on one GPU uses that GPU's one array, and no part
+ *   of it needs clearing (each call writes every byte it reads first), so
+ *   consecutive calls are independent; calls whose executions overlap on
+ *   one GPU (different streams without ordering, several host threads)
+ *   race on the array and give undefined results: order them on one stream.
+ * Errors: as eat_moe_forward, plus EAT_ERR_SCRATCH_LIMIT; EAT_ERR_HIP if the
+ * device or the array's address cannot be obtained or a launch fails. */
+#define EAT_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+
+eat_status_t eat_moe_forward_noalloc(eat_handle_t h, const void* x, int32_t T, const float* w_router,
+                                     const void* w1, const void* w3, const void* w2,
+                                     const void* ws1, const void* ws3, const void* ws2,
+                                     eat_accounts_t acc, const int8_t* ppl_trend, void* y,
+                                     uint64_t* mask_out, int32_t* expert_load_out, hipStream_t stream);
 
 /* Static description of a status code (never NULL). */
 const char* eat_status_string(eat_status_t s);

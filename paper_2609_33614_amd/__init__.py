@@ -9,4 +9,5 @@ from ._lib import (  # noqa: F401
     eat_params_t, eat_reset_accounts, eat_route, eat_route_workspace_size, eat_stack_forward, eat_stack_layer_t,
     eat_stack_workspace_size, eat_status_string, eat_workspace_size, load, stack_layers, eat_ppl_workspace_size,
     eat_ppl_reset, eat_ppl_trend, EAT_LAYOUT_PACKED, EAT_LAYOUT_ROWS, eat_pack_weights, mask_words,
+    eat_moe_forward_noalloc, EAT_NOALLOC_SCRATCH_BYTES,
 )

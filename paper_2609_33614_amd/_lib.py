@@ -14,7 +14,9 @@ from typing import Optional
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("EAT_LIB_PATH") or os.path.join(_HERE, "libeat.so")
 
-EAT_OK, EAT_ERR_INVALID_ARG, EAT_ERR_UNSUPPORTED, EAT_ERR_WORKSPACE, EAT_ERR_HIP, EAT_ERR_INTERNAL = range(6)
+(EAT_OK, EAT_ERR_INVALID_ARG, EAT_ERR_UNSUPPORTED, EAT_ERR_WORKSPACE, EAT_ERR_HIP, EAT_ERR_INTERNAL,
+ EAT_ERR_SCRATCH_LIMIT) = range(7)
+EAT_NOALLOC_SCRATCH_BYTES = 256 << 20      # include/eat.h
 EAT_MODE_EAT, EAT_MODE_TOPK, EAT_MODE_TOPP = 0, 1, 2
 EAT_F32, EAT_BF16 = 0, 1
 EAT_LAYOUT_ROWS, EAT_LAYOUT_PACKED = 0, 1
@@ -86,12 +88,14 @@ def load() -> C.CDLL:
         lib.eat_ppl_trend.argtypes = [P, C.c_int32, C.c_int32, P, C.c_int32, P, P, P, P, P, P, P, C.c_size_t, P]
     if hasattr(lib, "eat_pack_weights"):
         lib.eat_pack_weights.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, P, P]
+    if hasattr(lib, "eat_moe_forward_noalloc"):
+        lib.eat_moe_forward_noalloc.argtypes = lib.eat_moe_forward.argtypes[:15] + [P]
     lib.eat_status_string.argtypes = [C.c_int]
     lib.eat_status_string.restype = C.c_char_p
     for name in ("eat_params_default", "eat_create", "eat_destroy", "eat_workspace_size", "eat_route_workspace_size",
                  "eat_reset_accounts", "eat_route", "eat_moe_forward", "eat_moe_forward_profiled",
                  "eat_stack_workspace_size", "eat_stack_forward", "eat_ppl_workspace_size", "eat_ppl_reset",
-                 "eat_ppl_trend", "eat_pack_weights"):
+                 "eat_ppl_trend", "eat_pack_weights", "eat_moe_forward_noalloc"):
         if hasattr(lib, name):
             getattr(lib, name).restype = st
     _lib = lib
@@ -207,6 +211,14 @@ def eat_moe_forward_profiled(handle: int, x, T: int, w_router, w1, w3, w2, ws1, 
                                            _ptr(y), _ptr(mask_out), _ptr(expert_load_out), _ptr(ws),
                                            int(ws_bytes), _stream(stream), arr, len(events)),
            "eat_moe_forward_profiled")
+
+
+def eat_moe_forward_noalloc(handle: int, x, T: int, w_router, w1, w3, w2, ws1, ws3, ws2, acc: eat_accounts_t,
+                            ppl_trend, y, mask_out, expert_load_out, stream=None) -> None:
+    _check(load().eat_moe_forward_noalloc(handle, _ptr(x), int(T), _ptr(w_router), _ptr(w1), _ptr(w3), _ptr(w2),
+                                          _ptr(ws1), _ptr(ws3), _ptr(ws2), acc, _ptr(ppl_trend), _ptr(y),
+                                          _ptr(mask_out), _ptr(expert_load_out), _stream(stream)),
+           "eat_moe_forward_noalloc")
 
 
 def stack_layers(entries) -> "C.Array":

@@ -31,7 +31,8 @@ CFLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", os.path.join(ROOT, "include"),
 ]
-SOURCES = ["api.cpp", "route.hip", "permute.hip", "expert.hip", "wide.hip", "combine.hip", "ppl.hip", "pack.hip"]
+SOURCES = ["api.cpp", "route.hip", "permute.hip", "expert.hip", "wide.hip", "combine.hip", "ppl.hip", "pack.hip",
+           "noalloc.hip"]
 
 
 def _compile(src: str, extra=(), tag: str = "") -> str:

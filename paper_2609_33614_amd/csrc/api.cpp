@@ -199,7 +199,7 @@ eat_status_t eat_route(eat_handle_t h, const void* x, int32_t T, const float* w_
 
 }  // extern "C"
 
-namespace {
+namespace eat {
 
 // Argument checks shared by the forward entry points (host only).
 eat_status_t check_forward(const eat_ctx* h, const void* x, int32_t T, const float* w_router, const void* w1,
@@ -299,6 +299,13 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
     mark(EAT_STAGE_END);
     return e;
 }
+
+}  // namespace eat
+
+namespace {
+
+using eat::check_forward;
+using eat::forward_impl;
 
 // Stacked-layer workspace: the largest layer workspace, then u, r and two
 // h rows (bf16 [T][d] each), then the mixing GEMM's fp32 slices.
@@ -501,6 +508,7 @@ const char* eat_status_string(eat_status_t s) {
         case EAT_ERR_WORKSPACE: return "workspace missing or too small";
         case EAT_ERR_HIP: return "HIP runtime error";
         case EAT_ERR_INTERNAL: return "internal error";
+        case EAT_ERR_SCRATCH_LIMIT: return "call needs more than the allocation-free entry point's fixed scratch";
     }
     return "unknown status";
 }

@@ -160,6 +160,20 @@ int ppl_splits(int32_t S, int d, int V);
 int ppl_chunks(int V);                 // (max, sum) pairs per row in `part`
 hipError_t launch_ppl_reset(int32_t S, double* nll_sum, int32_t* count, double* ppl_prev, hipStream_t s);
 
+// Forward entry points (api.cpp): host-side argument checks, and the
+// enqueue of one layer forward into a workspace of plan_workspace(h, T).total
+// bytes at `ws` (arguments checked, T > 0).  `residual` (bf16 [T][d] or
+// null) is added to y; `prob_out` (or null) receives the router probabilities.
+eat_status_t check_forward(const eat_ctx* h, const void* x, int32_t T, const float* w_router, const void* w1,
+                           const void* w3, const void* w2, const void* ws1, const void* ws3, const void* ws2,
+                           const eat_accounts_t& acc, const void* y, const uint64_t* mask_out,
+                           const int32_t* expert_load_out);
+hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float* w_router, const void* w1,
+                        const void* w3, const void* w2, const void* ws1, const void* ws3, const void* ws2,
+                        eat_accounts_t acc, const int8_t* ppl_trend, const uint16_t* residual, void* y,
+                        uint64_t* mask_out, int32_t* expert_load_out, float* prob_out, void* ws,
+                        hipStream_t stream, const hipEvent_t* events, int32_t n_events);
+
 hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets,
                                   const int32_t* tok_idx, const float* prob, const float* nrm2,
                                   eat_accounts_t acc, hipStream_t s);

@@ -207,6 +207,34 @@ def test_forward_validation_happens_on_the_host():
         eat.eat_destroy(h)
 
 
+def test_noalloc_forward_validation_happens_on_the_host():
+    """The allocation-free forward checks its arguments like eat_moe_forward
+    and rejects a call that needs more than its fixed scratch array, all on
+    the host before any HIP call."""
+    def noalloc(h, **kw):
+        args = dict(x=FAKE, T=4, w_router=FAKE, w1=FAKE, w3=FAKE, w2=FAKE, ws1=None, ws3=None, ws2=None,
+                    acc=L.accounts(FAKE, FAKE, FAKE), ppl_trend=None, y=FAKE, mask_out=None, expert_load_out=None,
+                    stream=0)
+        args.update(kw)
+        eat.eat_moe_forward_noalloc(h, **args)
+
+    # the fine-grained EAT layer at 256 tokens needs ~545 MB: above the limit
+    p = _params(E=64, d_model=2048, d_ffn=1024, top_k=8, act_dtype=eat.EAT_BF16, expert_dtype=eat.EAT_BF16)
+    h = eat.eat_create(p, 256)
+    try:
+        assert eat.eat_workspace_size(h, 256) > eat.EAT_NOALLOC_SCRATCH_BYTES
+        assert eat.eat_workspace_size(h, 16) <= eat.EAT_NOALLOC_SCRATCH_BYTES
+        for kw, status in [(dict(T=256), L.EAT_ERR_SCRATCH_LIMIT), (dict(x=None), L.EAT_ERR_INVALID_ARG),
+                           (dict(y=FAKE + 4), L.EAT_ERR_INVALID_ARG), (dict(T=257), L.EAT_ERR_INVALID_ARG),
+                           (dict(acc=L.accounts(FAKE, None, FAKE)), L.EAT_ERR_INVALID_ARG)]:
+            with pytest.raises(eat.EatError) as ei:
+                noalloc(h, **kw)
+            assert ei.value.status == status, kw
+        noalloc(h, T=0)                  # an empty call is valid and launches nothing
+    finally:
+        eat.eat_destroy(h)
+
+
 def test_shared_expert_pointers_required_when_declared():
     h = eat.eat_create(_params(d_shared=128), 8)
     try:
