@@ -87,6 +87,7 @@ Workspace plan_workspace(const eat_ctx& c, int32_t T) {
     w.ys = take(p.d_shared ? t * p.d_model * 4 : 0);
     w.gus = take(w.shared_up_splits > 1 ? 2 * static_cast<size_t>(w.shared_up_splits) * t * p.d_shared * 4 : 0);
     w.ysp = take(w.shared_splits > 1 ? static_cast<size_t>(w.shared_splits) * t * p.d_model * 4 : 0);
+    w.sync = take(static_cast<size_t>(kSyncWords) * 4);
     w.total = off;
     return w;
 }
@@ -251,6 +252,9 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
     b.ys = reinterpret_cast<float*>(base + w.ys);
     b.gus = reinterpret_cast<float*>(base + w.gus);
     b.ysp = reinterpret_cast<float*>(base + w.ysp);
+    b.sync = reinterpret_cast<unsigned*>(base + w.sync);
+    int32_t* const up_splits_dev = reinterpret_cast<int32_t*>(b.sync);
+    int32_t* const down_splits_dev = reinterpret_cast<int32_t*>(b.sync + 1);
 
     hipError_t e = hipSuccess;
     auto mark = [&](int stage) {
@@ -264,12 +268,13 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
         e = eat::launch_permute(p, T, b.mask, b.offsets, b.tok_idx, b.inv, b.row_expert, expert_load_out,
                                 stream);
     mark(EAT_STAGE_PERMUTED);
+    const bool bf16 = p.expert_dtype == EAT_BF16;
     if (e == hipSuccess) {
-        if (p.expert_dtype == EAT_BF16)
+        if (bf16)
             e = eat::launch_experts_bf16(p, T, w.rows, static_cast<const uint16_t*>(x),
                                          static_cast<const uint16_t*>(w1), static_cast<const uint16_t*>(w3),
                                          static_cast<const uint16_t*>(w2), b.offsets, b.tok_idx,
-                                         static_cast<uint16_t*>(b.h), b.gu, b.yp, stream,
+                                         static_cast<uint16_t*>(b.h), b.gu, b.yp, up_splits_dev, down_splits_dev, stream,
                                          [&]() { mark(EAT_STAGE_UP); });
         else
             e = eat::launch_experts_f32(p, T, w.rows, static_cast<const float*>(x),
@@ -280,7 +285,7 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
     mark(EAT_STAGE_DOWN);
     const bool shared = p.d_shared > 0;
     if (e == hipSuccess && shared) {
-        if (p.expert_dtype == EAT_BF16)
+        if (bf16)
             e = eat::launch_shared_bf16(p, T, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(ws1),
                                         static_cast<const uint16_t*>(ws3), static_cast<const uint16_t*>(ws2),
                                         static_cast<uint16_t*>(b.hs), b.ys, b.gus, b.ysp, stream);
@@ -290,9 +295,11 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
                                        static_cast<float*>(b.hs), b.ys, stream);
     }
     mark(EAT_STAGE_SHARED);
+    // the down projection's slices: chosen on the device when it could take several
+    const int32_t* splits_dev = bf16 && w.splits > 1 ? down_splits_dev : nullptr;
     if (e == hipSuccess)
         e = eat::launch_combine(p, T, b.mask, b.gate, b.inv, b.yp, shared ? b.ys : nullptr, residual, y, b.nrm2,
-                                w.splits, w.rows * p.d_model, stream);
+                                w.splits, w.rows * p.d_model, splits_dev, stream);
     mark(EAT_STAGE_COMBINED);
     if (e == hipSuccess && p.mode == EAT_MODE_EAT)
         e = eat::launch_update_accounts(p, b.offsets, b.tok_idx, b.prob, b.nrm2, acc, stream);

@@ -11,11 +11,14 @@
 // split partials) and the next layer's input u = bf16(h' / rms(h')), one
 // workgroup per token.
 //
-// accounts: one workgroup per expert reduces its contiguous row segment in fp64
-// and applies the Sec. 3.2 bookkeeping once per call:
+// accounts: the Sec. 3.2 bookkeeping once per call, each expert's contiguous
+// row segment reduced in fp64:
 //   N += n_e,  P_total += sum of the rows' router probabilities,
 //   C_s = (1 - alpha) C_s + alpha * mean row norm,
 // each row norm being sqrt of its slices' sums of squares added in order.
+// (Doing it in the combine's last workgroup to finish instead of a kernel of
+// its own needs a device-wide release in every combine workgroup, an L2
+// write-back on this part: measured slower at every decode size.)
 #include <math.h>
 
 #include "eat_device.h"
@@ -32,6 +35,7 @@ struct CombineArgs {
     const float* gate;
     const int32_t* inv;
     const float* yp;           // [splits][rows_cap][d]
+    const int32_t* splits_dev; // slices the down projection took (device), or null: `splits`
     const float* ys;           // [T][d] shared output or null
     const uint16_t* res;       // [T][d] bf16 residual rows added to y, or null
     void* y;
@@ -54,6 +58,10 @@ template <typename YT>
 __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     __shared__ float red[kBatch][kWaves];
     const int t = blockIdx.x, chunk = blockIdx.y;
+    // an unconditional load (from a stand-in address when the count is the
+    // host's), issued with the mask load below and waited for once
+    const int sdev = *(a.splits_dev ? a.splits_dev : reinterpret_cast<const int32_t*>(a.mask));
+    const int splits = a.splits_dev ? sdev : a.splits;
     const int lane = lane_id(), wave = threadIdx.x / kWave;
     const int j = chunk * kThreads + threadIdx.x;      // float4 index within the row
     const bool on = 4 * j < a.d;
@@ -97,7 +105,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
             const float* src = a.yp + static_cast<int64_t>(row) * a.d + 4 * jc;
 #pragma unroll
             for (int sp = 0; sp < kMaxSplits; ++sp)
-                if (sp < a.splits) dst[sp] = *reinterpret_cast<const float4*>(src + sp * a.split_stride);
+                if (sp < splits) dst[sp] = *reinterpret_cast<const float4*>(src + sp * a.split_stride);
         };
         issue(q[0], rows[0]);
         float ss[kBatch];
@@ -110,7 +118,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
                 float4 o = c[0];
 #pragma unroll
                 for (int sp = 1; sp < kMaxSplits; ++sp)
-                    if (sp < a.splits) { o.x += c[sp].x; o.y += c[sp].y; o.z += c[sp].z; o.w += c[sp].w; }
+                    if (sp < splits) { o.x += c[sp].x; o.y += c[sp].y; o.z += c[sp].z; o.w += c[sp].w; }
                 if (on) {
                     ss[b] = fmaf(o.x, o.x, ss[b]); ss[b] = fmaf(o.y, o.y, ss[b]);
                     ss[b] = fmaf(o.z, o.z, ss[b]); ss[b] = fmaf(o.w, o.w, ss[b]);
@@ -140,25 +148,26 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
         __syncthreads();
         if (nb < kBatch) break;
     }
-    if (!on) return;
-    if (a.ys) {
-        const float4 q = ysv;
-        acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
-    }
-    if (a.res) {
-        const uint2 q = rsv;
-        acc.x += bf16_to_f32(static_cast<uint16_t>(q.x & 0xffffu));
-        acc.y += bf16_to_f32(static_cast<uint16_t>(q.x >> 16));
-        acc.z += bf16_to_f32(static_cast<uint16_t>(q.y & 0xffffu));
-        acc.w += bf16_to_f32(static_cast<uint16_t>(q.y >> 16));
-    }
-    if constexpr (sizeof(YT) == 4) {
-        *reinterpret_cast<float4*>(static_cast<float*>(a.y) + static_cast<size_t>(t) * a.d + 4 * j) = acc;
-    } else {
-        uint2 pk;
-        pk.x = static_cast<uint32_t>(f32_to_bf16(acc.x)) | (static_cast<uint32_t>(f32_to_bf16(acc.y)) << 16);
-        pk.y = static_cast<uint32_t>(f32_to_bf16(acc.z)) | (static_cast<uint32_t>(f32_to_bf16(acc.w)) << 16);
-        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.y) + static_cast<size_t>(t) * a.d + 4 * j) = pk;
+    if (on) {
+        if (a.ys) {
+            const float4 q = ysv;
+            acc.x += q.x; acc.y += q.y; acc.z += q.z; acc.w += q.w;
+        }
+        if (a.res) {
+            const uint2 q = rsv;
+            acc.x += bf16_to_f32(static_cast<uint16_t>(q.x & 0xffffu));
+            acc.y += bf16_to_f32(static_cast<uint16_t>(q.x >> 16));
+            acc.z += bf16_to_f32(static_cast<uint16_t>(q.y & 0xffffu));
+            acc.w += bf16_to_f32(static_cast<uint16_t>(q.y >> 16));
+        }
+        if constexpr (sizeof(YT) == 4) {
+            *reinterpret_cast<float4*>(static_cast<float*>(a.y) + static_cast<size_t>(t) * a.d + 4 * j) = acc;
+        } else {
+            uint2 pk;
+            pk.x = static_cast<uint32_t>(f32_to_bf16(acc.x)) | (static_cast<uint32_t>(f32_to_bf16(acc.y)) << 16);
+            pk.y = static_cast<uint32_t>(f32_to_bf16(acc.z)) | (static_cast<uint32_t>(f32_to_bf16(acc.w)) << 16);
+            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.y) + static_cast<size_t>(t) * a.d + 4 * j) = pk;
+        }
     }
 }
 
@@ -279,11 +288,14 @@ int combine_chunks(const eat_params_t& p) { return (p.d_model / 4 + kThreads - 1
 
 hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask, const float* gate,
                           const int32_t* inv, const float* yp, const float* ys, const uint16_t* residual,
-                          void* y, float* nrm2, int splits, int64_t split_stride, hipStream_t s) {
+                          void* y, float* nrm2, int splits, int64_t split_stride, const int32_t* splits_dev,
+                          hipStream_t s) {
     if (splits < 1 || splits > kMaxSplits) return hipErrorInvalidValue;
     const int nchunk = combine_chunks(p);
-    CombineArgs a{mask,   gate,   inv, yp,  ys,        residual, y,     nrm2, split_stride,
-                  splits, T,      p.E, p.d_model, nchunk, mask_words(p.E)};
+    CombineArgs a{};
+    a.mask = mask; a.gate = gate; a.inv = inv; a.yp = yp; a.splits_dev = splits_dev; a.ys = ys; a.res = residual;
+    a.y = y; a.nrm2 = nrm2; a.split_stride = split_stride; a.splits = splits; a.T = T; a.E = p.E; a.d = p.d_model;
+    a.nchunk = nchunk; a.words = mask_words(p.E);
     const dim3 grid(T, nchunk);
     if (p.act_dtype == EAT_BF16) combine_kernel<uint16_t><<<grid, kThreads, 0, s>>>(a);
     else combine_kernel<float><<<grid, kThreads, 0, s>>>(a);

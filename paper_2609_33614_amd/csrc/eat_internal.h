@@ -25,8 +25,13 @@ inline int mask_words(int E) { return (E + 63) / 64; }
 
 // Offsets (bytes) of the workspace regions for T tokens.  Every region
 // starts on a 256-byte boundary.
+// Small values the kernels of one call hand to each other (workspace region
+// `sync`, kSyncWords words): [0] the slices the routed up/gate projection
+// took, [1] the slices the down projection took.
+constexpr int kSyncWords = 2;
+
 struct Workspace {
-    size_t lpart, prob, gate, mask, k, offsets, tok_idx, inv, row_expert, h, gu, yp, nrm, hs, ys, gus, ysp;
+    size_t lpart, prob, gate, mask, k, offsets, tok_idx, inv, row_expert, h, gu, yp, nrm, hs, ys, gus, ysp, sync;
     size_t route_total;      // bytes eat_route needs (the leading lpart region)
     size_t total;
     int64_t rows;            // capacity in (token, expert) rows = T * kmax
@@ -56,6 +61,7 @@ struct Buffers {
     float* ys;               // [T][d] shared-expert output
     float* gus;              // [2][shared_up_splits][T][F_sh] its gate / up partial sums
     float* ysp;              // [shared_splits][T][d] its down-projection partial sums
+    unsigned* sync;          // kSyncWords words (see above)
 };
 
 // ---- launchers (return hipGetLastError() after enqueueing) -------------
@@ -83,12 +89,15 @@ hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap
                               const int32_t* row_expert, float* h, float* yp, hipStream_t s,
                               const std::function<void()>& between);
 
-// bf16 weights and activations: MFMA kernels.
+// bf16 weights and activations: MFMA kernels.  Both projections choose
+// their slices on the device and write the count they took to
+// *up_splits_dev / *down_splits_dev (read by the up/gate slice reduce and
+// by the combine).
 hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_cap,
                                const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
                                const uint16_t* w2, const int32_t* offsets, const int32_t* tok_idx,
-                               uint16_t* h, float* gu, float* yp, hipStream_t s,
-                               const std::function<void()>& between);
+                               uint16_t* h, float* gu, float* yp, int32_t* up_splits_dev, int32_t* down_splits_dev,
+                               hipStream_t s, const std::function<void()>& between);
 
 // Always-on shared expert over all T tokens.
 hipError_t launch_shared_f32(const eat_params_t& p, int32_t T, const float* x, const float* ws1,
@@ -103,13 +112,14 @@ hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* 
                               const uint16_t* ws1, const uint16_t* ws3, const uint16_t* ws2,
                               uint16_t* hs, float* ys, float* gus, float* ysp, hipStream_t s);
 
-// yp holds `splits` partial slices of the down projection, `split_stride`
-// floats apart; they are added in slice order.  `residual` (bf16 [T][d], or
-// null) is added to y before the cast.
+// yp holds the down projection's partial slices, `split_stride` floats
+// apart (*splits_dev of them when set, else `splits`); they are added in
+// slice order.  `residual` (bf16 [T][d], or null) is added to y before the
+// cast.
 hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask,
                           const float* gate, const int32_t* inv, const float* yp,
                           const float* ys, const uint16_t* residual, void* y, float* nrm2,
-                          int splits, int64_t split_stride, hipStream_t s);
+                          int splits, int64_t split_stride, const int32_t* splits_dev, hipStream_t s);
 
 // Between stacked layers (combine.hip): h = bf16(sum of `splits` fp32
 // partial rows, or the bf16 rows of src when splits == 0), written to h_out

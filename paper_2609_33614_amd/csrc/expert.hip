@@ -8,8 +8,13 @@
 // the whole reduction dimension once, applying them to up to 16*NSUB
 // tokens of the same expert (the B operand, zero-padded).  Weight bytes are
 // read from HBM exactly once per token tile, which is what bounds decode.
-// The down projection may split its reduction dimension into slices;
-// the partial tiles are added, in split order, by the combine kernel.
+// Either projection may split its reduction dimension into slices, as many
+// as the tiles in use call for (chosen on the device from the tile count,
+// which only the device knows): the down projection's partial tiles are
+// added, in split order, by the combine kernel; the up/gate projection's by
+// a reduce kernel that then forms H = silu(G) * U.  (Adding them up inside
+// the projection, by the last slice of a tile to finish, needs a device-wide
+// release per work item, an L2 write-back on this part: measured slower.)
 // The grid is persistent: a flat list of (token tile, slice, row block)
 // work items over about as many workgroups as the chip keeps resident.
 // Weights may be in the packed layout (pack.hip), read one contiguous
@@ -95,6 +100,51 @@ hipError_t launch_f32_pair(F32Args a, int64_t rows_cap, hipStream_t s,
 
 // ------------------------------------------------------- bf16 streaming --
 
+// Reduction-dimension slices of a stream launch (split_rule): double them
+// while the number of 16-row wave tiles over the token tiles in use is below
+// a threshold.  The tiles in use (the experts a call's tokens touch) are
+// only known on the device, so the kernel applies the rule itself; the host
+// sizes the workspace for the most slices the rule can give.  Each slice
+// costs one more fp32 row per assignment in the partial buffers.
+#ifndef EAT_SPLIT_WAVES
+#define EAT_SPLIT_WAVES 4096
+#endif
+// Once the grid holds ~1024 wave tiles, a slice keeps at least
+// EAT_SPLIT_MIN_K reduction elements: shorter ones cost more in partial rows
+// than their extra waves gain (measured: 4 slices of a 1024-wide down
+// projection over 8 experts are slower than 2); smaller grids split down
+// to 128 (the same projection over 2 experts gains from 4 slices).
+#ifndef EAT_SPLIT_MIN_K
+#define EAT_SPLIT_MIN_K 384
+#endif
+// The gated projection pays for its slices with fp32 partials that the last
+// slice adds up, so it only splits grids that would leave most of the chip
+// idle.
+#ifndef EAT_UP_SPLIT_WAVES
+#define EAT_UP_SPLIT_WAVES 1024
+#endif
+// With 128-token tiles (calls of more than 64 tokens) an expert's tile is a
+// small prefill, and up to 2048 waves pay: the fine-grained layer's 256-token
+// EAT decode (~8 experts of ~256 tokens) +14%, Top-K unchanged; 1024 stays
+// for smaller tiles (the Mixtral-shaped 64-token decode loses 10% at 2048).
+#ifndef EAT_UP_SPLIT_WAVES_T128
+#define EAT_UP_SPLIT_WAVES_T128 2048
+#endif
+#ifndef EAT_UP_SPLIT_MAX
+#define EAT_UP_SPLIT_MAX 4
+#endif
+
+__host__ __device__ inline int split_rule(int64_t rows_m, int kdim, int64_t tiles, int max_splits,
+                                          int64_t threshold) {
+    const int64_t waves = (rows_m / 16) * tiles;
+    int s = 1;
+    while (s < max_splits && kdim % (64 * 2 * s) == 0 && waves * s < threshold &&
+           kdim / (2 * s) >= (waves * s < 1024 ? 128 : EAT_SPLIT_MIN_K))
+        s *= 2;
+    return s;
+}
+
+
 struct StreamArgs {
     const uint16_t* wa;        // [groups][M][K]  (W1 for up/gate, W2 for down)
     const uint16_t* wb;        // [groups][M][K]  (W3, gated kernel only)
@@ -103,13 +153,15 @@ struct StreamArgs {
     const int32_t* offsets;    // [groups+1] expert-major row offsets, or null
     int nrows;                 // rows of the single group when offsets is null
     int groups, M, K;
-    int splits;                // slices of the reduction dimension
-    int ksplit;                // reduction length per slice
+    int splits;                // slices of the reduction dimension; with rule_threshold > 0
+                               // the most the device-side choice may take
+    int64_t rule_threshold;    // > 0: the slices follow split_rule over the tiles in use
+    int32_t* splits_out;       // the slices taken, written by workgroup 0 (or null)
     int64_t split_stride;      // elements between split slices of out / out2
-    void* out;                 // gated: bf16 H [rows][M], or fp32 G partials
-                               // [split][rows][M] when `partial`; plain: fp32 [split][rows][M]
-    float* out2;               // gated + partial: fp32 U partials [split][rows][M]
-    int partial;               // gated: write G/U partial sums instead of H
+    void* out;                 // plain: fp32 [split][rows][M]; gated: fp32 G partials
+                               // [split][rows][M] (used when more than one slice)
+    float* out2;               // gated: fp32 U partials [split][rows][M]
+    uint16_t* h;               // gated: bf16 H [rows][M] (written here when one slice is taken)
 };
 
 __device__ __forceinline__ bf16x8 ld16(const uint16_t* p) {
@@ -125,6 +177,22 @@ __device__ __forceinline__ bf16x8 ld16_stream(const uint16_t* p) {
     return __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(p));
 }
 
+// Slices the gated projection may use (the last slice reads the others'
+// partials into registers).
+constexpr int kMaxUpSplits = EAT_UP_SPLIT_MAX;
+
+
+// H = bf16(silu(G) * U) for a lane's 4 consecutive features.
+__device__ __forceinline__ void store_h(uint16_t* dst, const f32x4& gsum, const f32x4& usum) {
+    uint16_t hv[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) hv[q] = f32_to_bf16(silu(gsum[q]) * usum[q]);
+    uint2 pk;
+    pk.x = static_cast<uint32_t>(hv[0]) | (static_cast<uint32_t>(hv[1]) << 16);
+    pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
+    *reinterpret_cast<uint2*>(dst) = pk;
+}
+
 // One workgroup = WPB waves = 16 WPB consecutive weight rows (16 per wave) of one
 // expert, applied to one tile of up to 16*NSUB of that expert's tokens.
 // The reduction dimension is walked in chunks of 32*KS:
@@ -136,10 +204,20 @@ __device__ __forceinline__ bf16x8 ld16_stream(const uint16_t* p) {
 // 16*KS*(GATED ? 2 : 1) bytes per lane of weights in flight.
 // Token sub-tiles beyond the tile's row count are skipped (uniform branch),
 // so a tile of 1 token costs one MFMA per k-step and matrix.
-// Token rows two chunks ahead (see the main loop) in the gated projection
-// with up to 64-token tiles; measured: the plain projection gains nothing.
+// Token rows two chunks ahead (see the main loop) in every variant.  Measured
+// against one chunk ahead: the 128-token gated tiles +12% on the fine-grained
+// layer's 256-token Top-K decode and +4-6% in EAT; the plain projection's
+// 128-token tiles +8% (down) on the shared-expert layer's EAT decode, the
+// 16-layer stack +1%; the 2-step chunks of 128-token gated tiles spill, and
+// with one chunk ahead they gain less (EAT_KS_G8 = 2: +2-5%).
+#ifndef EAT_DEEP_NSUB
+#define EAT_DEEP_NSUB 8
+#endif
+#ifndef EAT_DEEP_PLAIN_NSUB
+#define EAT_DEEP_PLAIN_NSUB 8
+#endif
 template <bool GATED, int NSUB>
-constexpr bool stream_deep() { return GATED && NSUB <= 4; }
+constexpr bool stream_deep() { return GATED ? NSUB <= EAT_DEEP_NSUB : NSUB <= EAT_DEEP_PLAIN_NSUB; }
 
 // At least 3 waves per SIMD: the register budget then keeps the MFMA
 // accumulators in VGPRs (no AGPR copies) and the 64-token gated variant
@@ -165,9 +243,14 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
     } else {
         ntiles = (a.nrows + BN - 1) / BN;
     }
+    // slices of the reduction dimension: fixed, or chosen from the tiles in
+    // use (every workgroup computes the same value)
+    const int splits = a.rule_threshold > 0 ? split_rule(a.M, a.K, ntiles, a.splits, a.rule_threshold) : a.splits;
+    if (a.splits_out && blockIdx.x == 0 && tid == 0) *a.splits_out = splits;
+    const int ksplit = a.K / splits;
 
     const int i = lane & 15, g = lane >> 4;
-    const int nch = a.ksplit / KC;
+    const int nch = ksplit / KC;
     const int nrb = a.M / (16 * WPB);                 // weight-row blocks
 
     // Work items (token tile, reduction slice, row block), row block
@@ -176,14 +259,14 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
     // so a call whose tokens land on few experts leaves no idle workgroups
     // behind the working ones.
     // (the launcher keeps the item count below 2^31)
-    const unsigned items = static_cast<unsigned>(ntiles) * a.splits * nrb;
+    const unsigned items = static_cast<unsigned>(ntiles) * splits * nrb;
     for (unsigned w = blockIdx.x; w < items; w += gridDim.x) {
         const int rb = static_cast<int>(w % nrb);
         const unsigned rest = w / nrb;
-        const int split = static_cast<int>(rest % a.splits);
-        const int tile = static_cast<int>(rest / a.splits);
+        const int split = static_cast<int>(rest % splits);
+        const int tile = static_cast<int>(rest / splits);
         const int m0 = rb * (16 * WPB) + wave * 16;
-        const int kbeg = split * a.ksplit;
+        const int kbeg = split * ksplit;
         int e = 0, r0, n;
         if (a.offsets) {
             e = tile_group(tstart, a.groups, tile);
@@ -346,29 +429,36 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
         }
 
         // result: lane holds weight rows m0 + 4g + q (q < 4) for token column s*16 + i
+        if constexpr (GATED) {
+            if (splits == 1) {
 #pragma unroll
-        for (int s = 0; s < NSUB; ++s) {
-            const int c = s * 16 + i;
-            if (c >= n) continue;
-            const size_t o = static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g;
-            if (GATED && a.partial) {
-                const size_t po = split * a.split_stride + o;
-                *reinterpret_cast<float4*>(static_cast<float*>(a.out) + po) =
-                    make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
-                *reinterpret_cast<float4*>(a.out2 + po) =
-                    make_float4(acc_b[s][0], acc_b[s][1], acc_b[s][2], acc_b[s][3]);
-            } else if constexpr (GATED) {
-                uint16_t hv[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) hv[q] = f32_to_bf16(silu(acc_a[s][q]) * acc_b[s][q]);
-                uint2 pk;
-                pk.x = static_cast<uint32_t>(hv[0]) | (static_cast<uint32_t>(hv[1]) << 16);
-                pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
-                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + o) = pk;
+                for (int s = 0; s < NSUB; ++s) {
+                    const int c = s * 16 + i;
+                    if (c >= n) continue;
+                    store_h(a.h + static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g, acc_a[s], acc_b[s]);
+                }
             } else {
-                float* op = static_cast<float*>(a.out) + split * a.split_stride + o;
-                *reinterpret_cast<float4*>(op) =
-                    make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
+                // this slice's G/U partial sums (swiglu_reduce_kernel adds
+                // the slices in order and forms H)
+#pragma unroll
+                for (int s = 0; s < NSUB; ++s) {
+                    const int c = s * 16 + i;
+                    if (c >= n) continue;
+                    const size_t po = split * a.split_stride + static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g;
+                    *reinterpret_cast<float4*>(static_cast<float*>(a.out) + po) =
+                        make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
+                    *reinterpret_cast<float4*>(a.out2 + po) =
+                        make_float4(acc_b[s][0], acc_b[s][1], acc_b[s][2], acc_b[s][3]);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int s = 0; s < NSUB; ++s) {
+                const int c = s * 16 + i;
+                if (c >= n) continue;
+                float* op = static_cast<float*>(a.out) + split * a.split_stride +
+                            static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g;
+                *reinterpret_cast<float4*>(op) = make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
             }
         }
     }
@@ -389,12 +479,17 @@ __global__ __launch_bounds__(256) void sum_slices_kernel(const float* __restrict
 
 // H[r][f] = bf16(silu(sum_s G[s][r][f]) * sum_s U[s][r][f]) over the rows
 // in use (*rows_dev of them, or rows_host when rows_dev is null), slices
-// added in slice order.
+// added in slice order.  The slice count is *splits_dev (the gated launch's
+// own choice) when set, else splits_host; with one slice the projection
+// wrote H itself and there is nothing to do.
 __global__ __launch_bounds__(256) void swiglu_reduce_kernel(const float* __restrict__ gp,
                                                             const float* __restrict__ up,
                                                             const int32_t* __restrict__ rows_dev, int rows_host,
-                                                            int M, int splits, int64_t split_stride,
+                                                            int M, const int32_t* __restrict__ splits_dev,
+                                                            int splits_host, int64_t split_stride,
                                                             uint16_t* __restrict__ h) {
+    const int splits = splits_dev ? *splits_dev : splits_host;
+    if (splits <= 1) return;                          // uniform: one load, then every thread leaves
     const int64_t total = static_cast<int64_t>(rows_dev ? *rows_dev : rows_host) * (M / 4);
     for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < total;
          v += int64_t(gridDim.x) * blockDim.x) {
@@ -407,12 +502,7 @@ __global__ __launch_bounds__(256) void swiglu_reduce_kernel(const float* __restr
             gs.x += ga.x; gs.y += ga.y; gs.z += ga.z; gs.w += ga.w;
             us.x += ua.x; us.y += ua.y; us.z += ua.z; us.w += ua.w;
         }
-        uint2 pk;
-        pk.x = static_cast<uint32_t>(f32_to_bf16(silu(gs.x) * us.x)) |
-               (static_cast<uint32_t>(f32_to_bf16(silu(gs.y) * us.y)) << 16);
-        pk.y = static_cast<uint32_t>(f32_to_bf16(silu(gs.z) * us.z)) |
-               (static_cast<uint32_t>(f32_to_bf16(silu(gs.w) * us.w)) << 16);
-        *reinterpret_cast<uint2*>(h + o) = pk;
+        store_h(h + o, f32x4{gs.x, gs.y, gs.z, gs.w}, f32x4{us.x, us.y, us.z, us.w});
     }
 }
 
@@ -436,6 +526,9 @@ static int pick_ks(int ksplit) {
 #ifndef EAT_KS_G2
 #define EAT_KS_G2 4
 #endif
+#ifndef EAT_KS_G8
+#define EAT_KS_G8 1
+#endif
 #ifndef EAT_KS_G4
 #define EAT_KS_G4 2
 #endif
@@ -450,7 +543,7 @@ static int pick_ks(int ksplit) {
 #endif
 template <bool GATED, int NSUB>
 constexpr int max_ks() {
-    if (GATED) return NSUB >= 8 ? 1 : NSUB >= 4 ? EAT_KS_G4 : NSUB >= 2 ? EAT_KS_G2 : EAT_KS_G1;
+    if (GATED) return NSUB >= 8 ? EAT_KS_G8 : NSUB >= 4 ? EAT_KS_G4 : NSUB >= 2 ? EAT_KS_G2 : EAT_KS_G1;
     return NSUB >= 8 ? 2 : NSUB >= 4 ? EAT_KS_P4 : NSUB >= 2 ? EAT_KS_P2 : EAT_KS_P1;
 }
 
@@ -495,7 +588,7 @@ template <bool GATED, int NSUB, int KS, int WPB, bool PACKED>
 hipError_t launch_stream_w(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
     const int64_t items = max_tiles * a.splits * (a.M / (16 * WPB));
     if (items >= (int64_t{1} << 31)) return hipErrorInvalidValue;
-    const int64_t blocks = std::max<int64_t>(1, std::min(items, stream_resident<GATED, NSUB, KS, WPB, PACKED>()));
+    int64_t blocks = std::max<int64_t>(1, std::min(items, stream_resident<GATED, NSUB, KS, WPB, PACKED>()));
     stream_kernel<GATED, NSUB, KS, WPB, PACKED><<<dim3(static_cast<unsigned>(blocks)), dim3(WPB * 64), 0, s>>>(a);
     return hipGetLastError();
 }
@@ -517,7 +610,9 @@ hipError_t launch_stream_k(const StreamArgs& a, int64_t max_tiles, hipStream_t s
 
 template <bool GATED, int NSUB, bool PACKED>
 hipError_t launch_stream_n(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
-    const int ks = std::min(pick_ks(a.ksplit), max_ks<GATED, NSUB>());
+    // the device may take fewer slices than a.splits; K / a.splits divides
+    // every longer slice, so its chunk depth fits them all
+    const int ks = std::min(pick_ks(a.K / a.splits), max_ks<GATED, NSUB>());
     switch (ks) {
         case 8: return launch_stream_k<GATED, NSUB, 8, PACKED>(a, max_tiles, s);
         case 4: return launch_stream_k<GATED, NSUB, 4, PACKED>(a, max_tiles, s);
@@ -536,7 +631,7 @@ hipError_t launch_stream_p(const StreamArgs& a, int nsub, int64_t max_tiles, hip
     }
 }
 
-// `a.splits` slices of `a.ksplit` each; max_tiles bounds the token tiles a
+// Up to `a.splits` slices; max_tiles bounds the token tiles a
 // call can hold (their count is only known on the device); `packed` selects
 // the packed weight layout (pack.hip).
 template <bool GATED>
@@ -557,55 +652,30 @@ static int pick_nsub(int64_t T) {
     return 8;
 }
 
-// Reduction-dimension slices of a stream launch: double them while the
-// number of 16-row wave tiles over the experts a call may be left with is
-// below EAT_SPLIT_WAVES.  The union is only known on the device, so the host
-// counts the experts a call is expected to touch: in EAT mode only K (EAT
-// concentrates its picks, and short launches must still spread over the
-// whole chip and end without a long tail); with Top-K and Top-P routing
-// min(E, T K), since their tokens spread over the experts (each slice costs
-// the combine one more fp32 row per assignment to read).
-#ifndef EAT_SPLIT_WAVES
-#define EAT_SPLIT_WAVES 4096
-#endif
-// Once the grid holds ~1024 wave tiles, a slice keeps at least
-// EAT_SPLIT_MIN_K reduction elements: shorter ones cost more in partial rows
-// than their extra waves gain (measured: 4 slices of a 1024-wide down
-// projection over 8 experts are slower than 2); smaller grids split down
-// to 128 (the same projection over 2 experts gains from 4 slices).
-#ifndef EAT_SPLIT_MIN_K
-#define EAT_SPLIT_MIN_K 384
-#endif
-// The gated projection pays for its slices with fp32 partials and a reduce
-// pass, so it only splits grids that would leave most of the chip idle.
-#ifndef EAT_UP_SPLIT_WAVES
-#define EAT_UP_SPLIT_WAVES 1024
-#endif
-// With 128-token tiles (calls of more than 64 tokens) an expert's tile is a
-// small prefill, and up to 2048 waves pay: the fine-grained layer's 256-token
-// EAT decode (~8 experts of ~256 tokens) +14%, Top-K unchanged; 1024 stays
-// for smaller tiles (the Mixtral-shaped 64-token decode loses 10% at 2048).
-#ifndef EAT_UP_SPLIT_WAVES_T128
-#define EAT_UP_SPLIT_WAVES_T128 2048
-#endif
-#ifndef EAT_UP_SPLIT_MAX
-#define EAT_UP_SPLIT_MAX 4
-#endif
-static int pick_nsub(int64_t T);
+// Most slices a launch of T tokens may take: the rule over the fewest tiles
+// the call can hold (the rule only shrinks as tiles grow).  Every token of
+// a Top-K call selects exactly K experts, so it holds at least
+// max(K, ceil(T K / bn)) tiles; an EAT or Top-P token selects at least one
+// expert, so at least ceil(T / bn).  The device takes the rule over the
+// tiles actually in use (stream_kernel).
+static int min_tiles(const eat_params_t& p, int32_t T) {
+    const int64_t bn = 16 * pick_nsub(T);
+    const int64_t t = std::max<int64_t>(1, T);
+    return static_cast<int>(p.mode == EAT_MODE_TOPK ? std::max<int64_t>(p.top_k, (t * p.top_k + bn - 1) / bn)
+                                                    : (t + bn - 1) / bn);
+}
 
-static int stream_splits(int64_t rows_m, int kdim, const eat_params_t& p, int32_t T, int max_splits,
-                         int64_t threshold) {
+// Tiles a call is expected to hold: EAT concentrates its picks on about K
+// experts; Top-K and Top-P tokens spread over min(E, T K).  The up/gate
+// projection plans its slices for this many (the device may take fewer,
+// never more): its slices need a reduce kernel, and planning for a
+// one-expert union would launch it for nothing in most calls.
+static int expected_tiles(const eat_params_t& p, int32_t T) {
     const int64_t assign = std::max<int64_t>(1, static_cast<int64_t>(T) * p.top_k);
     const int64_t active = std::min<int64_t>(
         {static_cast<int64_t>(p.E), assign, p.mode == EAT_MODE_EAT ? static_cast<int64_t>(p.top_k) : assign});
     const int64_t bn = 16 * pick_nsub(T);
-    const int64_t tiles = std::max<int64_t>(active, (assign + bn - 1) / bn);
-    const int64_t waves = (rows_m / 16) * tiles;
-    int s = 1;
-    while (s < max_splits && kdim % (64 * 2 * s) == 0 && waves * s < threshold &&
-           kdim / (2 * s) >= (waves * s < 1024 ? 128 : EAT_SPLIT_MIN_K))
-        s *= 2;
-    return s;
+    return static_cast<int>(std::max<int64_t>(active, (assign + bn - 1) / bn));
 }
 
 // Calls averaging at least this many rows per expert take the wide MFMA
@@ -628,13 +698,13 @@ static bool shared_wide(const eat_params_t& p, int32_t T) {
 
 int down_splits(const eat_params_t& p, int32_t T) {
     if (p.expert_dtype != EAT_BF16 || use_wide(p, T)) return 1;
-    return stream_splits(p.d_model, p.d_ffn, p, T, 8, EAT_SPLIT_WAVES);
+    return split_rule(p.d_model, p.d_ffn, min_tiles(p, T), 8, EAT_SPLIT_WAVES);
 }
 
 int up_splits(const eat_params_t& p, int32_t T) {
     if (p.expert_dtype != EAT_BF16 || use_wide(p, T)) return 1;
-    return stream_splits(p.d_ffn, p.d_model, p, T, EAT_UP_SPLIT_MAX,
-                         pick_nsub(T) >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES);
+    return split_rule(p.d_ffn, p.d_model, expected_tiles(p, T), EAT_UP_SPLIT_MAX,
+                      pick_nsub(T) >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES);
 }
 
 // Dense projection (one group of T identity rows): the wide tiles from 384
@@ -659,7 +729,7 @@ hipError_t launch_dense_bf16(const uint16_t* src, int32_t T, const uint16_t* w, 
     const int bn = 16 * nsub;
     const int tiles = (T + bn - 1) / bn;
     StreamArgs a{};
-    a.wa = w; a.src = src; a.nrows = T; a.groups = 1; a.M = M; a.K = K; a.splits = splits; a.ksplit = K / splits;
+    a.wa = w; a.src = src; a.nrows = T; a.groups = 1; a.M = M; a.K = K; a.splits = splits;
     a.split_stride = split_stride; a.out = out;
     return launch_stream<false>(a, nsub, tiles, false, s);
 }
@@ -684,7 +754,8 @@ hipError_t launch_shared_f32(const eat_params_t& p, int32_t T, const float* x, c
 hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_cap, const uint16_t* x,
                                const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
                                const int32_t* offsets, const int32_t* tok_idx, uint16_t* h,
-                               float* gu, float* yp, hipStream_t s, const std::function<void()>& between) {
+                               float* gu, float* yp, int32_t* up_splits_dev, int32_t* down_splits_dev, hipStream_t s,
+                               const std::function<void()>& between) {
     const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;
     // no expert holds more than T rows, so it needs at most ceil(T / bn) tiles
@@ -700,21 +771,24 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
         return launch_wide(false, w2, nullptr, h, nullptr, offsets, p.E, 0, p.d_model, p.d_ffn, yp, rows_cap, packed,
                            s);
     }
+    // both projections take their slices on the device, from the tiles in use
     const int usplits = up_splits(p, T);
     StreamArgs up{};
     up.wa = w1; up.wb = w3; up.src = x; up.gather = tok_idx; up.offsets = offsets;
-    up.groups = p.E; up.M = p.d_ffn; up.K = p.d_model; up.splits = usplits; up.ksplit = p.d_model / usplits;
+    up.groups = p.E; up.M = p.d_ffn; up.K = p.d_model; up.splits = usplits;
+    up.rule_threshold = usplits > 1 ? (nsub >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES) : 0;
     up.split_stride = rows_cap * p.d_ffn;
-    up.partial = usplits > 1;
-    up.out = up.partial ? static_cast<void*>(gu) : static_cast<void*>(h);
-    up.out2 = up.partial ? gu + usplits * up.split_stride : nullptr;
+    up.out = gu;
+    up.out2 = gu + usplits * up.split_stride;
+    up.h = h;
+    up.splits_out = up_splits_dev;
     hipError_t err = launch_stream<true>(up, nsub, max_tiles, packed, s);
     if (err != hipSuccess) return err;
-    if (up.partial) {
+    if (usplits > 1) {
         const int64_t vec = rows_cap * (p.d_ffn / 4);
         const int grid = static_cast<int>(std::min<int64_t>((vec + 255) / 256, 4096));
-        swiglu_reduce_kernel<<<grid, 256, 0, s>>>(gu, up.out2, offsets + p.E, 0, p.d_ffn, usplits, up.split_stride,
-                                                  h);
+        swiglu_reduce_kernel<<<grid, 256, 0, s>>>(gu, up.out2, offsets + p.E, 0, p.d_ffn, up_splits_dev, usplits,
+                                                  up.split_stride, h);
         err = hipGetLastError();
         if (err != hipSuccess) return err;
     }
@@ -723,7 +797,9 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     const int splits = down_splits(p, T);
     StreamArgs dn{};
     dn.wa = w2; dn.wb = nullptr; dn.src = h; dn.gather = nullptr; dn.offsets = offsets;
-    dn.groups = p.E; dn.M = p.d_model; dn.K = p.d_ffn; dn.splits = splits; dn.ksplit = p.d_ffn / splits;
+    dn.groups = p.E; dn.M = p.d_model; dn.K = p.d_ffn; dn.splits = splits;
+    dn.rule_threshold = splits > 1 ? EAT_SPLIT_WAVES : 0;
+    dn.splits_out = down_splits_dev;
     dn.split_stride = rows_cap * p.d_model; dn.out = yp;
     return launch_stream<false>(dn, nsub, max_tiles, packed, s);
 }
@@ -737,8 +813,8 @@ int shared_up_splits(const eat_params_t& p, int32_t T) {
     eat_params_t one = p;
     one.E = 1;
     one.top_k = 1;
-    return stream_splits(p.d_shared, p.d_model, one, T, EAT_UP_SPLIT_MAX,
-                         pick_nsub(T) >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES);
+    return split_rule(p.d_shared, p.d_model, expected_tiles(one, T), EAT_UP_SPLIT_MAX,
+                      pick_nsub(T) >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES);
 }
 
 int shared_splits(const eat_params_t& p, int32_t T) {
@@ -762,24 +838,25 @@ hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* 
     const int usplits = shared_up_splits(p, T);
     StreamArgs up{};
     up.wa = ws1; up.wb = ws3; up.src = x; up.gather = nullptr; up.offsets = nullptr; up.nrows = T;
-    up.groups = 1; up.M = p.d_shared; up.K = p.d_model; up.splits = usplits; up.ksplit = p.d_model / usplits;
+    up.groups = 1; up.M = p.d_shared; up.K = p.d_model; up.splits = usplits;
     up.split_stride = static_cast<int64_t>(T) * p.d_shared;
-    up.partial = usplits > 1;
-    up.out = up.partial ? static_cast<void*>(gus) : static_cast<void*>(hs);
-    up.out2 = up.partial ? gus + usplits * up.split_stride : nullptr;
+    up.out = gus;
+    up.out2 = gus + usplits * up.split_stride;
+    up.h = hs;
     hipError_t err = launch_stream<true>(up, nsub, tiles, packed, s);
     if (err != hipSuccess) return err;
-    if (up.partial) {
+    if (usplits > 1) {
         const int64_t vec = static_cast<int64_t>(T) * (p.d_shared / 4);
         const int grid = static_cast<int>(std::min<int64_t>((vec + 255) / 256, 4096));
-        swiglu_reduce_kernel<<<grid, 256, 0, s>>>(gus, up.out2, nullptr, T, p.d_shared, usplits, up.split_stride, hs);
+        swiglu_reduce_kernel<<<grid, 256, 0, s>>>(gus, up.out2, nullptr, T, p.d_shared, nullptr, usplits,
+                                                  up.split_stride, hs);
         err = hipGetLastError();
         if (err != hipSuccess) return err;
     }
     const int splits = shared_splits(p, T);
     StreamArgs dn{};
     dn.wa = ws2; dn.wb = nullptr; dn.src = hs; dn.gather = nullptr; dn.offsets = nullptr; dn.nrows = T;
-    dn.groups = 1; dn.M = p.d_model; dn.K = p.d_shared; dn.splits = splits; dn.ksplit = p.d_shared / splits;
+    dn.groups = 1; dn.M = p.d_model; dn.K = p.d_shared; dn.splits = splits;
     dn.split_stride = static_cast<int64_t>(T) * p.d_model;
     dn.out = splits > 1 ? ysp : ys;
     err = launch_stream<false>(dn, nsub, tiles, packed, s);

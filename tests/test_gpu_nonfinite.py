@@ -1,9 +1,14 @@
 """Non-finite hidden states (reading R25): a token whose row holds NaN or Inf
 gets NaN router scores; its selection follows the documented rule of each
 mode and never exceeds what the workspace holds, and every other token of the
-call is unaffected -- its output row and mask are bit-identical to a call
-without the bad tokens, and the EAT accounts equal those of a call with the
-bad tokens removed (snapshot semantics: tokens are independent)."""
+call is unaffected -- its mask is identical to a call without the bad
+tokens and its output row finite and equal to that call's: bit for bit in
+EAT mode, where the bad tokens select nothing and the experts in use are the
+same, to the bf16 tolerance in the baselines, where the bad tokens' experts
+join the call's and so may change the number of reduction slices the
+expert kernels take (an order of additions); and the EAT accounts equal
+those of a call with the bad tokens removed (snapshot semantics: tokens are
+independent)."""
 import numpy as np
 import pytest
 import torch
@@ -56,7 +61,13 @@ def test_nonfinite_tokens_are_contained(shape_name, E, d, F, mode):
     keep = [t for t in range(T) if t not in BAD]
     for t in keep:
         assert mb[t] == mg[t], t
-        assert torch.equal(yb[t], yg[t]), t
+        if mode == "eat":
+            assert torch.equal(yb[t], yg[t]), t
+        else:
+            fb = yb[t].view(torch.bfloat16).float()
+            fg = yg[t].view(torch.bfloat16).float()
+            assert torch.isfinite(fb).all(), t
+            assert (fb - fg).abs().max() <= PT.TOL_Y_BF16 * fg.abs().max(), t
     K = shape.K
     for t in BAD:
         k = bin(mb[t]).count("1")

@@ -209,6 +209,18 @@ def test_forward_parity(case, mode, T):
     _forward_check(f"forward {case} {mode} T={T}", lay, shape, x, w, prm, acc=acc)
 
 
+# larger decode-sized calls on the 64-expert layer: several 128-token tiles
+# per expert, the slice counts the device picks for 256-513 tokens
+@pytest.mark.parametrize("mode", ["eat", "topk", "topp"])
+@pytest.mark.parametrize("T", [256, 512, 513])
+def test_forward_parity_larger_decodes(mode, T):
+    c = SMALL["finegrained"]
+    shape, w, lay, prm = _layer(c, mode, max_tokens=T)
+    x = _x_host(shape, T, c["d"], seed=400 + T)
+    acc = make_accounts(c["E"], seed=T, c_scale=0.05)
+    _forward_check(f"larger decode {mode} T={T}", lay, shape, x, w, prm, acc=acc)
+
+
 # degenerate configurations: one expert (fp32 and bf16, the smallest d and
 # F), a cap equal to the expert count, Top-P with p = 1
 DEGENERATE = {

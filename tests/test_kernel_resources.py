@@ -1,7 +1,9 @@
 """Every gfx950 kernel must run without private (scratch) memory or VGPR
 spills: a local array left in scratch turned the expert kernels' stores
-into tens of MB of extra HBM writes per launch.  Compiles each HIP source
-with hipcc's resource-usage remarks (CPU only, no GPU needed)."""
+into tens of MB of extra HBM writes per launch.  SGPR spills are allowed
+while the scratch size stays zero: the compiler then parks them in VGPR
+lanes, which costs no memory traffic.  Compiles each HIP source with
+hipcc's resource-usage remarks (CPU only, no GPU needed)."""
 import os
 import re
 import shutil
@@ -12,7 +14,8 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2609_33614_amd", "csrc")
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
-SOURCES = sorted(f for f in os.listdir(CSRC) if f.endswith(".hip"))
+SOURCES = sorted(f for f in os.listdir(CSRC)
+                 if f.endswith(".hip") and "__global__" in open(os.path.join(CSRC, f)).read())
 
 
 @pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc missing")
@@ -38,4 +41,4 @@ def test_no_scratch_or_spills(src, tmp_path):
     assert kernels, "no kernels reported"
     for name, info in kernels.items():
         assert info.get("ScratchSize [bytes/lane]") == "0", f"{name} uses scratch: {info}"
-        assert info.get("VGPRs Spill") == "0" and info.get("SGPRs Spill") == "0", f"{name} spills: {info}"
+        assert info.get("VGPRs Spill") == "0", f"{name} spills VGPRs: {info}"
