@@ -56,7 +56,10 @@ constexpr int kWaves = 4 * kWM / (32 * kTF);   // token groups x 4 weight quarte
 constexpr int kThreads = kWaves * kWave;
 constexpr int kRegion = kWM * kRB;        // bytes of one operand's rows per stage
 constexpr int kStage = 2 * kRegion;       // tokens then weights
-constexpr int kStages = (128 * 1024) / kStage;   // ring depth in 128 KB of LDS
+#ifndef EAT_WIDE_RING_KB
+#define EAT_WIDE_RING_KB 128
+#endif
+constexpr int kStages = (EAT_WIDE_RING_KB * 1024) / kStage;   // ring depth
 constexpr int kXcd = 8;
 static_assert(kWN * kWK * 2 == kRegion, "token and weight regions have the same size");
 
@@ -70,12 +73,14 @@ struct WideArgs {
     void* out;                 // gated: bf16 H [rows][M]; plain: fp32 [rows][M]
 };
 
-// Byte offset of 16-byte vector v of row r in a region of kRB-byte rows;
-// the XOR spreads the rows that one LDS cycle serves for an MFMA operand
-// read (consecutive rows, same vector) over distinct banks.
-__device__ __forceinline__ int wswz(int r, int v) {
-    return r * kRB + ((v ^ ((r >> 1) & (kVPR - 1))) << 4);
-}
+// Byte offset of 16-byte vector v of row r in a region of kRB-byte rows.
+// An MFMA operand read takes one vector of 16 consecutive rows per pass of
+// the 64 LDS banks (256 bytes = kRowsPerLine rows); the XOR of the vector
+// index with the row's line number spreads those 16 rows over distinct
+// banks: (r >> 1) & 7 for 128-byte rows, (r >> 2) & 3 for 64-byte rows.
+constexpr int kRowsPerLine = 256 / kRB;
+__device__ __forceinline__ int swz(int r) { return (r / kRowsPerLine) & (kVPR - 1); }
+__device__ __forceinline__ int wswz(int r, int v) { return r * kRB + ((v ^ swz(r)) << 4); }
 
 constexpr int kNB = (kWM + kWN) / kRPB;       // 1 KB DMA blocks per stage
 constexpr int kBPW = kNB / kWaves;            // per wave
@@ -129,12 +134,12 @@ __device__ __forceinline__ ItemLoads item_loads(const WideArgs& a, const Item& i
         const int b = wave + kWaves * j;
         if (j < kBT) {
             const int r = kRPB * b + lane / kVPR;
-            const int v = slot ^ ((r >> 1) & (kVPR - 1));
+            const int v = slot ^ swz(r);
             L.srct[j] = a.src + static_cast<size_t>(srow[j]) * a.K + 8 * v;
         } else {
             const int rb0 = kRPB * (b - kWM / kRPB);          // the block's first weight row
             const int r = rb0 + lane / kVPR;
-            const int v = slot ^ ((r >> 1) & (kVPR - 1));
+            const int v = slot ^ swz(r);
             const int row = it.m0 + (GATED ? (r & (kWN / 2 - 1)) : r);
             // packed: vector v of a chunk is k-step v / 4 of the chunk,
             // fragment (v % 4, row % 16) of that step's block (pack.hip)
