@@ -80,14 +80,17 @@ __device__ __forceinline__ float wave_max(float v) {
 // Tile table of expert-major row segments: tstart[g] = sum over h < g of
 // ceil((offsets[h+1] - offsets[h]) / bm), for g = 0..groups.  Wave 0 reads
 // one segment per lane and scans 64 at a time (integer sums, so the order
-// does not matter); every thread of the workgroup must call it.
-__device__ __forceinline__ void tile_starts(const int32_t* offsets, int groups, int bm, int* tstart) {
+// does not matter); every thread of the workgroup must call it.  `used`, if
+// given (LDS), receives the number of non-empty segments.
+__device__ __forceinline__ void tile_starts(const int32_t* offsets, int groups, int bm, int* tstart,
+                                            int* used = nullptr) {
     if (threadIdx.x < kWave) {
         const int lane = __lane_id();
-        int carry = 0;
+        int carry = 0, nonempty = 0;
         for (int g0 = 0; g0 < groups; g0 += kWave) {
             const int g = g0 + lane;
             int c = g < groups ? (offsets[g + 1] - offsets[g] + bm - 1) / bm : 0;
+            nonempty += __popcll(__ballot(c > 0));
 #pragma unroll
             for (int o = 1; o < kWave; o <<= 1) {
                 const int u = __shfl_up(c, o, kWave);
@@ -96,7 +99,10 @@ __device__ __forceinline__ void tile_starts(const int32_t* offsets, int groups, 
             if (g < groups) tstart[g + 1] = carry + c;
             carry += __shfl(c, kWave - 1, kWave);
         }
-        if (lane == 0) tstart[0] = 0;
+        if (lane == 0) {
+            tstart[0] = 0;
+            if (used) *used = nonempty;
+        }
     }
     __syncthreads();
 }

@@ -25,6 +25,7 @@
 // fp32 path: plain dot products, one thread per output element, for layers
 // whose weights are fp32 (small correctness-sized layers).
 #include <algorithm>
+#include <type_traits>
 
 #include "eat_device.h"
 #include "eat_internal.h"
@@ -176,6 +177,24 @@ __device__ __forceinline__ bf16x8 ld16(const uint16_t* p) {
 __device__ __forceinline__ bf16x8 ld16_stream(const uint16_t* p) {
     return __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(p));
 }
+// Weight loads of 128-token tiles follow the launch's weight footprint:
+// when the experts in use hold at most this many bytes of the launch's
+// matrices they are loaded through the caches and stay in the chip's
+// last-level cache for the next call (decode steps keep selecting the same
+// experts); more than that streams past the caches (non-temporal), which
+// keeps them for the token rows.  Smaller tiles always stream: they serve
+// calls whose experts' weights far exceed the cache.
+#ifndef EAT_CACHE_WEIGHT_BYTES
+#define EAT_CACHE_WEIGHT_BYTES (96ll << 20)
+#endif
+#ifndef EAT_CACHE_MIN_NSUB
+#define EAT_CACHE_MIN_NSUB 8
+#endif
+template <bool STREAM>
+__device__ __forceinline__ bf16x8 ld16_w(const uint16_t* p) {
+    if constexpr (STREAM) return ld16_stream(p);
+    else return ld16(p);
+}
 
 // Slices the gated projection may use (the last slice reads the others'
 // partials into registers).
@@ -233,13 +252,15 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
     constexpr bool DEEP = stream_deep<GATED, NSUB>();
     __shared__ __attribute__((aligned(16))) uint16_t xs[2][BN * LDS_ROW];
     __shared__ int tstart[kMaxExperts + 1];
+    __shared__ int used_groups;
     const int tid = threadIdx.x;
     const int lane = lane_id(), wave = tid / kWave;
 
-    int ntiles;
+    int ntiles, used = 1;
     if (a.offsets) {
-        tile_starts(a.offsets, a.groups, BN, tstart);
+        tile_starts(a.offsets, a.groups, BN, tstart, &used_groups);
         ntiles = tstart[a.groups];
+        used = used_groups;
     } else {
         ntiles = (a.nrows + BN - 1) / BN;
     }
@@ -260,207 +281,244 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
     // behind the working ones.
     // (the launcher keeps the item count below 2^31)
     const unsigned items = static_cast<unsigned>(ntiles) * splits * nrb;
-    for (unsigned w = blockIdx.x; w < items; w += gridDim.x) {
-        const int rb = static_cast<int>(w % nrb);
-        const unsigned rest = w / nrb;
-        const int split = static_cast<int>(rest % splits);
-        const int tile = static_cast<int>(rest / splits);
-        const int m0 = rb * (16 * WPB) + wave * 16;
-        const int kbeg = split * ksplit;
-        int e = 0, r0, n;
-        if (a.offsets) {
-            e = tile_group(tstart, a.groups, tile);
-            r0 = a.offsets[e] + (tile - tstart[e]) * BN;
-            n = min(BN, a.offsets[e + 1] - r0);
-        } else {
-            r0 = tile * BN;
-            n = min(BN, a.nrows - r0);
-        }
-        const int nsub = (n + 15) >> 4;
-        // Row-major weights: this lane's 8 elements of row m0 + i at k-offset
-        // 8 g of each 32-wide k-step.  Packed weights: the wave's 16 rows form
-        // one 1 KB block per k-step, lane l's fragment at 16 l bytes.
-        const size_t wrow = PACKED ? (static_cast<size_t>(e) * (a.M / 16) + m0 / 16) * (a.K / 32) * 512 + 8 * lane
-                                   : (static_cast<size_t>(e) * a.M + m0 + i) * a.K + 8 * g;
-        const uint16_t* pa = a.wa + wrow;
-        const uint16_t* pb = GATED ? a.wb + wrow : nullptr;
-
-        // token-row vectors this thread moves into LDS each chunk
-        const uint16_t* xsrc[RMAX];
-        int xdst[RMAX];
-        bool xon[RMAX];
-#pragma unroll
-        for (int r = 0; r < RMAX; ++r) {
-            const int v = tid + NT * r;
-            const int row = v / VPR, col = v % VPR;
-            xon[r] = row < n;
-            const int srow = xon[r] ? (a.gather ? a.gather[r0 + row] : r0 + row) : 0;
-            xsrc[r] = a.src + static_cast<size_t>(srow) * a.K + kbeg + 8 * col;
-            xdst[r] = row * LDS_ROW + 8 * col;
-        }
-        // Every lane loads (rows past the tile read a valid row and are not
-        // stored), so xr stays in registers instead of private memory.
-        // (native vector type: HIP's uint4 struct would be copied with
-        // memcpy and kept in private memory)
-        bf16x8 xr[RMAX];
-        auto load_xr = [&](int c, bf16x8 (&R)[RMAX]) __attribute__((always_inline)) {
-#pragma unroll
-            for (int r = 0; r < RMAX; ++r) R[r] = ld16(xsrc[r] + c * KC);
-        };
-        auto store_xr = [&](int buf, const bf16x8 (&R)[RMAX]) __attribute__((always_inline)) {
-#pragma unroll
-            for (int r = 0; r < RMAX; ++r)
-                if (xon[r]) *reinterpret_cast<bf16x8*>(&xs[buf][xdst[r]]) = R[r];
-        };
-        auto load_x = [&](int c) __attribute__((always_inline)) { load_xr(c, xr); };
-        auto store_x = [&](int buf) __attribute__((always_inline)) { store_xr(buf, xr); };
-        auto load_w = [&](int c, bf16x8 (&A)[KS], bf16x8 (&B)[KS]) __attribute__((always_inline)) {
-            const int k = kbeg + c * KC;
-#pragma unroll
-            for (int j = 0; j < KS; ++j) {
-                if constexpr (PACKED) {
-                    const size_t o = static_cast<size_t>(k / 32 + j) * 512;
-                    A[j] = ld16_stream(pa + o);
-                    if constexpr (GATED) B[j] = ld16_stream(pb + o);
-                } else {
-                    A[j] = ld16(pa + k + 32 * j);
-                    if constexpr (GATED) B[j] = ld16(pb + k + 32 * j);
-                }
+    const int64_t footprint = static_cast<int64_t>(used) * a.M * a.K * (GATED ? 4 : 2);
+    const bool stream_w = NSUB < EAT_CACHE_MIN_NSUB || footprint > EAT_CACHE_WEIGHT_BYTES;
+    auto run = [&](auto stream_tag) __attribute__((always_inline)) {
+        constexpr bool kStreamW = decltype(stream_tag)::value;
+        for (unsigned w = blockIdx.x; w < items; w += gridDim.x) {
+            const int rb = static_cast<int>(w % nrb);
+            const unsigned rest = w / nrb;
+            const int split = static_cast<int>(rest % splits);
+            const int tile = static_cast<int>(rest / splits);
+            const int m0 = rb * (16 * WPB) + wave * 16;
+            const int kbeg = split * ksplit;
+            int e = 0, r0, n;
+            if (a.offsets) {
+                e = tile_group(tstart, a.groups, tile);
+                r0 = a.offsets[e] + (tile - tstart[e]) * BN;
+                n = min(BN, a.offsets[e + 1] - r0);
+            } else {
+                r0 = tile * BN;
+                n = min(BN, a.nrows - r0);
             }
-        };
+            const int nsub = (n + 15) >> 4;
+            // Row-major weights: this lane's 8 elements of row m0 + i at k-offset
+            // 8 g of each 32-wide k-step.  Packed weights: the wave's 16 rows form
+            // one 1 KB block per k-step, lane l's fragment at 16 l bytes.
+            const size_t wrow = PACKED ? (static_cast<size_t>(e) * (a.M / 16) + m0 / 16) * (a.K / 32) * 512 + 8 * lane
+                                       : (static_cast<size_t>(e) * a.M + m0 + i) * a.K + 8 * g;
+            const uint16_t* pa = a.wa + wrow;
+            const uint16_t* pb = GATED ? a.wb + wrow : nullptr;
 
-        f32x4 acc_a[NSUB], acc_b[NSUB];
+            // token-row vectors this thread moves into LDS each chunk
+            const uint16_t* xsrc[RMAX];
+            int xdst[RMAX];
+            bool xon[RMAX];
 #pragma unroll
-        for (int s = 0; s < NSUB; ++s) {
-            acc_a[s] = f32x4{0.f, 0.f, 0.f, 0.f};
-            acc_b[s] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-        auto compute = [&](int buf, const bf16x8 (&A)[KS], const bf16x8 (&B)[KS]) __attribute__((always_inline)) {
-            const uint16_t* xb = xs[buf];
-#pragma unroll
-            for (int j = 0; j < KS; ++j) {
-#pragma unroll
-                for (int s = 0; s < NSUB; ++s) {
-                    if (s < nsub) {
-                        const bf16x8 X = *reinterpret_cast<const bf16x8*>(xb + (s * 16 + i) * LDS_ROW + 32 * j + 8 * g);
-                        acc_a[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[j], X, acc_a[s], 0, 0, 0);
-                        if constexpr (GATED)
-                            acc_b[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(B[j], X, acc_b[s], 0, 0, 0);
-                    }
-                }
+            for (int r = 0; r < RMAX; ++r) {
+                const int v = tid + NT * r;
+                const int row = v / VPR, col = v % VPR;
+                xon[r] = row < n;
+                const int srow = xon[r] ? (a.gather ? a.gather[r0 + row] : r0 + row) : 0;
+                xsrc[r] = a.src + static_cast<size_t>(srow) * a.K + kbeg + 8 * col;
+                xdst[r] = row * LDS_ROW + 8 * col;
             }
-        };
-
-        if constexpr (DEEP) {
-            // Token rows two chunks ahead: chunk c + 2's rows are loaded into
-            // one of two register sets while chunk c + 1's (loaded a chunk
-            // earlier) go to LDS, so no chunk waits on a token-row load it
-            // issued itself; weights one chunk ahead in two register sets.
-            // Every load is issued unconditionally (a conditional load leaves
-            // a merge the register allocator resolves with copies, and a copy
-            // waits for its load): past the last chunk the weight loads read
-            // a token row instead and the token loads read the last chunk
-            // again (valid, L2-resident, unused).
-            auto load_w_at = [&](int c, bf16x8 (&A)[KS], bf16x8 (&B)[KS]) __attribute__((always_inline)) {
-                const bool in = c < nch;
-                const int k = kbeg + (in ? c : 0) * KC;
+            // Every lane loads (rows past the tile read a valid row and are not
+            // stored), so xr stays in registers instead of private memory.
+            // (native vector type: HIP's uint4 struct would be copied with
+            // memcpy and kept in private memory)
+            bf16x8 xr[RMAX];
+            auto load_xr = [&](int c, bf16x8 (&R)[RMAX]) __attribute__((always_inline)) {
+#pragma unroll
+                for (int r = 0; r < RMAX; ++r) R[r] = ld16(xsrc[r] + c * KC);
+            };
+            auto store_xr = [&](int buf, const bf16x8 (&R)[RMAX]) __attribute__((always_inline)) {
+#pragma unroll
+                for (int r = 0; r < RMAX; ++r)
+                    if (xon[r]) *reinterpret_cast<bf16x8*>(&xs[buf][xdst[r]]) = R[r];
+            };
+            auto load_x = [&](int c) __attribute__((always_inline)) { load_xr(c, xr); };
+            auto store_x = [&](int buf) __attribute__((always_inline)) { store_xr(buf, xr); };
+            auto load_w = [&](int c, bf16x8 (&A)[KS], bf16x8 (&B)[KS]) __attribute__((always_inline)) {
+                const int k = kbeg + c * KC;
 #pragma unroll
                 for (int j = 0; j < KS; ++j) {
-                    const size_t o = PACKED ? static_cast<size_t>(k / 32 + j) * 512 : static_cast<size_t>(k + 32 * j);
-                    const uint16_t* qa = in ? pa + o : xsrc[0];
-                    A[j] = PACKED ? ld16_stream(qa) : ld16(qa);
-                    if constexpr (GATED) {
-                        const uint16_t* qb = in ? pb + o : xsrc[0];
-                        B[j] = PACKED ? ld16_stream(qb) : ld16(qb);
+                    if constexpr (PACKED) {
+                        const size_t o = static_cast<size_t>(k / 32 + j) * 512;
+                        A[j] = ld16_w<kStreamW>(pa + o);
+                        if constexpr (GATED) B[j] = ld16_w<kStreamW>(pb + o);
+                    } else {
+                        A[j] = ld16(pa + k + 32 * j);
+                        if constexpr (GATED) B[j] = ld16(pb + k + 32 * j);
                     }
                 }
             };
-            bf16x8 A0[KS], B0[KS], A1[KS], B1[KS], X0[RMAX], X1[RMAX];
-            load_xr(0, X0);
-            load_w_at(0, A0, B0);
-            load_xr(min(1, nch - 1), X1);
-            store_xr(0, X0);
-            lds_barrier();
-            // chunk c: weights in set c % 2, token rows in LDS buffer c % 2;
-            // issue token rows c + 2 into set c % 2 and weights c + 1 into set
-            // (c + 1) % 2, then move token set (c + 1) % 2 to LDS (c + 1) % 2
-            auto stage = [&](int c, const bf16x8 (&Ac)[KS], const bf16x8 (&Bc)[KS], bf16x8 (&An)[KS],
-                             bf16x8 (&Bn)[KS], bf16x8 (&Xn2)[RMAX], const bf16x8 (&Xn1)[RMAX],
-                             int cur) __attribute__((always_inline)) {
-                load_xr(min(c + 2, nch - 1), Xn2);
-                load_w_at(c + 1, An, Bn);
-                compute(cur, Ac, Bc);
-                if (c + 1 < nch) store_xr(cur ^ 1, Xn1);
-                lds_barrier();
-            };
-            for (int c = 0; c < nch; c += 2) {
-                stage(c, A0, B0, A1, B1, X0, X1, 0);
-                if (c + 1 >= nch) break;
-                stage(c + 1, A1, B1, A0, B0, X1, X0, 1);
-            }
-        } else {
-        // Two register sets in ping-pong: while the MFMAs consume one chunk's
-        // weights, the next chunk's are in flight in the other set (no
-        // register copies, so the loads are not waited for early).
-        bf16x8 A0[KS], B0[KS], A1[KS], B1[KS];
-        load_x(0);
-        load_w(0, A0, B0);
-        store_x(0);
-        lds_barrier();
-        for (int c = 0; c < nch; c += 2) {
-            const bool has1 = c + 1 < nch;
-            if (has1) {
-                load_x(c + 1);
-                load_w(c + 1, A1, B1);
-            }
-            compute(0, A0, B0);
-            if (has1) store_x(1);
-            lds_barrier();
-            if (!has1) break;
-            const bool has2 = c + 2 < nch;
-            if (has2) {
-                load_x(c + 2);
-                load_w(c + 2, A0, B0);
-            }
-            compute(1, A1, B1);
-            if (has2) store_x(0);
-            lds_barrier();
-        }
-        }
 
-        // result: lane holds weight rows m0 + 4g + q (q < 4) for token column s*16 + i
-        if constexpr (GATED) {
-            if (splits == 1) {
-#pragma unroll
-                for (int s = 0; s < NSUB; ++s) {
-                    const int c = s * 16 + i;
-                    if (c >= n) continue;
-                    store_h(a.h + static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g, acc_a[s], acc_b[s]);
-                }
-            } else {
-                // this slice's G/U partial sums (swiglu_reduce_kernel adds
-                // the slices in order and forms H)
-#pragma unroll
-                for (int s = 0; s < NSUB; ++s) {
-                    const int c = s * 16 + i;
-                    if (c >= n) continue;
-                    const size_t po = split * a.split_stride + static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g;
-                    *reinterpret_cast<float4*>(static_cast<float*>(a.out) + po) =
-                        make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
-                    *reinterpret_cast<float4*>(a.out2 + po) =
-                        make_float4(acc_b[s][0], acc_b[s][1], acc_b[s][2], acc_b[s][3]);
-                }
-            }
-        } else {
+            f32x4 acc_a[NSUB], acc_b[NSUB];
 #pragma unroll
             for (int s = 0; s < NSUB; ++s) {
-                const int c = s * 16 + i;
-                if (c >= n) continue;
-                float* op = static_cast<float*>(a.out) + split * a.split_stride +
-                            static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g;
-                *reinterpret_cast<float4*>(op) = make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
+                acc_a[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+                acc_b[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+            // Gated tiles read every populated sub-tile's token fragment before
+            // the first MFMA of a k-step and pin the reads there (an empty asm
+            // that takes them as inputs), so the LDS latency is paid once per
+            // k-step.  Left to itself the compiler sinks each read into its
+            // sub-tile's guard, behind the previous sub-tile's MFMAs: one full
+            // LDS round trip per sub-tile.  Rows of the last sub-tile past its
+            // tokens hold stale values that only reach output columns that are
+            // never stored.  The plain projection keeps the guarded reads: with
+            // one MFMA per read the pins cost it more than the latency they hide
+            // (measured).
+            auto compute = [&](int buf, const bf16x8 (&A)[KS], const bf16x8 (&B)[KS]) __attribute__((always_inline)) {
+                const uint16_t* xb = xs[buf];
+#pragma unroll
+                for (int j = 0; j < KS; ++j) {
+                    if constexpr (GATED) {
+                        bf16x8 X[NSUB];
+#pragma unroll
+                        for (int s = 0; s < NSUB; ++s)
+                            X[s] = s < nsub ? *reinterpret_cast<const bf16x8*>(xb + (s * 16 + i) * LDS_ROW + 32 * j + 8 * g)
+                                            : bf16x8{};
+#pragma unroll
+                        for (int s = 0; s < NSUB; ++s) asm volatile("" ::"v"(X[s]));
+#pragma unroll
+                        for (int s = 0; s < NSUB; ++s) {
+                            if (s < nsub) {
+                                acc_a[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[j], X[s], acc_a[s], 0, 0, 0);
+                                acc_b[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(B[j], X[s], acc_b[s], 0, 0, 0);
+                            }
+                        }
+                    } else {
+#pragma unroll
+                        for (int s = 0; s < NSUB; ++s) {
+                            if (s < nsub) {
+                                const bf16x8 X =
+                                    *reinterpret_cast<const bf16x8*>(xb + (s * 16 + i) * LDS_ROW + 32 * j + 8 * g);
+                                acc_a[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[j], X, acc_a[s], 0, 0, 0);
+                            }
+                        }
+                    }
+                }
+            };
+
+            if constexpr (DEEP) {
+                // Token rows two chunks ahead: chunk c + 2's rows are loaded into
+                // one of two register sets while chunk c + 1's (loaded a chunk
+                // earlier) go to LDS, so no chunk waits on a token-row load it
+                // issued itself; weights one chunk ahead in two register sets.
+                // Every load is issued unconditionally (a conditional load leaves
+                // a merge the register allocator resolves with copies, and a copy
+                // waits for its load): past the last chunk the weight loads read
+                // a token row instead and the token loads read the last chunk
+                // again (valid, L2-resident, unused).
+                auto load_w_at = [&](int c, bf16x8 (&A)[KS], bf16x8 (&B)[KS]) __attribute__((always_inline)) {
+                    const bool in = c < nch;
+                    const int k = kbeg + (in ? c : 0) * KC;
+#pragma unroll
+                    for (int j = 0; j < KS; ++j) {
+                        const size_t o = PACKED ? static_cast<size_t>(k / 32 + j) * 512 : static_cast<size_t>(k + 32 * j);
+                        const uint16_t* qa = in ? pa + o : xsrc[0];
+                        A[j] = PACKED ? ld16_w<kStreamW>(qa) : ld16(qa);
+                        if constexpr (GATED) {
+                            const uint16_t* qb = in ? pb + o : xsrc[0];
+                            B[j] = PACKED ? ld16_w<kStreamW>(qb) : ld16(qb);
+                        }
+                    }
+                };
+                bf16x8 A0[KS], B0[KS], A1[KS], B1[KS], X0[RMAX], X1[RMAX];
+                load_xr(0, X0);
+                load_w_at(0, A0, B0);
+                load_xr(min(1, nch - 1), X1);
+                store_xr(0, X0);
+                lds_barrier();
+                // chunk c: weights in set c % 2, token rows in LDS buffer c % 2;
+                // issue token rows c + 2 into set c % 2 and weights c + 1 into set
+                // (c + 1) % 2, then move token set (c + 1) % 2 to LDS (c + 1) % 2
+                auto stage = [&](int c, const bf16x8 (&Ac)[KS], const bf16x8 (&Bc)[KS], bf16x8 (&An)[KS],
+                                 bf16x8 (&Bn)[KS], bf16x8 (&Xn2)[RMAX], const bf16x8 (&Xn1)[RMAX],
+                                 int cur) __attribute__((always_inline)) {
+                    load_xr(min(c + 2, nch - 1), Xn2);
+                    load_w_at(c + 1, An, Bn);
+                    compute(cur, Ac, Bc);
+                    if (c + 1 < nch) store_xr(cur ^ 1, Xn1);
+                    lds_barrier();
+                };
+                for (int c = 0; c < nch; c += 2) {
+                    stage(c, A0, B0, A1, B1, X0, X1, 0);
+                    if (c + 1 >= nch) break;
+                    stage(c + 1, A1, B1, A0, B0, X1, X0, 1);
+                }
+            } else {
+            // Two register sets in ping-pong: while the MFMAs consume one chunk's
+            // weights, the next chunk's are in flight in the other set (no
+            // register copies, so the loads are not waited for early).
+            bf16x8 A0[KS], B0[KS], A1[KS], B1[KS];
+            load_x(0);
+            load_w(0, A0, B0);
+            store_x(0);
+            lds_barrier();
+            for (int c = 0; c < nch; c += 2) {
+                const bool has1 = c + 1 < nch;
+                if (has1) {
+                    load_x(c + 1);
+                    load_w(c + 1, A1, B1);
+                }
+                compute(0, A0, B0);
+                if (has1) store_x(1);
+                lds_barrier();
+                if (!has1) break;
+                const bool has2 = c + 2 < nch;
+                if (has2) {
+                    load_x(c + 2);
+                    load_w(c + 2, A0, B0);
+                }
+                compute(1, A1, B1);
+                if (has2) store_x(0);
+                lds_barrier();
+            }
+            }
+
+            // result: lane holds weight rows m0 + 4g + q (q < 4) for token column s*16 + i
+            if constexpr (GATED) {
+                if (splits == 1) {
+#pragma unroll
+                    for (int s = 0; s < NSUB; ++s) {
+                        const int c = s * 16 + i;
+                        if (c >= n) continue;
+                        store_h(a.h + static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g, acc_a[s], acc_b[s]);
+                    }
+                } else {
+                    // this slice's G/U partial sums (swiglu_reduce_kernel adds
+                    // the slices in order and forms H)
+#pragma unroll
+                    for (int s = 0; s < NSUB; ++s) {
+                        const int c = s * 16 + i;
+                        if (c >= n) continue;
+                        const size_t po = split * a.split_stride + static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g;
+                        *reinterpret_cast<float4*>(static_cast<float*>(a.out) + po) =
+                            make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
+                        *reinterpret_cast<float4*>(a.out2 + po) =
+                            make_float4(acc_b[s][0], acc_b[s][1], acc_b[s][2], acc_b[s][3]);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int s = 0; s < NSUB; ++s) {
+                    const int c = s * 16 + i;
+                    if (c >= n) continue;
+                    float* op = static_cast<float*>(a.out) + split * a.split_stride +
+                                static_cast<size_t>(r0 + c) * a.M + m0 + 4 * g;
+                    *reinterpret_cast<float4*>(op) = make_float4(acc_a[s][0], acc_a[s][1], acc_a[s][2], acc_a[s][3]);
+                }
             }
         }
+    };
+    if constexpr (NSUB >= EAT_CACHE_MIN_NSUB) {
+        if (stream_w) run(std::true_type{});
+        else run(std::false_type{});
+    } else {
+        run(std::true_type{});
     }
 }
 
