@@ -80,8 +80,9 @@ __device__ __forceinline__ float wave_max(float v) {
 // Tile table of expert-major row segments: tstart[g] = sum over h < g of
 // ceil((offsets[h+1] - offsets[h]) / bm), for g = 0..groups.  Wave 0 reads
 // one segment per lane and scans 64 at a time (integer sums, so the order
-// does not matter); every thread of the workgroup must call it.  `used`, if
-// given (LDS), receives the number of non-empty segments.
+// does not matter); every thread of the workgroup must call it.  With
+// COUNT, `used` (LDS) receives the number of non-empty segments.
+template <bool COUNT = false>
 __device__ __forceinline__ void tile_starts(const int32_t* offsets, int groups, int bm, int* tstart,
                                             int* used = nullptr) {
     if (threadIdx.x < kWave) {
@@ -90,7 +91,7 @@ __device__ __forceinline__ void tile_starts(const int32_t* offsets, int groups, 
         for (int g0 = 0; g0 < groups; g0 += kWave) {
             const int g = g0 + lane;
             int c = g < groups ? (offsets[g + 1] - offsets[g] + bm - 1) / bm : 0;
-            nonempty += __popcll(__ballot(c > 0));
+            if constexpr (COUNT) nonempty += __popcll(__ballot(c > 0));
 #pragma unroll
             for (int o = 1; o < kWave; o <<= 1) {
                 const int u = __shfl_up(c, o, kWave);
@@ -101,7 +102,7 @@ __device__ __forceinline__ void tile_starts(const int32_t* offsets, int groups, 
         }
         if (lane == 0) {
             tstart[0] = 0;
-            if (used) *used = nonempty;
+            if constexpr (COUNT) *used = nonempty;
         }
     }
     __syncthreads();

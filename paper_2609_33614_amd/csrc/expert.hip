@@ -258,7 +258,7 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
 
     int ntiles, used = 1;
     if (a.offsets) {
-        tile_starts(a.offsets, a.groups, BN, tstart, &used_groups);
+        tile_starts<true>(a.offsets, a.groups, BN, tstart, &used_groups);
         ntiles = tstart[a.groups];
         used = used_groups;
     } else {

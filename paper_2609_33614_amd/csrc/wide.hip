@@ -79,7 +79,9 @@ struct WideArgs {
 // index with the row's line number spreads those 16 rows over distinct
 // banks: (r >> 1) & 7 for 128-byte rows, (r >> 2) & 3 for 64-byte rows.
 constexpr int kRowsPerLine = 256 / kRB;
-__device__ __forceinline__ int swz(int r) { return (r / kRowsPerLine) & (kVPR - 1); }
+// (unsigned: a signed division by the power of two costs a rounding fix-up
+// and, in the wide kernel, the registers that then spill)
+__device__ __forceinline__ int swz(int r) { return (static_cast<unsigned>(r) / kRowsPerLine) & (kVPR - 1); }
 __device__ __forceinline__ int wswz(int r, int v) { return r * kRB + ((v ^ swz(r)) << 4); }
 
 constexpr int kNB = (kWM + kWN) / kRPB;       // 1 KB DMA blocks per stage
