@@ -118,9 +118,9 @@ hipError_t launch_f32_pair(F32Args a, int64_t rows_cap, hipStream_t s,
 #ifndef EAT_SPLIT_MIN_K
 #define EAT_SPLIT_MIN_K 384
 #endif
-// The gated projection pays for its slices with fp32 partials that the last
-// slice adds up, so it only splits grids that would leave most of the chip
-// idle.
+// The gated projection pays for its slices with fp32 G and U partials that a
+// second kernel adds up (swiglu_reduce_kernel), so it only splits grids that
+// would leave most of the chip idle.
 #ifndef EAT_UP_SPLIT_WAVES
 #define EAT_UP_SPLIT_WAVES 1024
 #endif
@@ -196,9 +196,6 @@ __device__ __forceinline__ bf16x8 ld16_w(const uint16_t* p) {
     else return ld16(p);
 }
 
-// Slices the gated projection may use (the last slice reads the others'
-// partials into registers).
-constexpr int kMaxUpSplits = EAT_UP_SPLIT_MAX;
 
 
 // H = bf16(silu(G) * U) for a lane's 4 consecutive features.
