@@ -541,6 +541,8 @@ def main(argv=None) -> int:
                     help="skip the decode of the fine-grained (B=256) and shared-expert (B=128) layers")
     ap.add_argument("--stack-steps", type=int, default=1024)
     ap.add_argument("--only-stack", action="store_true", help="time only the 16-layer stack and print its JSON")
+    ap.add_argument("--only-decode-layer", default="", metavar="LAYER",
+                    help="time only one decode_layers workload (finegrained or shared) and print its JSON")
     ap.add_argument("--only-prefill", default="", metavar="LAYER",
                     help="time only the prefill of LAYER (finegrained or shared) in --modes and print "
                          "its JSON object (for kernel traces of the MFMA-bound path)")
@@ -569,6 +571,13 @@ def main(argv=None) -> int:
         res = run_stack(args.stack_steps, 16, ev, modes=[m for m in args.modes.split(",") if m])
         ev.close()
         print(json.dumps({"stack": res}), flush=True)
+        return 0
+    if args.only_decode_layer:
+        ev = HipEvents()
+        res = run_decode(args.only_decode_layer, None, args.warmup, ev,
+                         modes=[m for m in args.modes.split(",") if m])
+        ev.close()
+        print(json.dumps({"decode_layers": [res]}), flush=True)
         return 0
     if args.only_prefill:
         ev = HipEvents()

@@ -26,6 +26,14 @@ Prefill (MFMA-bound) summary of the wide tile kernels, from a trace of
 
     python profile_summary.py --prefill --trace T --bench-json B.json --name NAME
 
+One more decode layer (per-step kernel breakdown of bench's decode_layers
+workload, e.g. the fine-grained layer's 256-token EAT decode), from a trace of
+
+  TRACE   rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run --
+              python3 bench.py --only-decode-layer LAYER --modes eat
+
+    python profile_summary.py --layer-decode --trace T --bench-json B.json --name NAME
+
 Stacked-layer decode (per-layer kernel breakdown), from a trace of
 
   TRACE   rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run --
@@ -124,6 +132,69 @@ def prefill_summary(args) -> int:
     return 0
 
 
+def per_kernel(trace_dir):
+    """Durations (us) of every eat:: kernel launch of a trace, in launch order."""
+    trace = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_trace.csv"))))
+    trace.sort(key=lambda x: int(x["Start_Timestamp"]))
+    per = {}
+    for x in trace:
+        name = x["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0].replace("void ", "")
+        if name.startswith("eat::") and "pack_kernel" not in name and "reset_accounts" not in name:
+            per.setdefault(name, []).append((int(x["End_Timestamp"]) - int(x["Start_Timestamp"])) / 1e3)
+    return per
+
+
+def layer_decode_summary(args) -> int:
+    """Per-step kernel breakdown of one traced decode_layers workload (one
+    routing mode), with the gated expert kernel's achieved MFMA rate and
+    weight bandwidth on its algorithmic flops and bytes."""
+    bench = json.loads(open(args.bench_json).read().strip().splitlines()[-1])
+    dl = bench["decode_layers"][0]
+    modes = [m for m in ("eat", "topk", "topp") if m in dl]
+    assert len(modes) == 1, "trace one routing mode at a time"
+    r = dl[modes[0]]
+    B, steps, d, F = dl["batch"], dl["steps"], dl["d_model"], dl["d_ffn"]
+    warm = args.warmup
+    per = per_kernel(args.trace)
+    md = os.path.join(ROOT, "profiles", args.name + ".md")
+    rows = []
+    for name, durs in per.items():
+        n_per = len(durs) / (steps + warm)
+        timed = durs[-int(round(n_per * steps)):] if n_per > 0 else durs
+        avg = statistics.mean(timed)
+        rows.append((avg * n_per, name, n_per, avg))
+    up = [x for x in rows if x[1].startswith("eat::stream_kernel<true") or x[1].startswith("eat::wide_kernel<true")]
+    sk = r["mean_activated_experts"] * B
+    with open(md, "w") as f:
+        f.write(f"# {args.name}\n\n")
+        f.write(f"Workload: {dl['workload']}, batch {B}, d_model {d}, {dl['experts']} experts of width {F}"
+                f"{', always-on expert of width ' + str(dl['d_shared']) if dl.get('d_shared') else ''}, "
+                f"K={dl['top_k']}, {modes[0]} routing, {steps} timed steps after {warm} warm-up steps from zero "
+                f"accounts; {r['mean_activated_experts']} experts per token, "
+                f"{r['mean_experts_touched_per_step']} touched per step, MI355X.\n\n")
+        f.write("Commands (from the repository root):\n\n```\n")
+        f.write(f"rocprofv3 --kernel-trace --stats --output-format csv -d TRACE -o run -- "
+                f"python3 bench.py --only-decode-layer {dl['workload'].split()[0]} --modes {modes[0]}\n")
+        f.write(f"python3 profile_summary.py --layer-decode --trace TRACE --bench-json TRACED_BENCH.json "
+                f"--name {args.name}\n```\n\n")
+        f.write(f"Step time in the traced run (HIP events): {r['ms_per_step'] * 1e3:.1f} us; "
+                f"{r['tokens_per_s']:.0f} tokens/s.\n\n")
+        f.write("| kernel | launches per step | avg us per launch | us per step |\n|---|---|---|---|\n")
+        for tot, name, n_per, avg in sorted(rows, reverse=True):
+            f.write(f"| `{name}` | {n_per:.2f} | {avg:.2f} | {tot:.2f} |\n")
+        f.write(f"| **sum** | | | **{sum(x[0] for x in rows):.1f}** |\n")
+        if up:
+            us = sum(x[0] for x in up)
+            fl = 4.0 * d * F * sk
+            wb = r["mean_experts_touched_per_step"] * 4.0 * d * F
+            f.write(f"\nRouted up/gate per step: {us:.1f} us for {fl / 1e9:.2f} GFLOP (4 d F sum(k), "
+                    f"sum(k) = {sk:.0f}) = {fl / us / 1e6:.0f} TFLOP/s = "
+                    f"{fl / us / 1e6 / BF16_PEAK_TFLOPS * 100:.1f}% of the 2.5 PF bf16 peak; weights of the "
+                    f"experts touched {wb / 1e6:.1f} MB = {wb / us / 1e6:.2f} TB/s.\n")
+    print(open(md).read())
+    return 0
+
+
 def stack_summary(args) -> int:
     """Average duration of every kernel of the traced stacked-layer decode
     per launch and per layer of a timed step (16 warm-up steps, then the
@@ -134,14 +205,8 @@ def stack_summary(args) -> int:
     assert len(modes) == 1, "trace one routing mode at a time"
     r = st[modes[0]]
     layers, steps = st["layers"], st["steps"]
-    trace = list(csv.DictReader(open(os.path.join(args.trace, "run_kernel_trace.csv"))))
-    trace.sort(key=lambda x: int(x["Start_Timestamp"]))
     # the timed steps' launches are the last ones of the kernels a step runs
-    per = {}
-    for x in trace:
-        name = x["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0].replace("void ", "")
-        if name.startswith("eat::") and "pack_kernel" not in name and "reset_accounts" not in name:
-            per.setdefault(name, []).append((int(x["End_Timestamp"]) - int(x["Start_Timestamp"])) / 1e3)
+    per = per_kernel(args.trace)
     total_steps = steps + 16
     md = os.path.join(ROOT, "profiles", args.name + ".md")
     with open(md, "w") as f:
@@ -182,11 +247,15 @@ def main(argv=None) -> int:
     ap.add_argument("--prefill", action="store_true", help="summarise a prefill trace (wide tile kernels)")
     ap.add_argument("--reps", type=int, default=10, help="timed prefill calls in the traced run")
     ap.add_argument("--stack", action="store_true", help="summarise a stacked-layer decode trace")
+    ap.add_argument("--layer-decode", action="store_true", help="summarise a decode_layers trace")
+    ap.add_argument("--warmup", type=int, default=16, help="warm-up steps of the traced decode_layers run")
     args = ap.parse_args(argv)
     if args.prefill:
         return prefill_summary(args)
     if args.stack:
         return stack_summary(args)
+    if args.layer_decode:
+        return layer_decode_summary(args)
     assert args.fetch and args.write, "--fetch and --write are needed for the decode summary"
 
     bench = json.loads(open(args.bench_json).read().strip().splitlines()[-1])
