@@ -512,6 +512,42 @@ def cpu_baseline(shape, w_host, xs_host, B, max_seconds: float, single_seconds: 
     return out
 
 
+def oracle_workloads(decode_seconds: float):
+    """The oracle (unchanged) on the fine-grained and shared-expert layers:
+    EAT decode steps from zero accounts (at least one, until
+    `decode_seconds` have passed) at the layer's decode batch, then one
+    prefill call at its prefill size, each on the host's BLAS threads."""
+    import oracle as O
+    from workload import SHAPES, HiddenStream, make_layer_weights
+
+    out = []
+    for name, T in (("finegrained", 4096), ("shared", 8192)):
+        shape = SHAPES[name]
+        B = shape.decode_batches[0]
+        w = make_layer_weights(shape)
+        prm = O.Params(mode=O.MODE_EAT, K=shape.K, inv_temp=shape.inv_temp)
+        xs = HiddenStream(shape, B).steps(64)
+        acc = O.zero_accounts(shape.E)
+        t = time.time()
+        n = 0
+        while n < xs.shape[0]:
+            acc = O.moe_step(xs[n], w, acc, None, prm).acc
+            n += 1
+            if time.time() - t >= decode_seconds:
+                break
+        dt = time.time() - t
+        xp = HiddenStream(shape, T).steps(1)[0]
+        t = time.time()
+        O.moe_step(xp, w, O.zero_accounts(shape.E), None, prm)
+        dp = time.time() - t
+        out.append({"workload": f"{name} layer", "decode": {"value": round(n * B / dt, 3), "unit": "tokens/s",
+                                                           "sample": f"{n} EAT step(s) of B={B}, {dt:.1f} s"},
+                    "prefill": {"value": round(T / dp, 3), "unit": "tokens/s",
+                                "sample": f"one EAT call of {T} tokens, {dp:.1f} s"}})
+        del w
+    return out
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -523,6 +559,9 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--cpu-single-seconds", type=float, default=10.0,
                     help="seconds of the one-BLAS-thread oracle timing (0 = skip)")
+    ap.add_argument("--cpu-workload-seconds", type=float, default=3.0,
+                    help="seconds of oracle decode steps on each of the fine-grained and shared-expert layers, "
+                         "each followed by one prefill call (0 = skip both)")
     ap.add_argument("--modes", default="eat,topk,topp", help="routing modes to time (eat first)")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill (MFMA-bound) measurement")
     ap.add_argument("--prefill-reps", type=int, default=10)
@@ -698,6 +737,10 @@ def main(argv=None) -> int:
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         cpu = cpu_baseline(shape, w_host, xs_host[W:], B, args.cpu_seconds, args.cpu_single_seconds)
+        if args.cpu_workload_seconds > 0:
+            log("timing the CPU oracle on the fine-grained and shared-expert layers")
+            del w_host
+            cpu["other_workloads"] = oracle_workloads(args.cpu_workload_seconds)
 
     out = {
         "metric": METRIC,

@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cstring>
 #include <cmath>
 #include <functional>
 #include <new>
@@ -508,7 +509,11 @@ eat_status_t eat_ppl_trend(const void* h, int32_t S, int32_t d, const void* w_vo
 }
 
 const char* eat_status_string(eat_status_t s) {
-    switch (s) {
+    // a C caller may pass any int: read the argument's bits, not the enum
+    // (a C++ enum value outside its enumerators' range is undefined)
+    int v;
+    std::memcpy(&v, &s, sizeof v);
+    switch (v) {
         case EAT_OK: return "ok";
         case EAT_ERR_INVALID_ARG: return "invalid argument";
         case EAT_ERR_UNSUPPORTED: return "unsupported shape or dtype";
