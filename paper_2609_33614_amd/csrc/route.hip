@@ -16,7 +16,10 @@
 // reweighting (Sec. 3.5) and the mode's selection
 // (EAT: history score S_h from the account snapshot in fp64 (Eq. 1),
 // importance (Eq. 2), threshold (Eq. 3-5, Sec. 3.3), activation set (Eq. 6);
-// Top-K; Top-P) and the renormalisation of Eq. 7-8.
+// Top-K; Top-P) and the renormalisation of Eq. 7-8.  Orderings over a
+// token's experts (the quantile bounds' ranks, Top-K / Top-P ranks, the
+// candidates that beat a candidate) are counts against the other lanes'
+// values, read back from LDS as broadcasts.
 // All reductions use fixed butterfly or sequential orders, so results are
 // bit-reproducible run to run.
 #include <math.h>
@@ -83,6 +86,60 @@ __device__ __forceinline__ float value_at_rank(const float (&v)[J], const int (&
         }
     }
     return out;
+}
+
+typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Lanes of one wave exchanging values through LDS: every lane's stores are
+// ordered before the loads that follow (a wave's LDS operations run in
+// issue order; the fences keep the compiler from moving them).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Order-preserving bits of a non-NaN float: a < b exactly when
+// ord_bits(a) < ord_bits(b); -0 and +0 (equal values) map alike.
+__device__ __forceinline__ uint32_t ord_bits(float f) {
+    const uint32_t u = f == 0.f ? 0u : __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Ranks of a token's E values (lane l of group j holds expert 64 j + l):
+// how many values come before each one, ascending (ASC) or descending, with
+// equal values in expert-index order, so the ranks are a permutation of
+// 0..E-1.  Only for values without NaN.  Each value becomes one 64-bit key
+// (order-preserving bits, then the expert index); the wave's keys go to
+// `kbuf` (this wave's 64 J LDS entries, 16-byte aligned), and every lane
+// counts the keys below its own, reading them two at a time from one address
+// for the whole wave (a broadcast: two compares per value, against a lane
+// read and three hazard-separated scalar steps per value for the readlane
+// loop).  `srt` (64 J floats of LDS) receives the values in rank order.
+template <int J, bool ASC>
+__device__ __forceinline__ void rank_by_keys(const float (&v)[J], const bool (&valid)[J], int E,
+                                             uint64_t* kbuf, float* srt, int (&rank)[J]) {
+    const int lane = lane_id();
+    uint64_t key[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        const uint32_t o = ASC ? ord_bits(v[j]) : ~ord_bits(v[j]);
+        key[j] = valid[j] ? (static_cast<uint64_t>(o) << 32) | static_cast<uint32_t>(64 * j + lane) : ~0ull;
+        kbuf[64 * j + lane] = key[j];
+        rank[j] = 0;
+    }
+    wave_lds_sync();
+    // an odd E reads one entry past it: an all-ones key, below no key
+    for (int l = 0; l < E; l += 2) {
+        const u64x2 q = *reinterpret_cast<const u64x2*>(kbuf + l);
+#pragma unroll
+        for (int j = 0; j < J; ++j) rank[j] += static_cast<int>(q.x < key[j]) + static_cast<int>(q.y < key[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+        if (valid[j]) srt[rank[j]] = v[j];
+    wave_lds_sync();
 }
 
 template <typename XT, int NT, int TT>
@@ -194,6 +251,8 @@ __device__ __forceinline__ float wave_sum_j(const float (&v)[J]) {
 template <int J>
 __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
     __shared__ float sh[64 * J];
+    __shared__ __align__(16) uint64_t kb[kSelWaves][64 * J];   // per-wave rank keys
+    __shared__ __align__(16) float srt[kSelWaves][64 * J];     // per-wave values in rank order
     const int lane = lane_id();
     const int wave = threadIdx.x / kWave;
     const int E = a.E;
@@ -289,6 +348,18 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
         for (int j = 0; j < J; ++j) p[j] = p[j] / den;
     }
 
+    // Without NaN among the token's weights the ranks below come from LDS
+    // keys; a token with NaN weights keeps the lane-by-lane comparisons, whose
+    // treatment of NaN (it compares as neither smaller nor larger, so it
+    // takes rank 0 and the ranks of the others close up) is the documented
+    // rule for non-finite tokens.
+    uint64_t nan_lanes = 0;
+#pragma unroll
+    for (int j = 0; j < J; ++j) nan_lanes |= ballot(valid[j] && p[j] != p[j]);
+    const bool by_keys = nan_lanes == 0;
+    uint64_t* const kbw = kb[wave];
+    float* const srtw = srt[wave];
+
     uint64_t msk[J];
 #pragma unroll
     for (int j = 0; j < J; ++j) msk[j] = 0;
@@ -310,16 +381,20 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
         const float tau_s = a.kappa1 * (f * tau) + a.kappa2 * tau;
         // bounds: q_lo / q_hi points of the sorted routing weights
         int rank[J];
+        if (by_keys) {
+            rank_by_keys<J, true>(p, valid, E, kbw, srtw, rank);
+        } else {
 #pragma unroll
-        for (int j = 0; j < J; ++j) rank[j] = 0;
+            for (int j = 0; j < J; ++j) rank[j] = 0;
 #pragma unroll
-        for (int jj = 0; jj < J; ++jj) {
-            const int nl = min(64, E - 64 * jj);
-            for (int l = 0; l < nl; ++l) {
-                const float pv = read_lane(p[jj], l);
-                const int ev = 64 * jj + l;
+            for (int jj = 0; jj < J; ++jj) {
+                const int nl = min(64, E - 64 * jj);
+                for (int l = 0; l < nl; ++l) {
+                    const float pv = read_lane(p[jj], l);
+                    const int ev = 64 * jj + l;
 #pragma unroll
-                for (int j = 0; j < J; ++j) rank[j] += (pv < p[j]) || (pv == p[j] && ev < 64 * j + lane);
+                    for (int j = 0; j < J; ++j) rank[j] += (pv < p[j]) || (pv == p[j] && ev < 64 * j + lane);
+                }
             }
         }
         float qv[2];
@@ -329,8 +404,8 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
             const float h = qs[qi] * static_cast<float>(E - 1);
             const int lo = static_cast<int>(floorf(h));
             const int hi = lo + 1 < E ? lo + 1 : E - 1;
-            const float vlo = value_at_rank<J>(p, rank, lo, valid);
-            const float vhi = value_at_rank<J>(p, rank, hi, valid);
+            const float vlo = by_keys ? srtw[lo] : value_at_rank<J>(p, rank, lo, valid);
+            const float vhi = by_keys ? srtw[hi] : value_at_rank<J>(p, rank, hi, valid);
             qv[qi] = vlo + (h - static_cast<float>(lo)) * (vhi - vlo);
         }
         const float tau_final = fminf(fmaxf(tau_s, qv[0]), qv[1]);
@@ -360,33 +435,49 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
 #pragma unroll
             for (int j = 0; j < J; ++j) msk[j] = cand[j];
         } else {
-            // keep the candidates beaten (strictly) by fewer than K others
+            // keep the candidates beaten (strictly) by fewer than K others:
+            // each lane counts the candidates' order-preserving importance
+            // bits above its own (a candidate's importance exceeds the
+            // threshold, so it is never NaN; other lanes store 0, below every
+            // candidate's bits), four at a time from LDS broadcasts
+            uint32_t* const ib = reinterpret_cast<uint32_t*>(kbw);
+            uint32_t ki[J];
             int beaten[J];
 #pragma unroll
-            for (int j = 0; j < J; ++j) beaten[j] = 0;
+            for (int j = 0; j < J; ++j) {
+                ki[j] = ((cand[j] >> lane) & 1ull) ? ord_bits(I[j]) : 0u;
+                ib[64 * j + lane] = ki[j];
+                beaten[j] = 0;
+            }
+            wave_lds_sync();
+            // entries up to E rounded to 4 hold 0 (lanes past E)
+            for (int l = 0; l < E; l += 4) {
+                const u32x4 q = *reinterpret_cast<const u32x4*>(ib + l);
 #pragma unroll
-            for (int jj = 0; jj < J; ++jj)
-                for (uint64_t rest = cand[jj]; rest; rest &= rest - 1) {
-                    const float iv = read_lane(I[jj], __builtin_ctzll(rest));
-#pragma unroll
-                    for (int j = 0; j < J; ++j) beaten[j] += iv > I[j];
-                }
+                for (int j = 0; j < J; ++j)
+                    beaten[j] += static_cast<int>(q.x > ki[j]) + static_cast<int>(q.y > ki[j]) +
+                                 static_cast<int>(q.z > ki[j]) + static_cast<int>(q.w > ki[j]);
+            }
 #pragma unroll
             for (int j = 0; j < J; ++j) msk[j] = ballot(valid[j] && ((cand[j] >> lane) & 1ull) && beaten[j] < a.K);
         }
     } else {
         // descending rank, ties to the lower expert index
         int rank[J];
+        if (by_keys) {
+            rank_by_keys<J, false>(p, valid, E, kbw, srtw, rank);
+        } else {
 #pragma unroll
-        for (int j = 0; j < J; ++j) rank[j] = 0;
+            for (int j = 0; j < J; ++j) rank[j] = 0;
 #pragma unroll
-        for (int jj = 0; jj < J; ++jj) {
-            const int nl = min(64, E - 64 * jj);
-            for (int l = 0; l < nl; ++l) {
-                const float pv = read_lane(p[jj], l);
-                const int ev = 64 * jj + l;
+            for (int jj = 0; jj < J; ++jj) {
+                const int nl = min(64, E - 64 * jj);
+                for (int l = 0; l < nl; ++l) {
+                    const float pv = read_lane(p[jj], l);
+                    const int ev = 64 * jj + l;
 #pragma unroll
-                for (int j = 0; j < J; ++j) rank[j] += (pv > p[j]) || (pv == p[j] && ev < 64 * j + lane);
+                    for (int j = 0; j < J; ++j) rank[j] += (pv > p[j]) || (pv == p[j] && ev < 64 * j + lane);
+                }
             }
         }
         int kk;
@@ -397,7 +488,7 @@ __global__ __launch_bounds__(256) void select_kernel(RouteArgs a) {
             float run = 0.f;
             kk = E;
             for (int r = 0; r < E; ++r) {
-                run += value_at_rank<J>(p, rank, r, valid);
+                run += by_keys ? srtw[r] : value_at_rank<J>(p, rank, r, valid);
                 if (run >= a.top_p) { kk = r + 1; break; }
             }
             if (a.top_p_cap > 0 && kk > a.top_p_cap) kk = a.top_p_cap;
