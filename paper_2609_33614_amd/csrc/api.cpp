@@ -81,7 +81,7 @@ Workspace plan_workspace(const eat_ctx& c, int32_t T) {
     w.h = take(rows * p.d_ffn * es);
     w.gu = take(w.up_splits > 1 ? 2 * static_cast<size_t>(w.up_splits) * rows * p.d_ffn * 4 : 0);
     w.yp = take(static_cast<size_t>(w.splits) * rows * p.d_model * 4);
-    w.nrm = take(rows * static_cast<size_t>(combine_chunks(p)) * 4);
+    w.nrm = take(rows * static_cast<size_t>(norm_parts(p, T)) * 4);
     w.shared_splits = p.d_shared ? shared_splits(p, T) : 1;
     w.shared_up_splits = p.d_shared ? shared_up_splits(p, T) : 1;
     w.hs = take(p.d_shared ? t * p.d_shared * es : 0);
@@ -275,8 +275,8 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
             e = eat::launch_experts_bf16(p, T, w.rows, static_cast<const uint16_t*>(x),
                                          static_cast<const uint16_t*>(w1), static_cast<const uint16_t*>(w3),
                                          static_cast<const uint16_t*>(w2), b.offsets, b.tok_idx,
-                                         static_cast<uint16_t*>(b.h), b.gu, b.yp, up_splits_dev, down_splits_dev, stream,
-                                         [&]() { mark(EAT_STAGE_UP); });
+                                         static_cast<uint16_t*>(b.h), b.gu, b.yp, b.nrm2, up_splits_dev,
+                                         down_splits_dev, stream, [&]() { mark(EAT_STAGE_UP); });
         else
             e = eat::launch_experts_f32(p, T, w.rows, static_cast<const float*>(x),
                                         static_cast<const float*>(w1), static_cast<const float*>(w3),
@@ -298,12 +298,13 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
     mark(EAT_STAGE_SHARED);
     // the down projection's slices: chosen on the device when it could take several
     const int32_t* splits_dev = bf16 && w.splits > 1 ? down_splits_dev : nullptr;
+    const bool rows16 = bf16 && eat::rows_bf16(p, T);
     if (e == hipSuccess)
         e = eat::launch_combine(p, T, b.mask, b.gate, b.inv, b.yp, shared ? b.ys : nullptr, residual, y, b.nrm2,
-                                w.splits, w.rows * p.d_model, splits_dev, stream);
+                                w.splits, w.rows * p.d_model, splits_dev, rows16, stream);
     mark(EAT_STAGE_COMBINED);
     if (e == hipSuccess && p.mode == EAT_MODE_EAT)
-        e = eat::launch_update_accounts(p, b.offsets, b.tok_idx, b.prob, b.nrm2, acc, stream);
+        e = eat::launch_update_accounts(p, b.offsets, b.tok_idx, b.prob, b.nrm2, eat::norm_parts(p, T), acc, stream);
     mark(EAT_STAGE_END);
     return e;
 }

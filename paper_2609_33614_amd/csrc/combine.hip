@@ -4,8 +4,11 @@
 // rows in increasing expert order, adds the split-K partials of each row (in
 // split order), writes each row slice's sum of squares, and accumulates
 // y_t = sum_e g_norm,t,e o_t,e (+ shared expert) (+ a residual row) in fp32
-// (Eq. 7-8 and the weighted fusion of Sec. 3.4).  No atomics: every output
-// element has one writer and a fixed summation order.
+// (Eq. 7-8 and the weighted fusion of Sec. 3.4).  After a prefill-sized down
+// projection the rows come in bf16 with their sums of squares already taken
+// (from the projection's fp32 accumulators), which halves the bytes this
+// kernel reads.  No atomics: every output element has one writer and a
+// fixed summation order.
 //
 // mix_norm: between stacked layers, h' = bf16(sum of the mixing GEMM's
 // split partials) and the next layer's input u = bf16(h' / rms(h')), one
@@ -15,7 +18,8 @@
 // row segment reduced in fp64:
 //   N += n_e,  P_total += sum of the rows' router probabilities,
 //   C_s = (1 - alpha) C_s + alpha * mean row norm,
-// each row norm being sqrt of its slices' sums of squares added in order.
+// each row norm being sqrt of its partial sums of squares (the combine's
+// slices, or the prefill down projection's 32-feature parts) added in order.
 // (Doing it in the combine's last workgroup to finish instead of a kernel of
 // its own needs a device-wide release in every combine workgroup, an L2
 // write-back on this part: measured slower at every decode size.)
@@ -34,7 +38,7 @@ struct CombineArgs {
     const uint64_t* mask;      // [T][words]
     const float* gate;
     const int32_t* inv;
-    const float* yp;           // [splits][rows_cap][d]
+    const void* yp;            // fp32 [splits][rows_cap][d], or bf16 [rows_cap][d] (ROWS16)
     const int32_t* splits_dev; // slices the down projection took (device), or null: `splits`
     const float* ys;           // [T][d] shared output or null
     const uint16_t* res;       // [T][d] bf16 residual rows added to y, or null
@@ -54,7 +58,8 @@ struct CombineArgs {
 constexpr int kBatch = 8;
 constexpr int kMaxSplits = 8;                  // the down projection uses at most 8 slices
 
-template <typename YT>
+// ROWS16: bf16 rows, one slice, sums of squares not taken here.
+template <typename YT, bool ROWS16>
 __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     __shared__ float red[kBatch][kWaves];
     const int t = blockIdx.x, chunk = blockIdx.y;
@@ -71,10 +76,12 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     // they are loaded first, from in-bounds stand-ins when absent (slice 0 of
     // the partials; element 0 for threads past d), and used after the loop
     const int jc = on ? j : 0;
-    const float4 ysv =
-        *reinterpret_cast<const float4*>((a.ys ? a.ys + static_cast<size_t>(t) * a.d : a.yp) + 4 * jc);
-    const uint2 rsv = *reinterpret_cast<const uint2*>(
-        (a.res ? a.res + static_cast<size_t>(t) * a.d : reinterpret_cast<const uint16_t*>(a.yp)) + 4 * jc);
+    const float* ypf = static_cast<const float*>(a.yp);
+    const uint16_t* yph = static_cast<const uint16_t*>(a.yp);
+    const float4 ysv = *reinterpret_cast<const float4*>(
+        (a.ys ? a.ys + static_cast<size_t>(t) * a.d : reinterpret_cast<const float*>(a.gate)) + 4 * jc);
+    const uint2 rsv =
+        *reinterpret_cast<const uint2*>((a.res ? a.res + static_cast<size_t>(t) * a.d : yph) + 4 * jc);
 
     int w = 0;
     uint64_t rest = mt[0];
@@ -100,12 +107,21 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
         // each row slice's partials are all loaded at once and added in slice
         // order; the next row's loads are issued before this row is added up
         // (threads past d read the row's first elements and discard them)
-        float4 q[2][kMaxSplits];
-        auto issue = [&](float4 (&dst)[kMaxSplits], int row) __attribute__((always_inline)) {
-            const float* src = a.yp + static_cast<int64_t>(row) * a.d + 4 * jc;
+        constexpr int kS = ROWS16 ? 1 : kMaxSplits;
+        float4 q[2][kS];
+        auto issue = [&](float4 (&dst)[kS], int row) __attribute__((always_inline)) {
+            if constexpr (ROWS16) {
+                const uint2 v = *reinterpret_cast<const uint2*>(yph + static_cast<int64_t>(row) * a.d + 4 * jc);
+                dst[0] = make_float4(bf16_to_f32(static_cast<uint16_t>(v.x & 0xffffu)),
+                                     bf16_to_f32(static_cast<uint16_t>(v.x >> 16)),
+                                     bf16_to_f32(static_cast<uint16_t>(v.y & 0xffffu)),
+                                     bf16_to_f32(static_cast<uint16_t>(v.y >> 16)));
+            } else {
+                const float* src = ypf + static_cast<int64_t>(row) * a.d + 4 * jc;
 #pragma unroll
-            for (int sp = 0; sp < kMaxSplits; ++sp)
-                if (sp < splits) dst[sp] = *reinterpret_cast<const float4*>(src + sp * a.split_stride);
+                for (int sp = 0; sp < kMaxSplits; ++sp)
+                    if (sp < splits) dst[sp] = *reinterpret_cast<const float4*>(src + sp * a.split_stride);
+            }
         };
         issue(q[0], rows[0]);
         float ss[kBatch];
@@ -114,38 +130,42 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
             ss[b] = 0.f;
             if (b < nb) {
                 if (b + 1 < nb) issue(q[(b + 1) & 1], rows[b + 1]);
-                const float4 (&c)[kMaxSplits] = q[b & 1];
+                const float4 (&c)[kS] = q[b & 1];
                 float4 o = c[0];
 #pragma unroll
-                for (int sp = 1; sp < kMaxSplits; ++sp)
+                for (int sp = 1; sp < kS; ++sp)
                     if (sp < splits) { o.x += c[sp].x; o.y += c[sp].y; o.z += c[sp].z; o.w += c[sp].w; }
                 if (on) {
-                    ss[b] = fmaf(o.x, o.x, ss[b]); ss[b] = fmaf(o.y, o.y, ss[b]);
-                    ss[b] = fmaf(o.z, o.z, ss[b]); ss[b] = fmaf(o.w, o.w, ss[b]);
+                    if constexpr (!ROWS16) {
+                        ss[b] = fmaf(o.x, o.x, ss[b]); ss[b] = fmaf(o.y, o.y, ss[b]);
+                        ss[b] = fmaf(o.z, o.z, ss[b]); ss[b] = fmaf(o.w, o.w, ss[b]);
+                    }
                     const float g = gs[b];
                     acc.x = fmaf(g, o.x, acc.x); acc.y = fmaf(g, o.y, acc.y);
                     acc.z = fmaf(g, o.z, acc.z); acc.w = fmaf(g, o.w, acc.w);
                 }
             }
         }
-#pragma unroll
-        for (int b = 0; b < kBatch; ++b) {
-            if (b >= nb) break;
-            const float v = wave_sum(ss[b]);
-            if (lane == 0) red[b][wave] = v;
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
+        if constexpr (!ROWS16) {
 #pragma unroll
             for (int b = 0; b < kBatch; ++b) {
                 if (b >= nb) break;
-                float tot = 0.f;
-#pragma unroll
-                for (int q = 0; q < kWaves; ++q) tot += red[b][q];
-                a.nrm2[static_cast<int64_t>(rows[b]) * a.nchunk + chunk] = tot;
+                const float v = wave_sum(ss[b]);
+                if (lane == 0) red[b][wave] = v;
             }
+            __syncthreads();
+            if (threadIdx.x == 0) {
+#pragma unroll
+                for (int b = 0; b < kBatch; ++b) {
+                    if (b >= nb) break;
+                    float tot = 0.f;
+#pragma unroll
+                    for (int q = 0; q < kWaves; ++q) tot += red[b][q];
+                    a.nrm2[static_cast<int64_t>(rows[b]) * a.nchunk + chunk] = tot;
+                }
+            }
+            __syncthreads();
         }
-        __syncthreads();
         if (nb < kBatch) break;
     }
     if (on) {
@@ -185,7 +205,16 @@ __global__ __launch_bounds__(kThreads) void update_accounts_kernel(
     for (int r = beg + threadIdx.x; r < end; r += kThreads) {
         sp += static_cast<double>(prob[static_cast<size_t>(tok_idx[r]) * E + e]);
         float ss = 0.f;
-        for (int c = 0; c < nchunk; ++c) ss += nrm2[static_cast<size_t>(r) * nchunk + c];
+        const float* rp = nrm2 + static_cast<size_t>(r) * nchunk;
+        if ((nchunk & 3) == 0) {
+            // (the same order, four partials per load)
+            for (int c = 0; c < nchunk; c += 4) {
+                const float4 v = *reinterpret_cast<const float4*>(rp + c);
+                ss += v.x; ss += v.y; ss += v.z; ss += v.w;
+            }
+        } else {
+            for (int c = 0; c < nchunk; ++c) ss += rp[c];
+        }
         sn += static_cast<double>(sqrtf(ss));
     }
     sp = wave_sum(sp);
@@ -287,24 +316,26 @@ __global__ __launch_bounds__(kThreads) void reset_accounts_kernel(int E, int64_t
 int combine_chunks(const eat_params_t& p) { return (p.d_model / 4 + kThreads - 1) / kThreads; }
 
 hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask, const float* gate,
-                          const int32_t* inv, const float* yp, const float* ys, const uint16_t* residual,
+                          const int32_t* inv, const void* yp, const float* ys, const uint16_t* residual,
                           void* y, float* nrm2, int splits, int64_t split_stride, const int32_t* splits_dev,
-                          hipStream_t s) {
+                          bool rows_bf16, hipStream_t s) {
     if (splits < 1 || splits > kMaxSplits) return hipErrorInvalidValue;
+    if (rows_bf16 && (splits != 1 || splits_dev || p.act_dtype != EAT_BF16)) return hipErrorInvalidValue;
     const int nchunk = combine_chunks(p);
     CombineArgs a{};
     a.mask = mask; a.gate = gate; a.inv = inv; a.yp = yp; a.splits_dev = splits_dev; a.ys = ys; a.res = residual;
     a.y = y; a.nrm2 = nrm2; a.split_stride = split_stride; a.splits = splits; a.T = T; a.E = p.E; a.d = p.d_model;
     a.nchunk = nchunk; a.words = mask_words(p.E);
     const dim3 grid(T, nchunk);
-    if (p.act_dtype == EAT_BF16) combine_kernel<uint16_t><<<grid, kThreads, 0, s>>>(a);
-    else combine_kernel<float><<<grid, kThreads, 0, s>>>(a);
+    if (rows_bf16) combine_kernel<uint16_t, true><<<grid, kThreads, 0, s>>>(a);
+    else if (p.act_dtype == EAT_BF16) combine_kernel<uint16_t, false><<<grid, kThreads, 0, s>>>(a);
+    else combine_kernel<float, false><<<grid, kThreads, 0, s>>>(a);
     return hipGetLastError();
 }
 
 hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets, const int32_t* tok_idx,
-                                  const float* prob, const float* nrm2, eat_accounts_t acc, hipStream_t s) {
-    update_accounts_kernel<<<p.E, kThreads, 0, s>>>(offsets, tok_idx, prob, nrm2, combine_chunks(p), p.E, p.alpha,
+                                  const float* prob, const float* nrm2, int parts, eat_accounts_t acc, hipStream_t s) {
+    update_accounts_kernel<<<p.E, kThreads, 0, s>>>(offsets, tok_idx, prob, nrm2, parts, p.E, p.alpha,
                                                  acc.n, acc.p_total, acc.c_s);
     return hipGetLastError();
 }

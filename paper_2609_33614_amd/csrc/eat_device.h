@@ -10,6 +10,8 @@ constexpr int kWave = 64;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
@@ -138,6 +140,12 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     const uint32_t rne = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
     const uint32_t qnan = (u >> 16) | 0x40u;
     return static_cast<uint16_t>((u & 0x7fffffffu) > 0x7f800000u ? qnan : rne);
+}
+
+// Two fp32 values -> packed bf16 bits (a in the low half), round to nearest
+// even by the hardware conversion (one instruction; NaN stays NaN).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
 
 __device__ __forceinline__ float silu(float a) { return a / (1.0f + __expf(-a)); }

@@ -56,7 +56,7 @@ struct Buffers {
     void* h;                 // [rows][F] SwiGLU hidden (bf16 or fp32)
     float* gu;               // [2][up_splits][rows][F] gate / up partial sums
     float* yp;               // [splits][rows][d] un-gated expert outputs (partials)
-    float* nrm2;             // [rows][combine_chunks] partial sums of squares of yp rows
+    float* nrm2;             // [rows][norm_parts] partial sums of squares of yp rows
     void* hs;                // [T][F_sh] shared-expert hidden
     float* ys;               // [T][d] shared-expert output
     float* gus;              // [2][shared_up_splits][T][F_sh] its gate / up partial sums
@@ -92,12 +92,13 @@ hipError_t launch_experts_f32(const eat_params_t& p, int32_t T, int64_t rows_cap
 // bf16 weights and activations: MFMA kernels.  Both projections choose
 // their slices on the device and write the count they took to
 // *up_splits_dev / *down_splits_dev (read by the up/gate slice reduce and
-// by the combine).
+// by the combine).  When rows_bf16(p, T), yp receives bf16 rows and nrm2
+// their partial sums of squares (norm_parts per row).
 hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_cap,
                                const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
                                const uint16_t* w2, const int32_t* offsets, const int32_t* tok_idx,
-                               uint16_t* h, float* gu, float* yp, int32_t* up_splits_dev, int32_t* down_splits_dev,
-                               hipStream_t s, const std::function<void()>& between);
+                               uint16_t* h, float* gu, float* yp, float* nrm2, int32_t* up_splits_dev,
+                               int32_t* down_splits_dev, hipStream_t s, const std::function<void()>& between);
 
 // Always-on shared expert over all T tokens.
 hipError_t launch_shared_f32(const eat_params_t& p, int32_t T, const float* x, const float* ws1,
@@ -114,12 +115,15 @@ hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* 
 
 // yp holds the down projection's partial slices, `split_stride` floats
 // apart (*splits_dev of them when set, else `splits`); they are added in
-// slice order.  `residual` (bf16 [T][d], or null) is added to y before the
-// cast.
+// slice order, and each row slice's sum of squares goes to nrm2.  With
+// rows_bf16 yp holds bf16 rows instead (one slice) whose sums of squares
+// are already in nrm2.  `residual` (bf16 [T][d], or null) is added to y
+// before the cast.
 hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask,
-                          const float* gate, const int32_t* inv, const float* yp,
+                          const float* gate, const int32_t* inv, const void* yp,
                           const float* ys, const uint16_t* residual, void* y, float* nrm2,
-                          int splits, int64_t split_stride, const int32_t* splits_dev, hipStream_t s);
+                          int splits, int64_t split_stride, const int32_t* splits_dev, bool rows_bf16,
+                          hipStream_t s);
 
 // Between stacked layers (combine.hip): h = bf16(sum of `splits` fp32
 // partial rows, or the bf16 rows of src when splits == 0), written to h_out
@@ -134,8 +138,15 @@ hipError_t launch_mix_norm(const float* part, int splits, int64_t split_stride, 
 int dense_splits(int M, int K, int32_t T);
 hipError_t launch_dense_bf16(const uint16_t* src, int32_t T, const uint16_t* w, int M, int K, float* out,
                              int splits, int64_t split_stride, hipStream_t s);
-// 1024-element slices of d the combine works in (and nrm2 holds per row).
+// 1024-element slices of d the combine works in.
 int combine_chunks(const eat_params_t& p);
+// Prefill-sized bf16 calls: the down projection (wide tiles) stores the
+// expert rows of yp in bf16 with their norms' partial sums of squares, one
+// per 32 features (expert.hip); other calls keep fp32 rows whose sums of
+// squares the combine takes, one per combine chunk.
+bool rows_bf16(const eat_params_t& p, int32_t T);
+// Partial sums of squares per expert row in nrm2.
+int norm_parts(const eat_params_t& p, int32_t T);
 
 // Number of reduction-dimension slices the bf16 down projection uses for T
 // tokens (1 for fp32 layers).
@@ -149,11 +160,13 @@ int up_splits(const eat_params_t& p, int32_t T);
 // fp32 out = src W^T over 256-row tiles.  Rows are the expert segments given
 // by offsets (gather maps them to source rows), or nrows identity rows when
 // offsets is null.  wide_fits tells whether M and K suit the tiling; `packed`
-// reads wa / wb in the packed layout.
+// reads wa / wb in the packed layout.  With nrm2 (plain tiles) out holds
+// bf16 rows and nrm2 [rows][M / 32] partial sums of squares of each row (32
+// features each), taken before the cast.
 bool wide_fits(bool gated, int M, int K);
 hipError_t launch_wide(bool gated, const uint16_t* wa, const uint16_t* wb, const uint16_t* src,
                        const int32_t* gather, const int32_t* offsets, int groups, int nrows, int M,
-                       int K, void* out, int64_t rows_cap, bool packed, hipStream_t s);
+                       int K, void* out, int64_t rows_cap, bool packed, float* nrm2, hipStream_t s);
 
 // Packed weight layout (pack.hip): dst = the 1 KB-block form of the
 // row-major bf16 [groups][M][K] src (M % 16 == 0, K % 32 == 0).
@@ -184,8 +197,9 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
                         uint64_t* mask_out, int32_t* expert_load_out, float* prob_out, void* ws,
                         hipStream_t stream, const hipEvent_t* events, int32_t n_events);
 
+// nrm2: `parts` partial sums of squares per row, added in order.
 hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets,
-                                  const int32_t* tok_idx, const float* prob, const float* nrm2,
+                                  const int32_t* tok_idx, const float* prob, const float* nrm2, int parts,
                                   eat_accounts_t acc, hipStream_t s);
 
 }  // namespace eat

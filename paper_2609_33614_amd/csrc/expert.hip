@@ -751,6 +751,12 @@ static bool shared_wide(const eat_params_t& p, int32_t T) {
            wide_fits(false, p.d_model, p.d_shared);
 }
 
+bool rows_bf16(const eat_params_t& p, int32_t T) { return use_wide(p, T); }
+
+int norm_parts(const eat_params_t& p, int32_t T) {
+    return rows_bf16(p, T) ? p.d_model / 32 : combine_chunks(p);
+}
+
 int down_splits(const eat_params_t& p, int32_t T) {
     if (p.expert_dtype != EAT_BF16 || use_wide(p, T)) return 1;
     return split_rule(p.d_model, p.d_ffn, min_tiles(p, T), 8, EAT_SPLIT_WAVES);
@@ -779,7 +785,7 @@ int dense_splits(int M, int K, int32_t T) {
 hipError_t launch_dense_bf16(const uint16_t* src, int32_t T, const uint16_t* w, int M, int K, float* out,
                              int splits, int64_t split_stride, hipStream_t s) {
     if (dense_wide(M, K, T))
-        return launch_wide(false, w, nullptr, src, nullptr, nullptr, 1, T, M, K, out, T, false, s);
+        return launch_wide(false, w, nullptr, src, nullptr, nullptr, 1, T, M, K, out, T, false, nullptr, s);
     const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;
     const int tiles = (T + bn - 1) / bn;
@@ -809,8 +815,8 @@ hipError_t launch_shared_f32(const eat_params_t& p, int32_t T, const float* x, c
 hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_cap, const uint16_t* x,
                                const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
                                const int32_t* offsets, const int32_t* tok_idx, uint16_t* h,
-                               float* gu, float* yp, int32_t* up_splits_dev, int32_t* down_splits_dev, hipStream_t s,
-                               const std::function<void()>& between) {
+                               float* gu, float* yp, float* nrm2, int32_t* up_splits_dev, int32_t* down_splits_dev,
+                               hipStream_t s, const std::function<void()>& between) {
     const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;
     // no expert holds more than T rows, so it needs at most ceil(T / bn) tiles
@@ -819,12 +825,12 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
 
     const bool packed = p.weight_layout == EAT_LAYOUT_PACKED;
     if (use_wide(p, T)) {
-        hipError_t err =
-            launch_wide(true, w1, w3, x, tok_idx, offsets, p.E, 0, p.d_ffn, p.d_model, h, rows_cap, packed, s);
+        hipError_t err = launch_wide(true, w1, w3, x, tok_idx, offsets, p.E, 0, p.d_ffn, p.d_model, h, rows_cap,
+                                     packed, nullptr, s);
         if (err != hipSuccess) return err;
         if (between) between();
         return launch_wide(false, w2, nullptr, h, nullptr, offsets, p.E, 0, p.d_model, p.d_ffn, yp, rows_cap, packed,
-                           s);
+                           rows_bf16(p, T) ? nrm2 : nullptr, s);
     }
     // both projections take their slices on the device, from the tiles in use
     const int usplits = up_splits(p, T);
@@ -883,9 +889,10 @@ hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* 
     const bool packed = p.weight_layout == EAT_LAYOUT_PACKED;
     if (shared_wide(p, T)) {
         hipError_t err =
-            launch_wide(true, ws1, ws3, x, nullptr, nullptr, 1, T, p.d_shared, p.d_model, hs, T, packed, s);
+            launch_wide(true, ws1, ws3, x, nullptr, nullptr, 1, T, p.d_shared, p.d_model, hs, T, packed, nullptr, s);
         if (err != hipSuccess) return err;
-        return launch_wide(false, ws2, nullptr, hs, nullptr, nullptr, 1, T, p.d_model, p.d_shared, ys, T, packed, s);
+        return launch_wide(false, ws2, nullptr, hs, nullptr, nullptr, 1, T, p.d_model, p.d_shared, ys, T, packed,
+                           nullptr, s);
     }
     const int nsub = pick_nsub(T);
     const int bn = 16 * nsub;

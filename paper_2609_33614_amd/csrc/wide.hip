@@ -19,7 +19,7 @@
 // MFMAs and every SIMD's work shrinks with the tile.
 //
 // The grid is persistent: the work list (per expert, its weight tiles in
-// turn and each one's token tiles adjacent) is cut into 8 contiguous parts,
+// turn and each one's token tiles adjacent) is cut into contiguous parts,
 // one per XCD (workgroups are dealt to XCDs round-robin), so the workgroups
 // that share an expert's weight tiles share one L2 and read them together.
 // A workgroup's ring runs on from one item to the next, so the refill after
@@ -60,7 +60,6 @@ constexpr int kStage = 2 * kRegion;       // tokens then weights
 #define EAT_WIDE_RING_KB 128
 #endif
 constexpr int kStages = (EAT_WIDE_RING_KB * 1024) / kStage;   // ring depth
-constexpr int kXcd = 8;
 static_assert(kWN * kWK * 2 == kRegion, "token and weight regions have the same size");
 
 struct WideArgs {
@@ -70,7 +69,9 @@ struct WideArgs {
     const int32_t* gather;     // row -> source row, or null (identity)
     const int32_t* offsets;    // [groups+1] expert-major row offsets, or null
     int groups, nrows, M, K;
-    void* out;                 // gated: bf16 H [rows][M]; plain: fp32 [rows][M]
+    void* out;                 // gated: bf16 H [rows][M]; plain: fp32 [rows][M] (bf16 with ROWS)
+    float* nrm2;               // plain with ROWS: [rows][M / 32] sums of squares of 32 features of each row
+    int xcds;                  // XCDs the grid is dealt over (the grid is a multiple of it)
 };
 
 // Byte offset of 16-byte vector v of row r in a region of kRB-byte rows.
@@ -197,7 +198,11 @@ __device__ __forceinline__ void wait_chunks(int after) {
     }
 }
 
-template <bool GATED, bool PACKED>
+// ROWS (plain tiles): the output rows are stored in bf16, and each lane
+// writes the sum of squares of the 32 output features it holds of a row
+// (half of its wave's 64), taken from the fp32 accumulators (the row norms
+// of the account update).
+template <bool GATED, bool PACKED, bool ROWS = false>
 __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
     __shared__ __attribute__((aligned(1024))) uint8_t ring[kStages * kStage];
     __shared__ int tstart[kMaxExperts + 1];
@@ -214,9 +219,9 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
     constexpr int kOut = GATED ? kWN / 2 : kWN;     // output features per tile
     const int nx = a.M / kOut;
     const int work = ntiles * nx;
-    const int xcd = blockIdx.x % kXcd, slot = blockIdx.x / kXcd;
-    const int per_xcd = gridDim.x / kXcd;
-    const int part = (work + kXcd - 1) / kXcd;
+    const int xcd = blockIdx.x % a.xcds, slot = blockIdx.x / a.xcds;
+    const int per_xcd = gridDim.x / a.xcds;
+    const int part = (work + a.xcds - 1) / a.xcds;
     const int wbeg = xcd * part, wend = min(work, wbeg + part);
 
     // a workgroup's items only increase, so its segment search resumes where
@@ -356,6 +361,26 @@ __global__ __launch_bounds__(kThreads) void wide_kernel(WideArgs a) {
                         pk.y = static_cast<uint32_t>(hv[2]) | (static_cast<uint32_t>(hv[3]) << 16);
                         *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + orow + f) = pk;
                     }
+                } else if constexpr (ROWS) {
+                    float ss = 0.f;
+#pragma unroll
+                    for (int i = 0; i < 2; ++i)
+#pragma unroll
+                        for (int qb = 0; qb < 4; ++qb) {
+                            const int f = cur.m0 + 64 * wn + 32 * i + 8 * qb + 4 * lh;
+                            uint2 pk;
+                            pk.x = pack_bf16x2(acc[i][j][4 * qb + 0], acc[i][j][4 * qb + 1]);
+                            pk.y = pack_bf16x2(acc[i][j][4 * qb + 2], acc[i][j][4 * qb + 3]);
+                            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + orow + f) = pk;
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) ss = fmaf(acc[i][j][4 * qb + q], acc[i][j][4 * qb + q], ss);
+                        }
+                    // lanes l and l + 32 each hold half of the row's 64 features:
+                    // slot m0 / 32 + 2 wn + lh of the row, whose slots start at
+                    // r M / 32 = orow / 32 (from the first store's feature
+                    // f0 = m0 + 64 wn + 4 lh, already at hand)
+                    const int f0 = cur.m0 + 64 * wn + 4 * lh;
+                    a.nrm2[(orow >> 5) + (f0 >> 5) + ((f0 >> 2) & 1)] = ss;
                 } else {
 #pragma unroll
                     for (int i = 0; i < 2; ++i)
@@ -381,21 +406,56 @@ bool wide_fits(bool gated, int M, int K) {
     return M % (gated ? kWN / 2 : kWN) == 0 && K % 128 == 0;
 }
 
+namespace {
+
+// The part's geometry, asked once on the device current at the first call
+// (every device a process uses is assumed to be the same part): workgroups
+// of the wide kernel it keeps resident (one per CU: the ring takes 128 KB of
+// LDS and the 16 waves fill the SIMDs) and the XCDs they are dealt over.
+struct WideGeometry {
+    int64_t resident;
+    int xcds;
+};
+
+const WideGeometry& wide_geometry() {
+    static const WideGeometry g = [] {
+        int dev = 0, cus = 0, xccs = 0, per_cu = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+            cus = 256;
+        if (hipDeviceGetAttribute(&xccs, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || xccs < 1 ||
+            xccs > cus)
+            xccs = 1;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wide_kernel<true, true>, kThreads, 0) !=
+                hipSuccess ||
+            per_cu < 1)
+            per_cu = 1;
+        return WideGeometry{static_cast<int64_t>(cus) * per_cu, xccs};
+    }();
+    return g;
+}
+
+}  // namespace
+
 hipError_t launch_wide(bool gated, const uint16_t* wa, const uint16_t* wb, const uint16_t* src,
                        const int32_t* gather, const int32_t* offsets, int groups, int nrows, int M, int K,
-                       void* out, int64_t rows_cap, bool packed, hipStream_t s) {
-    WideArgs a{wa, wb, src, gather, offsets, groups, nrows, M, K, out};
+                       void* out, int64_t rows_cap, bool packed, float* nrm2, hipStream_t s) {
+    if (nrm2 && gated) return hipErrorInvalidValue;
+    const WideGeometry& geo = wide_geometry();
+    WideArgs a{wa, wb, src, gather, offsets, groups, nrows, M, K, out, nrm2, geo.xcds};
     // every group may end in a partial tile
     const int64_t tiles = offsets ? std::min<int64_t>(rows_cap, (rows_cap + kWM - 1) / kWM + groups)
                                   : (nrows + kWM - 1) / kWM;
     const int64_t work = tiles * (M / (gated ? kWN / 2 : kWN));
-    // persistent: one workgroup per CU (the ring takes 128 KB of LDS and the
-    // 16 waves fill the SIMDs), a multiple of the XCD count
-    int64_t blocks = std::min<int64_t>(work, 256);
-    blocks = std::max<int64_t>(kXcd, (blocks + kXcd - 1) / kXcd * kXcd);
+    // persistent: the workgroups the part keeps resident (or one per item),
+    // a multiple of the XCD count
+    int64_t blocks = std::min<int64_t>(work, geo.resident);
+    blocks = std::max<int64_t>(geo.xcds, (blocks + geo.xcds - 1) / geo.xcds * geo.xcds);
     const int nb = static_cast<int>(blocks);
     if (gated && packed) wide_kernel<true, true><<<nb, kThreads, 0, s>>>(a);
     else if (gated) wide_kernel<true, false><<<nb, kThreads, 0, s>>>(a);
+    else if (nrm2 && packed) wide_kernel<false, true, true><<<nb, kThreads, 0, s>>>(a);
+    else if (nrm2) wide_kernel<false, false, true><<<nb, kThreads, 0, s>>>(a);
     else if (packed) wide_kernel<false, true><<<nb, kThreads, 0, s>>>(a);
     else wide_kernel<false, false><<<nb, kThreads, 0, s>>>(a);
     return hipGetLastError();
