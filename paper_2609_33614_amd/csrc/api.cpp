@@ -231,7 +231,7 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
                         const void* w3, const void* w2, const void* ws1, const void* ws3, const void* ws2,
                         eat_accounts_t acc, const int8_t* ppl_trend, const uint16_t* residual, void* y,
                         uint64_t* mask_out, int32_t* expert_load_out, float* prob_out, void* ws,
-                        hipStream_t stream, const hipEvent_t* events, int32_t n_events) {
+                        hipStream_t stream, const hipEvent_t* events, int32_t n_events, AccountJob* defer) {
     const eat_params_t& p = h.p;
     const eat::Workspace w = eat::plan_workspace(h, T);
     char* base = static_cast<char*>(ws);
@@ -303,8 +303,14 @@ hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float*
         e = eat::launch_combine(p, T, b.mask, b.gate, b.inv, b.yp, shared ? b.ys : nullptr, residual, y, b.nrm2,
                                 w.splits, w.rows * p.d_model, splits_dev, rows16, stream);
     mark(EAT_STAGE_COMBINED);
-    if (e == hipSuccess && p.mode == EAT_MODE_EAT)
-        e = eat::launch_update_accounts(p, b.offsets, b.tok_idx, b.prob, b.nrm2, eat::norm_parts(p, T), acc, stream);
+    if (defer) *defer = AccountJob{};
+    if (e == hipSuccess && p.mode == EAT_MODE_EAT) {
+        if (defer)
+            *defer = AccountJob{b.offsets, b.tok_idx, b.prob, b.nrm2, eat::norm_parts(p, T), p.E, p.alpha, acc};
+        else
+            e = eat::launch_update_accounts(p, b.offsets, b.tok_idx, b.prob, b.nrm2, eat::norm_parts(p, T), acc,
+                                            stream);
+    }
     mark(EAT_STAGE_END);
     return e;
 }
@@ -419,14 +425,17 @@ eat_status_t eat_stack_forward(const eat_stack_layer_t* layers, int32_t n_layers
     size_t mask_off = 0;                      // and its masks after T * mask_words(E_j)
     // u_0 = bf16(RMSNorm(x))
     hipError_t e = eat::launch_mix_norm(nullptr, 0, 0, static_cast<const uint16_t*>(x), T, d, rms_eps, nullptr, u,
-                                        stream);
+                                        nullptr, stream);
     const uint16_t* h = static_cast<const uint16_t*>(x);
     for (int32_t l = 0; l < n_layers && e == hipSuccess; ++l) {
         const eat_stack_layer_t& L = layers[l];
-        // r = bf16(h + MoE_l(u))
+        // r = bf16(h + MoE_l(u)); the layer's account update rides on the
+        // RMSNorm launch below (it reads the layer workspace, which the next
+        // layer reuses only after that launch)
+        eat::AccountJob job{};
         e = forward_impl(*L.layer, u, T, L.w_router, L.w1, L.w3, L.w2, L.ws1, L.ws3, L.ws2, L.acc, ppl_trend, h, r,
                          masks_out ? masks_out + mask_off : nullptr, nullptr,
-                         probs_out ? probs_out + prob_off : nullptr, base + sp.layer, stream, nullptr, 0);
+                         probs_out ? probs_out + prob_off : nullptr, base + sp.layer, stream, nullptr, 0, &job);
         prob_off += static_cast<size_t>(T) * L.layer->p.E;
         mask_off += static_cast<size_t>(T) * eat::mask_words(L.layer->p.E);
         // h' = bf16(r M_l^T); u = bf16(RMSNorm(h')) for the next layer
@@ -437,7 +446,7 @@ eat_status_t eat_stack_forward(const eat_stack_layer_t* layers, int32_t n_layers
         uint16_t* hn = last ? static_cast<uint16_t*>(h_out) : hb[l & 1];
         if (e == hipSuccess)
             e = eat::launch_mix_norm(mix, sp.splits, stride, nullptr, T, d, rms_eps, hn, last ? nullptr : u,
-                                     stream);
+                                     job.experts > 0 ? &job : nullptr, stream);
         h = hn;
     }
     return e == hipSuccess ? EAT_OK : EAT_ERR_HIP;

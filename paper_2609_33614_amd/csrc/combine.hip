@@ -191,12 +191,18 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     }
 }
 
-__global__ __launch_bounds__(kThreads) void update_accounts_kernel(
-    const int32_t* __restrict__ offsets, const int32_t* __restrict__ tok_idx,
-    const float* __restrict__ prob, const float* __restrict__ nrm2, int nchunk, int E, float alpha,
-    int64_t* __restrict__ n, float* __restrict__ p_total, float* __restrict__ c_s) {
+// Expert e's account update by one workgroup (every thread of it calls this).
+__device__ __forceinline__ void account_update(const AccountJob& j, int e) {
     __shared__ double red[2][kWaves];
-    const int e = blockIdx.x;
+    const int32_t* __restrict__ offsets = j.offsets;
+    const int32_t* __restrict__ tok_idx = j.tok_idx;
+    const float* __restrict__ prob = j.prob;
+    const float* __restrict__ nrm2 = j.nrm2;
+    const int nchunk = j.parts, E = j.experts;
+    const float alpha = j.alpha;
+    int64_t* __restrict__ n = j.acc.n;
+    float* __restrict__ p_total = j.acc.p_total;
+    float* __restrict__ c_s = j.acc.c_s;
     const int lane = lane_id(), wave = threadIdx.x / kWave;
     const int beg = offsets[e], end = offsets[e + 1];
     const int cnt = end - beg;
@@ -232,6 +238,8 @@ __global__ __launch_bounds__(kThreads) void update_accounts_kernel(
     }
 }
 
+__global__ __launch_bounds__(kThreads) void update_accounts_kernel(AccountJob j) { account_update(j, blockIdx.x); }
+
 // One workgroup per token row of d <= kMixMax elements: v = the row's
 // split partials added in split order (or the bf16 source row), h = bf16(v)
 // (written when h_out is set), then u = bf16(h * (1 / sqrt(mean(h^2) + eps)))
@@ -241,12 +249,18 @@ __global__ __launch_bounds__(kThreads) void update_accounts_kernel(
 // slice's load is issued before the first add; 0 = read the bf16 source row).
 constexpr int kMixVec = 4;                                  // floats per thread and group
 constexpr int kMixGroups = 8;                               // d <= 256 * 4 * 8 = 8192
+// Workgroups past the T rows do the deferred account update, one expert each.
 template <int S>
 __global__ __launch_bounds__(kThreads) void mix_norm_kernel(const float* __restrict__ part, int64_t split_stride,
-                                                            const uint16_t* __restrict__ src, int d, float eps,
-                                                            uint16_t* __restrict__ h_out, uint16_t* __restrict__ u_out) {
+                                                            const uint16_t* __restrict__ src, int T, int d, float eps,
+                                                            uint16_t* __restrict__ h_out, uint16_t* __restrict__ u_out,
+                                                            AccountJob job) {
     __shared__ float red[kWaves];
     const int t = blockIdx.x;
+    if (t >= T) {                             // uniform over the workgroup
+        account_update(job, t - T);
+        return;
+    }
     const int lane = lane_id(), wave = threadIdx.x / kWave;
     float v[kMixGroups][kMixVec];
     float ss = 0.f;
@@ -335,21 +349,23 @@ hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask
 
 hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets, const int32_t* tok_idx,
                                   const float* prob, const float* nrm2, int parts, eat_accounts_t acc, hipStream_t s) {
-    update_accounts_kernel<<<p.E, kThreads, 0, s>>>(offsets, tok_idx, prob, nrm2, parts, p.E, p.alpha,
-                                                 acc.n, acc.p_total, acc.c_s);
+    update_accounts_kernel<<<p.E, kThreads, 0, s>>>(AccountJob{offsets, tok_idx, prob, nrm2, parts, p.E, p.alpha, acc});
     return hipGetLastError();
 }
 
 bool mix_norm_fits(int d) { return d % (kMixVec * 2) == 0 && d <= kThreads * kMixVec * kMixGroups; }
 
 hipError_t launch_mix_norm(const float* part, int splits, int64_t split_stride, const uint16_t* src, int32_t T,
-                           int d, float eps, uint16_t* h_out, uint16_t* u_out, hipStream_t s) {
+                           int d, float eps, uint16_t* h_out, uint16_t* u_out, const AccountJob* accounts,
+                           hipStream_t s) {
+    const AccountJob job = accounts ? *accounts : AccountJob{};
+    const int grid = T + job.experts;
     switch (splits) {
-        case 0: mix_norm_kernel<0><<<T, kThreads, 0, s>>>(part, split_stride, src, d, eps, h_out, u_out); break;
-        case 1: mix_norm_kernel<1><<<T, kThreads, 0, s>>>(part, split_stride, src, d, eps, h_out, u_out); break;
-        case 2: mix_norm_kernel<2><<<T, kThreads, 0, s>>>(part, split_stride, src, d, eps, h_out, u_out); break;
-        case 4: mix_norm_kernel<4><<<T, kThreads, 0, s>>>(part, split_stride, src, d, eps, h_out, u_out); break;
-        case 8: mix_norm_kernel<8><<<T, kThreads, 0, s>>>(part, split_stride, src, d, eps, h_out, u_out); break;
+        case 0: mix_norm_kernel<0><<<grid, kThreads, 0, s>>>(part, split_stride, src, T, d, eps, h_out, u_out, job); break;
+        case 1: mix_norm_kernel<1><<<grid, kThreads, 0, s>>>(part, split_stride, src, T, d, eps, h_out, u_out, job); break;
+        case 2: mix_norm_kernel<2><<<grid, kThreads, 0, s>>>(part, split_stride, src, T, d, eps, h_out, u_out, job); break;
+        case 4: mix_norm_kernel<4><<<grid, kThreads, 0, s>>>(part, split_stride, src, T, d, eps, h_out, u_out, job); break;
+        case 8: mix_norm_kernel<8><<<grid, kThreads, 0, s>>>(part, split_stride, src, T, d, eps, h_out, u_out, job); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -128,9 +128,13 @@ hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask
 // Between stacked layers (combine.hip): h = bf16(sum of `splits` fp32
 // partial rows, or the bf16 rows of src when splits == 0), written to h_out
 // if set; u = bf16(h / sqrt(mean(h^2) + eps)) written to u_out if set.
+// `accounts` (or null): a deferred account update, done by extra
+// workgroups of the same launch (it depends on neither h nor u).
+struct AccountJob;
 bool mix_norm_fits(int d);
 hipError_t launch_mix_norm(const float* part, int splits, int64_t split_stride, const uint16_t* src,
-                           int32_t T, int d, float eps, uint16_t* h_out, uint16_t* u_out, hipStream_t s);
+                           int32_t T, int d, float eps, uint16_t* h_out, uint16_t* u_out,
+                           const AccountJob* accounts, hipStream_t s);
 
 // Dense bf16 projection out[split][T][M] = src[T][K] . W^T (fp32 slices of
 // the reduction dimension, split_stride floats apart), W [M][K]: the
@@ -191,11 +195,27 @@ eat_status_t check_forward(const eat_ctx* h, const void* x, int32_t T, const flo
                            const void* w3, const void* w2, const void* ws1, const void* ws3, const void* ws2,
                            const eat_accounts_t& acc, const void* y, const uint64_t* mask_out,
                            const int32_t* expert_load_out);
+// The account update of one call (Sec. 3.2): its inputs in the call's
+// workspace, and the accounts.  experts == 0: nothing to update (baseline
+// modes, or no call).
+struct AccountJob {
+    const int32_t* offsets;
+    const int32_t* tok_idx;
+    const float* prob;
+    const float* nrm2;
+    int parts;               // partial sums of squares per row in nrm2
+    int experts;
+    float alpha;
+    eat_accounts_t acc;
+};
+// With `defer` set, the account update is not enqueued but described there,
+// for a later launch on the same stream (before the workspace is reused).
 hipError_t forward_impl(const eat_ctx& h, const void* x, int32_t T, const float* w_router, const void* w1,
                         const void* w3, const void* w2, const void* ws1, const void* ws3, const void* ws2,
                         eat_accounts_t acc, const int8_t* ppl_trend, const uint16_t* residual, void* y,
                         uint64_t* mask_out, int32_t* expert_load_out, float* prob_out, void* ws,
-                        hipStream_t stream, const hipEvent_t* events, int32_t n_events);
+                        hipStream_t stream, const hipEvent_t* events, int32_t n_events,
+                        AccountJob* defer = nullptr);
 
 // nrm2: `parts` partial sums of squares per row, added in order.
 hipError_t launch_update_accounts(const eat_params_t& p, const int32_t* offsets,
