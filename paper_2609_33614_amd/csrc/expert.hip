@@ -163,6 +163,7 @@ struct StreamArgs {
                                // [split][rows][M] (used when more than one slice)
     float* out2;               // gated: fp32 U partials [split][rows][M]
     uint16_t* h;               // gated: bf16 H [rows][M] (written here when one slice is taken)
+    int kin;                   // gated: reduction groups per workgroup (2, or 1 when 0 or 1)
 };
 
 __device__ __forceinline__ bf16x8 ld16(const uint16_t* p) {
@@ -238,20 +239,42 @@ constexpr bool stream_deep() { return GATED ? NSUB <= EAT_DEEP_NSUB : NSUB <= EA
 // At least 3 waves per SIMD: the register budget then keeps the MFMA
 // accumulators in VGPRs (no AGPR copies) and the 64-token gated variant
 // holds 3 waves per SIMD instead of 2 (measured: more weight bytes in flight).
-template <bool GATED, int NSUB, int KS, int WPB, bool PACKED>
-__global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))) void stream_kernel(StreamArgs a) {
-    constexpr int NT = WPB * 64;                      // threads per workgroup
+// KIN = 2: the workgroup holds two groups of WPB waves over the same weight
+// rows, each taking one half of the item's reduction slice (its own token
+// staging); group 1 hands its accumulators to group 0 through LDS at the
+// end of the item.  This doubles the waves of a launch whose experts are few
+// without the fp32 partials and the reduce launch of a split across
+// workgroups.
+template <bool GATED, int NSUB, int KS, int WPB, bool PACKED, int KIN = 1>
+// (Two groups of the 128-token gated tiles need one register more than 3
+// waves per SIMD leave, and their 8 waves' LDS keeps one workgroup per CU
+// anyway: they take 2.)
+__global__ __launch_bounds__(WPB * 64 * KIN)
+__attribute__((amdgpu_waves_per_eu((KIN == 2 && NSUB >= 8) ? 2 : 3, 8))) void stream_kernel(StreamArgs a) {
+    static_assert(KIN == 1 || (KIN == 2 && GATED), "two reduction groups in the gated kernel only");
+    constexpr int NT = WPB * 64;                      // threads per reduction group
     constexpr int BN = 16 * NSUB;
     constexpr int KC = 32 * KS;
     constexpr int LDS_ROW = KC + 8;                   // +16 B per row against bank conflicts
     constexpr int VPR = KC / 8;                       // 16-byte vectors per token row per chunk
     constexpr int RMAX = (BN * VPR + NT - 1) / NT;    // vectors per thread per chunk
     constexpr bool DEEP = stream_deep<GATED, NSUB>();
-    __shared__ __attribute__((aligned(16))) uint16_t xs[2][BN * LDS_ROW];
+    // the token slabs (two per reduction group), also holding group 1's sums
+    // at the end of an item when KIN = 2
+    constexpr int kSlabs = KIN * 2 * BN * LDS_ROW;
+    constexpr int kSums = KIN == 2 ? NT * NSUB * 8 * 2 : 0;     // in 16-bit units
+    __shared__ __attribute__((aligned(16))) uint16_t xs[kSlabs > kSums ? kSlabs : kSums];
+    auto slab = [&](int grp, int buf) __attribute__((always_inline)) {
+        return xs + (grp * 2 + buf) * (BN * LDS_ROW);
+    };
     __shared__ int tstart[kMaxExperts + 1];
     __shared__ int used_groups;
-    const int tid = threadIdx.x;
-    const int lane = lane_id(), wave = tid / kWave;
+    const int lane = lane_id();
+    // reduction group (uniform over the wave), the wave's place in it and
+    // the thread's
+    const int kg = KIN == 1 ? 0 : __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / NT);
+    const int tid = KIN == 1 ? static_cast<int>(threadIdx.x) : static_cast<int>(threadIdx.x) - kg * NT;
+    const int wave = tid / kWave;
 
     int ntiles, used = 1;
     if (a.offsets) {
@@ -263,12 +286,14 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
     }
     // slices of the reduction dimension: fixed, or chosen from the tiles in
     // use (every workgroup computes the same value)
-    const int splits = a.rule_threshold > 0 ? split_rule(a.M, a.K, ntiles, a.splits, a.rule_threshold) : a.splits;
-    if (a.splits_out && blockIdx.x == 0 && tid == 0) *a.splits_out = splits;
+    // (the rule counts both reduction groups' waves)
+    const int splits =
+        a.rule_threshold > 0 ? split_rule(a.M * KIN, a.K / KIN, ntiles, a.splits, a.rule_threshold) : a.splits;
+    if (a.splits_out && blockIdx.x == 0 && threadIdx.x == 0) *a.splits_out = splits;
     const int ksplit = a.K / splits;
 
     const int i = lane & 15, g = lane >> 4;
-    const int nch = ksplit / KC;
+    const int nch = ksplit / KIN / KC;
     const int nrb = a.M / (16 * WPB);                 // weight-row blocks
 
     // Work items (token tile, reduction slice, row block), row block
@@ -288,7 +313,7 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
             const int split = static_cast<int>(rest % splits);
             const int tile = static_cast<int>(rest / splits);
             const int m0 = rb * (16 * WPB) + wave * 16;
-            const int kbeg = split * ksplit;
+            const int kbeg = split * ksplit + kg * (ksplit / KIN);
             int e = 0, r0, n;
             if (a.offsets) {
                 e = tile_group(tstart, a.groups, tile);
@@ -332,7 +357,7 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
             auto store_xr = [&](int buf, const bf16x8 (&R)[RMAX]) __attribute__((always_inline)) {
 #pragma unroll
                 for (int r = 0; r < RMAX; ++r)
-                    if (xon[r]) *reinterpret_cast<bf16x8*>(&xs[buf][xdst[r]]) = R[r];
+                    if (xon[r]) *reinterpret_cast<bf16x8*>(slab(kg, buf) + xdst[r]) = R[r];
             };
             auto load_x = [&](int c) __attribute__((always_inline)) { load_xr(c, xr); };
             auto store_x = [&](int buf) __attribute__((always_inline)) { store_xr(buf, xr); };
@@ -368,7 +393,7 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
             // one MFMA per read the pins cost it more than the latency they hide
             // (measured).
             auto compute = [&](int buf, const bf16x8 (&A)[KS], const bf16x8 (&B)[KS]) __attribute__((always_inline)) {
-                const uint16_t* xb = xs[buf];
+                const uint16_t* xb = slab(kg, buf);
 #pragma unroll
                 for (int j = 0; j < KS; ++j) {
                     if constexpr (GATED) {
@@ -476,6 +501,32 @@ __global__ __launch_bounds__(WPB * 64) __attribute__((amdgpu_waves_per_eu(3, 8))
             }
             }
 
+            if constexpr (KIN == 2) {
+                // group 1's sums to group 0 through the token slabs (every
+                // wave is past its last LDS read: the loop ends with a
+                // barrier), added after group 0's own; the second barrier
+                // keeps the next item's token staging off the slabs until
+                // they have been read
+                float* const cmb = reinterpret_cast<float*>(xs);
+                const int base = (wave * kWave + lane) * NSUB * 8;
+                if (kg == 1) {
+#pragma unroll
+                    for (int s = 0; s < NSUB; ++s) {
+                        *reinterpret_cast<f32x4*>(cmb + base + 8 * s) = acc_a[s];
+                        *reinterpret_cast<f32x4*>(cmb + base + 8 * s + 4) = acc_b[s];
+                    }
+                }
+                lds_barrier();
+                if (kg == 0) {
+#pragma unroll
+                    for (int s = 0; s < NSUB; ++s) {
+                        acc_a[s] += *reinterpret_cast<const f32x4*>(cmb + base + 8 * s);
+                        acc_b[s] += *reinterpret_cast<const f32x4*>(cmb + base + 8 * s + 4);
+                    }
+                }
+                lds_barrier();
+                if (kg == 1) continue;               // group 0 stores the item
+            }
             // result: lane holds weight rows m0 + 4g + q (q < 4) for token column s*16 + i
             if constexpr (GATED) {
                 if (splits == 1) {
@@ -621,15 +672,15 @@ constexpr int stream_wpb() { return (!GATED && NSUB >= 4) ? 8 : (GATED && NSUB >
 // (occupancy per CU x CUs), asked once per instance on the device current
 // at the first call (every device a process uses is assumed to be the same
 // part; a smaller grid on a larger part is still correct, only less full).
-template <bool GATED, int NSUB, int KS, int WPB, bool PACKED>
+template <bool GATED, int NSUB, int KS, int WPB, bool PACKED, int KIN>
 int64_t stream_resident() {
     static const int64_t v = [] {
         int dev = 0, cus = 0, per_cu = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
             cus = 256;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, stream_kernel<GATED, NSUB, KS, WPB, PACKED>,
-                                                         WPB * 64, 0) != hipSuccess ||
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, stream_kernel<GATED, NSUB, KS, WPB, PACKED, KIN>,
+                                                         WPB * 64 * KIN, 0) != hipSuccess ||
             per_cu < 1)
             per_cu = 1;
         return static_cast<int64_t>(cus) * per_cu;
@@ -639,13 +690,22 @@ int64_t stream_resident() {
 
 // Grid: as many workgroups as there can be work items (max_tiles token
 // tiles x slices x row blocks), at most what the chip keeps resident.
-template <bool GATED, int NSUB, int KS, int WPB, bool PACKED>
-hipError_t launch_stream_w(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
+template <bool GATED, int NSUB, int KS, int WPB, bool PACKED, int KIN>
+hipError_t launch_stream_wk(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
     const int64_t items = max_tiles * a.splits * (a.M / (16 * WPB));
     if (items >= (int64_t{1} << 31)) return hipErrorInvalidValue;
-    int64_t blocks = std::max<int64_t>(1, std::min(items, stream_resident<GATED, NSUB, KS, WPB, PACKED>()));
-    stream_kernel<GATED, NSUB, KS, WPB, PACKED><<<dim3(static_cast<unsigned>(blocks)), dim3(WPB * 64), 0, s>>>(a);
+    int64_t blocks = std::max<int64_t>(1, std::min(items, stream_resident<GATED, NSUB, KS, WPB, PACKED, KIN>()));
+    stream_kernel<GATED, NSUB, KS, WPB, PACKED, KIN>
+        <<<dim3(static_cast<unsigned>(blocks)), dim3(WPB * 64 * KIN), 0, s>>>(a);
     return hipGetLastError();
+}
+
+template <bool GATED, int NSUB, int KS, int WPB, bool PACKED>
+hipError_t launch_stream_w(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
+    if constexpr (GATED) {
+        if (a.kin == 2) return launch_stream_wk<GATED, NSUB, KS, WPB, PACKED, 2>(a, max_tiles, s);
+    }
+    return launch_stream_wk<GATED, NSUB, KS, WPB, PACKED, 1>(a, max_tiles, s);
 }
 
 template <bool GATED, int NSUB, int KS, bool PACKED>
@@ -667,7 +727,7 @@ template <bool GATED, int NSUB, bool PACKED>
 hipError_t launch_stream_n(const StreamArgs& a, int64_t max_tiles, hipStream_t s) {
     // the device may take fewer slices than a.splits; K / a.splits divides
     // every longer slice, so its chunk depth fits them all
-    const int ks = std::min(pick_ks(a.K / a.splits), max_ks<GATED, NSUB>());
+    const int ks = std::min(pick_ks(a.K / a.splits / (a.kin == 2 ? 2 : 1)), max_ks<GATED, NSUB>());
     switch (ks) {
         case 8: return launch_stream_k<GATED, NSUB, 8, PACKED>(a, max_tiles, s);
         case 4: return launch_stream_k<GATED, NSUB, 4, PACKED>(a, max_tiles, s);
@@ -762,10 +822,29 @@ int down_splits(const eat_params_t& p, int32_t T) {
     return split_rule(p.d_model, p.d_ffn, min_tiles(p, T), 8, EAT_SPLIT_WAVES);
 }
 
+// Reduction groups per workgroup of the gated stream kernel: two where the
+// rule would split the reduction across workgroups (few experts, few waves),
+// which halves the slices the projection writes and a reduce adds (none left
+// at one slice); one otherwise.
+#ifndef EAT_UP_KIN
+#define EAT_UP_KIN 1
+#endif
+static int up_groups(int M, int K, int64_t tiles, int64_t threshold) {
+    if (!EAT_UP_KIN || (K / 2) % 64 != 0) return 1;
+    return split_rule(M, K, tiles, EAT_UP_SPLIT_MAX, threshold) >= 2 ? 2 : 1;
+}
+
+static int64_t up_threshold(int32_t T) { return pick_nsub(T) >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES; }
+
+static int up_kin(const eat_params_t& p, int32_t T) {
+    if (p.expert_dtype != EAT_BF16 || use_wide(p, T)) return 1;
+    return up_groups(p.d_ffn, p.d_model, expected_tiles(p, T), up_threshold(T));
+}
+
 int up_splits(const eat_params_t& p, int32_t T) {
     if (p.expert_dtype != EAT_BF16 || use_wide(p, T)) return 1;
-    return split_rule(p.d_ffn, p.d_model, expected_tiles(p, T), EAT_UP_SPLIT_MAX,
-                      pick_nsub(T) >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES);
+    const int kin = up_kin(p, T);
+    return split_rule(p.d_ffn * kin, p.d_model / kin, expected_tiles(p, T), EAT_UP_SPLIT_MAX, up_threshold(T));
 }
 
 // Dense projection (one group of T identity rows): the wide tiles from 384
@@ -835,9 +914,10 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
     // both projections take their slices on the device, from the tiles in use
     const int usplits = up_splits(p, T);
     StreamArgs up{};
+    up.kin = up_kin(p, T);
     up.wa = w1; up.wb = w3; up.src = x; up.gather = tok_idx; up.offsets = offsets;
     up.groups = p.E; up.M = p.d_ffn; up.K = p.d_model; up.splits = usplits;
-    up.rule_threshold = usplits > 1 ? (nsub >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES) : 0;
+    up.rule_threshold = usplits > 1 ? up_threshold(T) : 0;
     up.split_stride = rows_cap * p.d_ffn;
     up.out = gu;
     up.out2 = gu + usplits * up.split_stride;
@@ -869,13 +949,22 @@ hipError_t launch_experts_bf16(const eat_params_t& p, int32_t T, int64_t rows_ca
 // weight rows is too few workgroups for the chip (88 for a 5632-wide expert,
 // 16 for its 2048-row down projection), so both projections split their
 // reduction dimension like a routed call whose tokens all go to one expert.
+static int shared_up_kin(const eat_params_t& p, int32_t T) {
+    if (p.expert_dtype != EAT_BF16 || p.d_shared == 0 || shared_wide(p, T)) return 1;
+    eat_params_t one = p;
+    one.E = 1;
+    one.top_k = 1;
+    return up_groups(p.d_shared, p.d_model, expected_tiles(one, T), up_threshold(T));
+}
+
 int shared_up_splits(const eat_params_t& p, int32_t T) {
     if (p.expert_dtype != EAT_BF16 || p.d_shared == 0 || shared_wide(p, T)) return 1;
     eat_params_t one = p;
     one.E = 1;
     one.top_k = 1;
-    return split_rule(p.d_shared, p.d_model, expected_tiles(one, T), EAT_UP_SPLIT_MAX,
-                      pick_nsub(T) >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES);
+    const int kin = shared_up_kin(p, T);
+    return split_rule(p.d_shared * kin, p.d_model / kin, expected_tiles(one, T), EAT_UP_SPLIT_MAX,
+                      up_threshold(T));
 }
 
 int shared_splits(const eat_params_t& p, int32_t T) {
@@ -899,6 +988,7 @@ hipError_t launch_shared_bf16(const eat_params_t& p, int32_t T, const uint16_t* 
     const int tiles = (T + bn - 1) / bn;
     const int usplits = shared_up_splits(p, T);
     StreamArgs up{};
+    up.kin = shared_up_kin(p, T);
     up.wa = ws1; up.wb = ws3; up.src = x; up.gather = nullptr; up.offsets = nullptr; up.nrows = T;
     up.groups = 1; up.M = p.d_shared; up.K = p.d_model; up.splits = usplits;
     up.split_stride = static_cast<int64_t>(T) * p.d_shared;
