@@ -6,9 +6,9 @@
 // y_t = sum_e g_norm,t,e o_t,e (+ shared expert) (+ a residual row) in fp32
 // (Eq. 7-8 and the weighted fusion of Sec. 3.4).  After a prefill-sized down
 // projection the rows come in bf16 with their sums of squares already taken
-// (from the projection's fp32 accumulators), which halves the bytes this
-// kernel reads.  No atomics: every output element has one writer and a
-// fixed summation order.
+// (from the projection's fp32 accumulators), which halves the bytes read;
+// combine_rows16_kernel gathers those, 8 elements a thread.  No atomics:
+// every output element has one writer and a fixed summation order.
 //
 // mix_norm: between stacked layers, h' = bf16(sum of the mixing GEMM's
 // split partials) and the next layer's input u = bf16(h' / rms(h')), one
@@ -38,7 +38,7 @@ struct CombineArgs {
     const uint64_t* mask;      // [T][words]
     const float* gate;
     const int32_t* inv;
-    const void* yp;            // fp32 [splits][rows_cap][d], or bf16 [rows_cap][d] (ROWS16)
+    const void* yp;            // fp32 [splits][rows_cap][d], or bf16 [rows_cap][d] (combine_rows16_kernel)
     const int32_t* splits_dev; // slices the down projection took (device), or null: `splits`
     const float* ys;           // [T][d] shared output or null
     const uint16_t* res;       // [T][d] bf16 residual rows added to y, or null
@@ -58,8 +58,7 @@ struct CombineArgs {
 constexpr int kBatch = 8;
 constexpr int kMaxSplits = 8;                  // the down projection uses at most 8 slices
 
-// ROWS16: bf16 rows, one slice, sums of squares not taken here.
-template <typename YT, bool ROWS16>
+template <typename YT>
 __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     __shared__ float red[kBatch][kWaves];
     const int t = blockIdx.x, chunk = blockIdx.y;
@@ -73,15 +72,15 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     const uint64_t* mt = a.mask + static_cast<size_t>(t) * a.words;
     // the shared-expert and residual slices do not depend on the routing, so
-    // they are loaded first, from in-bounds stand-ins when absent (slice 0 of
-    // the partials; element 0 for threads past d), and used after the loop
+    // they are loaded first, from in-bounds stand-ins when absent (row 0 of
+    // the partials, at least d floats; element 0 for threads past d), and
+    // used after the loop
     const int jc = on ? j : 0;
     const float* ypf = static_cast<const float*>(a.yp);
-    const uint16_t* yph = static_cast<const uint16_t*>(a.yp);
-    const float4 ysv = *reinterpret_cast<const float4*>(
-        (a.ys ? a.ys + static_cast<size_t>(t) * a.d : reinterpret_cast<const float*>(a.gate)) + 4 * jc);
-    const uint2 rsv =
-        *reinterpret_cast<const uint2*>((a.res ? a.res + static_cast<size_t>(t) * a.d : yph) + 4 * jc);
+    const float4 ysv =
+        *reinterpret_cast<const float4*>((a.ys ? a.ys + static_cast<size_t>(t) * a.d : ypf) + 4 * jc);
+    const uint2 rsv = *reinterpret_cast<const uint2*>(
+        (a.res ? a.res + static_cast<size_t>(t) * a.d : reinterpret_cast<const uint16_t*>(ypf)) + 4 * jc);
 
     int w = 0;
     uint64_t rest = mt[0];
@@ -107,21 +106,13 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
         // each row slice's partials are all loaded at once and added in slice
         // order; the next row's loads are issued before this row is added up
         // (threads past d read the row's first elements and discard them)
-        constexpr int kS = ROWS16 ? 1 : kMaxSplits;
+        constexpr int kS = kMaxSplits;
         float4 q[2][kS];
         auto issue = [&](float4 (&dst)[kS], int row) __attribute__((always_inline)) {
-            if constexpr (ROWS16) {
-                const uint2 v = *reinterpret_cast<const uint2*>(yph + static_cast<int64_t>(row) * a.d + 4 * jc);
-                dst[0] = make_float4(bf16_to_f32(static_cast<uint16_t>(v.x & 0xffffu)),
-                                     bf16_to_f32(static_cast<uint16_t>(v.x >> 16)),
-                                     bf16_to_f32(static_cast<uint16_t>(v.y & 0xffffu)),
-                                     bf16_to_f32(static_cast<uint16_t>(v.y >> 16)));
-            } else {
-                const float* src = ypf + static_cast<int64_t>(row) * a.d + 4 * jc;
+            const float* src = ypf + static_cast<int64_t>(row) * a.d + 4 * jc;
 #pragma unroll
-                for (int sp = 0; sp < kMaxSplits; ++sp)
-                    if (sp < splits) dst[sp] = *reinterpret_cast<const float4*>(src + sp * a.split_stride);
-            }
+            for (int sp = 0; sp < kMaxSplits; ++sp)
+                if (sp < splits) dst[sp] = *reinterpret_cast<const float4*>(src + sp * a.split_stride);
         };
         issue(q[0], rows[0]);
         float ss[kBatch];
@@ -136,36 +127,32 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
                 for (int sp = 1; sp < kS; ++sp)
                     if (sp < splits) { o.x += c[sp].x; o.y += c[sp].y; o.z += c[sp].z; o.w += c[sp].w; }
                 if (on) {
-                    if constexpr (!ROWS16) {
-                        ss[b] = fmaf(o.x, o.x, ss[b]); ss[b] = fmaf(o.y, o.y, ss[b]);
-                        ss[b] = fmaf(o.z, o.z, ss[b]); ss[b] = fmaf(o.w, o.w, ss[b]);
-                    }
+                    ss[b] = fmaf(o.x, o.x, ss[b]); ss[b] = fmaf(o.y, o.y, ss[b]);
+                    ss[b] = fmaf(o.z, o.z, ss[b]); ss[b] = fmaf(o.w, o.w, ss[b]);
                     const float g = gs[b];
                     acc.x = fmaf(g, o.x, acc.x); acc.y = fmaf(g, o.y, acc.y);
                     acc.z = fmaf(g, o.z, acc.z); acc.w = fmaf(g, o.w, acc.w);
                 }
             }
         }
-        if constexpr (!ROWS16) {
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            if (b >= nb) break;
+            const float v = wave_sum(ss[b]);
+            if (lane == 0) red[b][wave] = v;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
 #pragma unroll
             for (int b = 0; b < kBatch; ++b) {
                 if (b >= nb) break;
-                const float v = wave_sum(ss[b]);
-                if (lane == 0) red[b][wave] = v;
-            }
-            __syncthreads();
-            if (threadIdx.x == 0) {
+                float tot = 0.f;
 #pragma unroll
-                for (int b = 0; b < kBatch; ++b) {
-                    if (b >= nb) break;
-                    float tot = 0.f;
-#pragma unroll
-                    for (int q = 0; q < kWaves; ++q) tot += red[b][q];
-                    a.nrm2[static_cast<int64_t>(rows[b]) * a.nchunk + chunk] = tot;
-                }
+                for (int q = 0; q < kWaves; ++q) tot += red[b][q];
+                a.nrm2[static_cast<int64_t>(rows[b]) * a.nchunk + chunk] = tot;
             }
-            __syncthreads();
         }
+        __syncthreads();
         if (nb < kBatch) break;
     }
     if (on) {
@@ -189,6 +176,93 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
             *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.y) + static_cast<size_t>(t) * a.d + 4 * j) = pk;
         }
     }
+}
+
+// After a prefill-sized down projection: the expert rows come in bf16, one
+// slice, their sums of squares already taken (from the projection's fp32
+// accumulators), so this pass only gathers and weights them: one workgroup
+// per (token, 2048-element slice of d), 8 elements a thread (16-byte loads),
+// every row of a batch of the token's experts loaded before the first is
+// added; the same order of additions as combine_kernel.  y is bf16.
+constexpr int kRowVec = 8;
+__global__ __launch_bounds__(kThreads) void combine_rows16_kernel(CombineArgs a) {
+    const int t = blockIdx.x;
+    const int j = blockIdx.y * kThreads + threadIdx.x;     // 8-element group of the row
+    const bool on = kRowVec * j < a.d;
+    const int jc = on ? j : 0;
+    const uint16_t* yph = static_cast<const uint16_t*>(a.yp);
+    const uint64_t* mt = a.mask + static_cast<size_t>(t) * a.words;
+    // shared-expert and residual slices first, from in-bounds stand-ins when
+    // absent (expert row 0: the rows hold at least 2 d elements on this path)
+    const float* ysr = a.ys ? a.ys + static_cast<size_t>(t) * a.d : reinterpret_cast<const float*>(yph);
+    const float4 ys0 = *reinterpret_cast<const float4*>(ysr + kRowVec * jc);
+    const float4 ys1 = *reinterpret_cast<const float4*>(ysr + kRowVec * jc + 4);
+    const uint4 rsv = *reinterpret_cast<const uint4*>((a.res ? a.res + static_cast<size_t>(t) * a.d : yph) +
+                                                      kRowVec * jc);
+    float acc[kRowVec];
+#pragma unroll
+    for (int i = 0; i < kRowVec; ++i) acc[i] = 0.f;
+    auto unpack = [](const uint4& q, float (&v)[kRowVec]) __attribute__((always_inline)) {
+        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[2 * i] = bf16_to_f32(static_cast<uint16_t>(w[i] & 0xffffu));
+            v[2 * i + 1] = bf16_to_f32(static_cast<uint16_t>(w[i] >> 16));
+        }
+    };
+    int w = 0;
+    uint64_t rest = mt[0];
+    for (;;) {
+        int rows[kBatch];
+        float gs[kBatch];
+        int nb = 0;
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            while (rest == 0 && w + 1 < a.words) rest = mt[++w];
+            rows[b] = 0;
+            gs[b] = 0.f;
+            if (rest != 0) {
+                const int e = 64 * w + __builtin_ctzll(rest);
+                rest &= rest - 1;
+                rows[b] = a.inv[static_cast<size_t>(t) * a.E + e];
+                gs[b] = a.gate[static_cast<size_t>(t) * a.E + e];
+                nb = b + 1;
+            }
+        }
+        if (nb == 0) break;
+        // (rows past nb read row 0, unused)
+        uint4 q[kBatch];
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b)
+            q[b] = *reinterpret_cast<const uint4*>(yph + static_cast<int64_t>(rows[b]) * a.d + kRowVec * jc);
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            if (b >= nb) break;
+            float v[kRowVec];
+            unpack(q[b], v);
+            const float g = gs[b];
+#pragma unroll
+            for (int i = 0; i < kRowVec; ++i) acc[i] = fmaf(g, v[i], acc[i]);
+        }
+        if (nb < kBatch) break;
+    }
+    if (!on) return;
+    if (a.ys) {
+        acc[0] += ys0.x; acc[1] += ys0.y; acc[2] += ys0.z; acc[3] += ys0.w;
+        acc[4] += ys1.x; acc[5] += ys1.y; acc[6] += ys1.z; acc[7] += ys1.w;
+    }
+    if (a.res) {
+        float r[kRowVec];
+        unpack(rsv, r);
+#pragma unroll
+        for (int i = 0; i < kRowVec; ++i) acc[i] += r[i];
+    }
+    uint4 pk;
+    pk.x = static_cast<uint32_t>(f32_to_bf16(acc[0])) | (static_cast<uint32_t>(f32_to_bf16(acc[1])) << 16);
+    pk.y = static_cast<uint32_t>(f32_to_bf16(acc[2])) | (static_cast<uint32_t>(f32_to_bf16(acc[3])) << 16);
+    pk.z = static_cast<uint32_t>(f32_to_bf16(acc[4])) | (static_cast<uint32_t>(f32_to_bf16(acc[5])) << 16);
+    pk.w = static_cast<uint32_t>(f32_to_bf16(acc[6])) | (static_cast<uint32_t>(f32_to_bf16(acc[7])) << 16);
+    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(a.y) + static_cast<size_t>(t) * a.d + kRowVec * j) = pk;
 }
 
 // Expert e's account update by one workgroup (every thread of it calls this).
@@ -340,10 +414,14 @@ hipError_t launch_combine(const eat_params_t& p, int32_t T, const uint64_t* mask
     a.mask = mask; a.gate = gate; a.inv = inv; a.yp = yp; a.splits_dev = splits_dev; a.ys = ys; a.res = residual;
     a.y = y; a.nrm2 = nrm2; a.split_stride = split_stride; a.splits = splits; a.T = T; a.E = p.E; a.d = p.d_model;
     a.nchunk = nchunk; a.words = mask_words(p.E);
+    if (rows_bf16) {
+        const int n8 = (p.d_model / kRowVec + kThreads - 1) / kThreads;
+        combine_rows16_kernel<<<dim3(T, n8), kThreads, 0, s>>>(a);
+        return hipGetLastError();
+    }
     const dim3 grid(T, nchunk);
-    if (rows_bf16) combine_kernel<uint16_t, true><<<grid, kThreads, 0, s>>>(a);
-    else if (p.act_dtype == EAT_BF16) combine_kernel<uint16_t, false><<<grid, kThreads, 0, s>>>(a);
-    else combine_kernel<float, false><<<grid, kThreads, 0, s>>>(a);
+    if (p.act_dtype == EAT_BF16) combine_kernel<uint16_t><<<grid, kThreads, 0, s>>>(a);
+    else combine_kernel<float><<<grid, kThreads, 0, s>>>(a);
     return hipGetLastError();
 }
 

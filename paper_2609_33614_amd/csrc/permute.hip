@@ -18,6 +18,9 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 
+// PRE: chunks of kThreads tokens whose mask words are loaded together (1
+// for calls of at most kThreads tokens, where more would only add loads).
+template <int PRE>
 __global__ __launch_bounds__(kThreads) void permute_kernel(
     const uint64_t* __restrict__ mask, int T, int E, int W, int32_t* __restrict__ offsets,
     int32_t* __restrict__ tok_idx, int32_t* __restrict__ inv, int32_t* __restrict__ row_expert,
@@ -30,14 +33,36 @@ __global__ __launch_bounds__(kThreads) void permute_kernel(
     const uint64_t below = (be == 0) ? 0ull : ((~0ull) >> (64 - be));
     const uint64_t bit = 1ull << be;
 
+    // Both passes walk the tokens kPre chunks of kThreads at a time, loading
+    // the chunks' mask words before using any (one memory round trip per
+    // kPre chunks, not per chunk; tokens past T read token 0's word and are
+    // off).
+    constexpr int kPre = PRE;
+    auto load_words = [&](int base0, int word, uint64_t (&mw)[kPre]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < kPre; ++i) {
+            const int t = base0 + i * kThreads + static_cast<int>(threadIdx.x);
+            mw[i] = mask[static_cast<size_t>(t < T ? t : 0) * W + word];
+        }
+    };
+
     // segment start and size
     int before = 0, mine = 0;
-    for (int t = threadIdx.x; t < T; t += kThreads) {
-        const uint64_t* mt = mask + static_cast<size_t>(t) * W;
-        for (int w = 0; w < we; ++w) before += __popcll(mt[w]);
-        const uint64_t m = mt[we];
-        before += __popcll(m & below);
-        mine += (m & bit) ? 1 : 0;
+    for (int base0 = 0; base0 < T; base0 += kPre * kThreads) {
+        uint64_t mw[kPre];
+        load_words(base0, we, mw);
+#pragma unroll
+        for (int i = 0; i < kPre; ++i) {
+            const bool in = base0 + i * kThreads + static_cast<int>(threadIdx.x) < T;
+            before += in ? __popcll(mw[i] & below) : 0;
+            mine += (in && (mw[i] & bit)) ? 1 : 0;
+        }
+        for (int w = 0; w < we; ++w) {        // the whole words of lower experts (E > 64)
+            load_words(base0, w, mw);
+#pragma unroll
+            for (int i = 0; i < kPre; ++i)
+                before += base0 + i * kThreads + static_cast<int>(threadIdx.x) < T ? __popcll(mw[i]) : 0;
+        }
     }
     before = wave_sum(before);
     mine = wave_sum(mine);
@@ -55,26 +80,33 @@ __global__ __launch_bounds__(kThreads) void permute_kernel(
     // ordered scatter of this expert's tokens
     int running = 0;
     const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-    for (int base = 0; base < T; base += kThreads) {
-        const int t = base + threadIdx.x;
-        const bool on = t < T && (mask[static_cast<size_t>(t) * W + we] & bit);
-        const uint64_t b = ballot(on);
-        if (lane == 0) wtot[wave] = __popcll(b);
-        __syncthreads();
-        int pre = 0, all = 0;
+    for (int base0 = 0; base0 < T; base0 += kPre * kThreads) {
+        uint64_t mw[kPre];
+        load_words(base0, we, mw);
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
-            pre += (w < wave) ? wtot[w] : 0;
-            all += wtot[w];
+        for (int i = 0; i < kPre; ++i) {
+            const int base = base0 + i * kThreads;
+            if (base >= T) break;             // uniform
+            const int t = base + threadIdx.x;
+            const bool on = t < T && (mw[i] & bit);
+            const uint64_t b = ballot(on);
+            if (lane == 0) wtot[wave] = __popcll(b);
+            __syncthreads();
+            int pre = 0, all = 0;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) {
+                pre += (w < wave) ? wtot[w] : 0;
+                all += wtot[w];
+            }
+            if (on) {
+                const int row = off + running + pre + __popcll(b & lt);
+                tok_idx[row] = t;
+                row_expert[row] = e;
+                inv[static_cast<size_t>(t) * E + e] = row;
+            }
+            running += all;
+            __syncthreads();
         }
-        if (on) {
-            const int row = off + running + pre + __popcll(b & lt);
-            tok_idx[row] = t;
-            row_expert[row] = e;
-            inv[static_cast<size_t>(t) * E + e] = row;
-        }
-        running += all;
-        __syncthreads();
     }
 }
 
@@ -83,8 +115,12 @@ __global__ __launch_bounds__(kThreads) void permute_kernel(
 hipError_t launch_permute(const eat_params_t& p, int32_t T, const uint64_t* mask, int32_t* offsets,
                           int32_t* tok_idx, int32_t* inv, int32_t* row_expert, int32_t* expert_load,
                           hipStream_t s) {
-    permute_kernel<<<dim3(p.E), dim3(kThreads), 0, s>>>(mask, T, p.E, mask_words(p.E), offsets, tok_idx, inv,
-                                                        row_expert, expert_load);
+    if (T <= kThreads)
+        permute_kernel<1><<<dim3(p.E), dim3(kThreads), 0, s>>>(mask, T, p.E, mask_words(p.E), offsets, tok_idx,
+                                                               inv, row_expert, expert_load);
+    else
+        permute_kernel<16><<<dim3(p.E), dim3(kThreads), 0, s>>>(mask, T, p.E, mask_words(p.E), offsets, tok_idx,
+                                                                inv, row_expert, expert_load);
     return hipGetLastError();
 }
 
