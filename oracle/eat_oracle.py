@@ -63,6 +63,8 @@ class Params:
     cs_mode: int = 0           # 0: C_s used as is in Eq. 1; 1: C_s / sum(C_s)
     shared: bool = False       # always-on shared expert added with weight 1
     round_h: bool = False      # round the experts' hidden activation to bf16 (R27)
+    round_y: bool = False      # round each expert's output row to bf16 before it is weighted into y,
+                               # its norm still taken from the unrounded row (R27: prefill-sized calls)
     expert_scale: Optional[np.ndarray] = None   # OPD per-expert reweighting (Sec. 3.5), or None
 
 
@@ -318,7 +320,8 @@ class LayerOut:
 def layer_outputs(x, weights: dict, r: Routing, prm: Params, tokens: Optional[Sequence[int]] = None) -> LayerOut:
     """Sec. 3.1 / Eq. 7-8: y_t = sum_{e selected} g_norm,t,e Expert_e(x_t),
     plus the always-on shared expert with weight 1 when present.  Only the
-    rows in ``tokens`` are computed (all by default)."""
+    rows in ``tokens`` are computed (all by default).  With ``round_y`` each
+    expert's output row enters y rounded to bf16 (its norm does not)."""
     T, E = r.p.shape
     toks = list(range(T)) if tokens is None else sorted(set(int(t) for t in tokens))
     xw = widen(x)
@@ -332,7 +335,7 @@ def layer_outputs(x, weights: dict, r: Routing, prm: Params, tokens: Optional[Se
         o = swiglu(xw[rows], weights["w1"][e], weights["w3"][e], weights["w2"][e], prm.round_h)
         for j, t in enumerate(rows):
             norms[t, e] = math.sqrt(float(np.dot(o[j], o[j])))
-            y[t] += r.g_norm[t, e] * o[j]
+            y[t] += r.g_norm[t, e] * (round_bf16(o[j]) if prm.round_y else o[j])
     if prm.shared and "ws1" in weights:
         o = swiglu(xw[toks], weights["ws1"], weights["ws3"], weights["ws2"], prm.round_h)
         for j, t in enumerate(toks):

@@ -231,6 +231,14 @@ class CachedWeights(dict):
                 self[k] = O.widen(w[k])
 
 
+def rows_bf16(T: int, K: int, E: int, d: int, F: int) -> bool:
+    """Whether a bf16 layer call of T tokens takes the library's prefill-sized
+    path, whose down projection stores the expert rows in bf16 once their
+    norms are taken (reading R27): T K >= 256 E rows, with the wide tiles'
+    shapes (F a multiple of 128, d of 256)."""
+    return T * K >= 256 * E and F % 128 == 0 and d % 256 == 0
+
+
 def stack_follow(x, layers, mixes, accs, prms, pick, eps: float = 1e-6) -> O.StackOut:
     """The oracle's stacked-layer step, composed here from its pinned parts
     exactly as ``O.stack_step`` composes them (u = bf16(RMSNorm(h)),

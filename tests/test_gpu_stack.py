@@ -3,7 +3,8 @@ oracle: per-layer selection masks and router probabilities, the final
 hidden rows and every layer's accounts, at every step.
 
 The oracle rounds the experts' hidden activation to bf16 here as the GPU
-stores it (reading R27, ``round_h``).  What remains is that each side rounds
+stores it (reading R27, ``round_h``), and at prefill sizes each expert's
+output row too (``round_y``).  What remains is that each side rounds
 r, h and u to bf16 from its own value (fp32 on the GPU, fp64 in the
 oracle), so an element near a rounding boundary can differ by one bf16 step
 and reach the next router.  The borderline band of a token at a layer is
@@ -69,6 +70,7 @@ def _build(mode, n_layers, d, E, F, B, seed=None, zero_w2=False, caps=None):
     for l in range(n_layers):
         prm = PT.oracle_params(shape, L.MODES[mode], K=caps[l])
         prm.round_h = True
+        prm.round_y = PT.rows_bf16(B, caps[l], E, d, F)
         prms.append(prm)
     return shape, w_host, mixes, stack, prms
 
@@ -157,6 +159,15 @@ def test_stack_parity_layer_shape(mode):
     # the 16-layer workload's layer shape (d=2048, 64 experts of width 1024,
     # K=8) at its decode batch of 64, two layers, six steps (accounts carried)
     _run(mode, n_layers=2, d=2048, E=64, F=1024, B=64, steps=6, name="d2048")
+
+
+@pytest.mark.parametrize("mode", ["eat", "topk"])
+def test_stack_parity_prefill_sized(mode):
+    # 640 tokens: every layer's experts take the wide tiles (T K >= 256 E) and
+    # their bf16 rows go through the bf16-row combine with the residual, the
+    # mixing GEMM takes the wide tiles too (T >= 384), and the permutation
+    # walks several chunks of tokens; two layers, two steps
+    _run(mode, n_layers=2, d=256, E=16, F=128, B=640, steps=2, name="prefill-sized")
 
 
 @pytest.mark.parametrize("d", [192, 384])

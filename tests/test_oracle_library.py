@@ -72,6 +72,38 @@ def test_swiglu_matches_torch_silu_reference():
     assert np.abs(got_r - ref.numpy()).max() > 1e-4            # the rounding is really applied
 
 
+def test_layer_outputs_round_y_rounds_rows_not_norms():
+    """R27 at prefill sizes: each expert's output row enters y rounded to
+    bf16 (torch's conversion), its norm stays that of the unrounded row."""
+    rng = np.random.default_rng(31)
+    T, d, F, E = 6, 16, 24, 3
+    w = {"w1": rng.standard_normal((E, F, d)), "w3": rng.standard_normal((E, F, d)),
+         "w2": rng.standard_normal((E, d, F))}
+    x = rng.standard_normal((T, d))
+    masks = [0b011, 0b110, 0b101, 0b001, 0b111, 0b010]
+    p = rng.random((T, E))
+    g = np.zeros((T, E))
+    for t, m in enumerate(masks):
+        sel = [e for e in range(E) if (m >> e) & 1]
+        g[t, sel] = p[t, sel] / p[t, sel].sum()
+    r = O.Routing(p=p, masks=masks, k=np.array([bin(m).count("1") for m in masks]), g_norm=g)
+    plain = O.layer_outputs(x, w, r, O.Params())
+    got = O.layer_outputs(x, w, r, O.Params(round_y=True))
+    X = torch.from_numpy(x)
+    ref = np.zeros((T, d))
+    for e in range(E):
+        o = torch.nn.functional.linear(
+            torch.nn.functional.silu(torch.nn.functional.linear(X, torch.from_numpy(w["w1"][e])))
+            * torch.nn.functional.linear(X, torch.from_numpy(w["w3"][e])), torch.from_numpy(w["w2"][e]))
+        ob = o.float().to(torch.bfloat16).double().numpy()
+        for t, m in enumerate(masks):
+            if (m >> e) & 1:
+                ref[t] += g[t, e] * ob[t]
+    np.testing.assert_allclose(got.y, ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_array_equal(got.norms, plain.norms)
+    assert np.abs(got.y - plain.y).max() > 1e-4                 # the rounding is really applied
+
+
 def test_widen_bf16_matches_torch():
     rng = np.random.default_rng(4)
     a = (rng.standard_normal(1000) * 10).astype(np.float32)
