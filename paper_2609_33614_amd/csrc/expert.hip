@@ -164,6 +164,8 @@ struct StreamArgs {
     float* out2;               // gated: fp32 U partials [split][rows][M]
     uint16_t* h;               // gated: bf16 H [rows][M] (written here when one slice is taken)
     int kin;                   // gated: reduction groups per workgroup (2, or 1 when 0 or 1)
+    int narrow;                // host only: plain kernels keep 4-wave workgroups (more,
+                               // smaller work items) instead of 8
 };
 
 __device__ __forceinline__ bf16x8 ld16(const uint16_t* p) {
@@ -688,6 +690,18 @@ int64_t stream_resident() {
     return v;
 }
 
+// Compute units of the device current at the first call.
+static int chip_cus() {
+    static const int v = [] {
+        int dev = 0, cus = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+            cus = 256;
+        return cus;
+    }();
+    return v;
+}
+
 // Grid: as many workgroups as there can be work items (max_tiles token
 // tiles x slices x row blocks), at most what the chip keeps resident.
 template <bool GATED, int NSUB, int KS, int WPB, bool PACKED, int KIN>
@@ -713,7 +727,7 @@ hipError_t launch_stream_k(const StreamArgs& a, int64_t max_tiles, hipStream_t s
     if constexpr (KS > max_ks<GATED, NSUB>()) {
         return hipErrorInvalidValue;
     } else if constexpr (stream_wpb<GATED, NSUB>() == 8) {
-        if (a.M % 128 == 0) return launch_stream_w<GATED, NSUB, KS, 8, PACKED>(a, max_tiles, s);
+        if (a.M % 128 == 0 && !a.narrow) return launch_stream_w<GATED, NSUB, KS, 8, PACKED>(a, max_tiles, s);
         return launch_stream_w<GATED, NSUB, KS, 4, PACKED>(a, max_tiles, s);
     } else if constexpr (stream_wpb<GATED, NSUB>() == 2) {
         if (a.M % 32 == 0) return launch_stream_w<GATED, NSUB, KS, 2, PACKED>(a, max_tiles, s);
@@ -871,6 +885,9 @@ hipError_t launch_dense_bf16(const uint16_t* src, int32_t T, const uint16_t* w, 
     StreamArgs a{};
     a.wa = w; a.src = src; a.nrows = T; a.groups = 1; a.M = M; a.K = K; a.splits = splits;
     a.split_stride = split_stride; a.out = out;
+    // 8-wave items that would not reach every CU (the 2048-wide mixing GEMM
+    // of a 64-token decode: 128 items) take 4-wave ones instead
+    a.narrow = static_cast<int64_t>(tiles) * splits * (M / 128) < chip_cus();
     return launch_stream<false>(a, nsub, tiles, false, s);
 }
 
