@@ -135,11 +135,18 @@ hipError_t launch_f32_pair(F32Args a, int64_t rows_cap, hipStream_t s,
 #define EAT_UP_SPLIT_MAX 4
 #endif
 
+// The gated projection (gated = true) doubles only while the doubled count
+// stays within the threshold, never past it: its slices cost fp32 G and U
+// partials and a reduce launch, and a split that overshoots paid less than
+// it cost (the 128-expert layer's EAT decode, ~15 experts of 64-token tiles
+// around the 1024-wave threshold: +7% with it).  The plain projection keeps
+// doubling until it reaches the threshold: the Mixtral-shaped down projection
+// took 5% longer under the gated form.
 __host__ __device__ inline int split_rule(int64_t rows_m, int kdim, int64_t tiles, int max_splits,
-                                          int64_t threshold) {
+                                          int64_t threshold, bool gated) {
     const int64_t waves = (rows_m / 16) * tiles;
     int s = 1;
-    while (s < max_splits && kdim % (64 * 2 * s) == 0 && waves * s < threshold &&
+    while (s < max_splits && kdim % (64 * 2 * s) == 0 && (gated ? waves * s * 2 <= threshold : waves * s < threshold) &&
            kdim / (2 * s) >= (waves * s < 1024 ? 128 : EAT_SPLIT_MIN_K))
         s *= 2;
     return s;
@@ -290,7 +297,7 @@ __attribute__((amdgpu_waves_per_eu((KIN == 2 && NSUB >= 8) ? 2 : 3, 8))) void st
     // use (every workgroup computes the same value)
     // (the rule counts both reduction groups' waves)
     const int splits =
-        a.rule_threshold > 0 ? split_rule(a.M * KIN, a.K / KIN, ntiles, a.splits, a.rule_threshold) : a.splits;
+        a.rule_threshold > 0 ? split_rule(a.M * KIN, a.K / KIN, ntiles, a.splits, a.rule_threshold, GATED) : a.splits;
     if (a.splits_out && blockIdx.x == 0 && threadIdx.x == 0) *a.splits_out = splits;
     const int ksplit = a.K / splits;
 
@@ -833,7 +840,7 @@ int norm_parts(const eat_params_t& p, int32_t T) {
 
 int down_splits(const eat_params_t& p, int32_t T) {
     if (p.expert_dtype != EAT_BF16 || use_wide(p, T)) return 1;
-    return split_rule(p.d_model, p.d_ffn, min_tiles(p, T), 8, EAT_SPLIT_WAVES);
+    return split_rule(p.d_model, p.d_ffn, min_tiles(p, T), 8, EAT_SPLIT_WAVES, false);
 }
 
 // Reduction groups per workgroup of the gated stream kernel: two where the
@@ -845,7 +852,7 @@ int down_splits(const eat_params_t& p, int32_t T) {
 #endif
 static int up_groups(int M, int K, int64_t tiles, int64_t threshold) {
     if (!EAT_UP_KIN || (K / 2) % 64 != 0) return 1;
-    return split_rule(M, K, tiles, EAT_UP_SPLIT_MAX, threshold) >= 2 ? 2 : 1;
+    return split_rule(M, K, tiles, EAT_UP_SPLIT_MAX, threshold, true) >= 2 ? 2 : 1;
 }
 
 static int64_t up_threshold(int32_t T) { return pick_nsub(T) >= 8 ? EAT_UP_SPLIT_WAVES_T128 : EAT_UP_SPLIT_WAVES; }
@@ -858,7 +865,7 @@ static int up_kin(const eat_params_t& p, int32_t T) {
 int up_splits(const eat_params_t& p, int32_t T) {
     if (p.expert_dtype != EAT_BF16 || use_wide(p, T)) return 1;
     const int kin = up_kin(p, T);
-    return split_rule(p.d_ffn * kin, p.d_model / kin, expected_tiles(p, T), EAT_UP_SPLIT_MAX, up_threshold(T));
+    return split_rule(p.d_ffn * kin, p.d_model / kin, expected_tiles(p, T), EAT_UP_SPLIT_MAX, up_threshold(T), true);
 }
 
 // Dense projection (one group of T identity rows): the wide tiles from 384
@@ -981,7 +988,7 @@ int shared_up_splits(const eat_params_t& p, int32_t T) {
     one.top_k = 1;
     const int kin = shared_up_kin(p, T);
     return split_rule(p.d_shared * kin, p.d_model / kin, expected_tiles(one, T), EAT_UP_SPLIT_MAX,
-                      up_threshold(T));
+                      up_threshold(T), true);
 }
 
 int shared_splits(const eat_params_t& p, int32_t T) {
